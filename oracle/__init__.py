@@ -1,0 +1,10 @@
+"""CPU oracle for batched VLA rollout inference -- test infrastructure only.
+
+Imported by the test-suite, the smoke check and the benchmark's CPU-baseline
+leg; never by the library.  See ``vla_oracle`` for what it computes.
+"""
+from .vla_oracle import (MODES, Weights, action_logits, apply_rope, as_weights, bf16_round,  # noqa: F401
+                         causal_attention, decoder_layer, forward_rows, prefill_logits,
+                         prefix_embeddings, rms_norm, rollout, rollout_env, rope_angles,
+                         sample_bin, silu, teacher_forced, teacher_forced_env, to_f64,
+                         token_stats)

@@ -1,0 +1,287 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself:
+library routines (torch's bf16 cast, RMSNorm, scaled-dot-product attention,
+HuggingFace's Llama decoder), closed forms, invariants of the mathematics and
+brute force on tiny inputs.  Every function of the oracle is reached by at
+least one pin whose failure a plausible slip (dropped term, wrong sign or
+index, transposed operand) would trigger.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import vla_oracle as vo
+from paper_2505_18719_amd.inputs import TINY, gumbel_noise, make_inputs, make_weights
+
+# A very small decoder for brute-force and library pins: 2 layers, d 64,
+# 4 heads of 16, FFN 96, vocabulary 600 of which the last 256 are action bins.
+PIN = TINY.replace(name="pin", d_model=64, n_heads=4, d_ffn=96, vocab=600, n_visual=8,
+                   batch=3, prompt_min=3, prompt_max=6)
+
+
+@pytest.fixture(scope="module")
+def pin_setup():
+    w = make_weights(PIN, seed=3, gain_jitter=True)
+    inp = make_inputs(PIN, seed=5)
+    return w, inp
+
+
+# ---------------------------------------------------------------- bf16 rounding
+def test_bf16_round_matches_torch_cast():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.normal(size=4000) * 10.0 ** rng.integers(-8, 8, 4000),
+                        [0.0, -0.0, 1.0, 65504.0, 3.0e38]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(vo.bf16_round(x), ref)
+
+
+def test_bf16_round_ties_to_even():
+    # bf16 keeps 7 explicit mantissa bits: the spacing above 1 is 2^-7.
+    assert vo.bf16_round(np.array([1 + 2.0 ** -8]))[0] == 1.0
+    assert vo.bf16_round(np.array([1 + 3 * 2.0 ** -8]))[0] == 1 + 2.0 ** -6
+    assert vo.bf16_round(np.array([1 + 2.0 ** -8 + 2.0 ** -20]))[0] == 1 + 2.0 ** -7
+
+
+# ---------------------------------------------------------------- RMSNorm
+def test_rms_norm_unit_rms_and_scale_invariance():
+    rng = np.random.default_rng(1)
+    x = rng.normal(size=(5, 64)) * 3
+    y = vo.rms_norm(x, np.ones(64), 1e-6)
+    ms = np.mean(x * x, axis=-1)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, axis=-1)), np.sqrt(ms / (ms + 1e-6)), rtol=1e-12)
+    np.testing.assert_allclose(vo.rms_norm(7.5 * x, np.ones(64), 0.0), vo.rms_norm(x, np.ones(64), 0.0),
+                               rtol=1e-12)
+
+
+def test_rms_norm_matches_torch_library():
+    rng = np.random.default_rng(2)
+    x, g = rng.normal(size=(7, 96)), 1 + 0.1 * rng.normal(size=96)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps=1e-6)
+    np.testing.assert_allclose(vo.rms_norm(x, g, 1e-6), ref.numpy(), rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- RoPE
+def test_rope_preserves_norm_and_position_zero_is_identity():
+    rng = np.random.default_rng(3)
+    x = rng.normal(size=(9, 3, 32))
+    pos = np.arange(9) * 37
+    y = vo.apply_rope(x, pos, 1e4)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-12)
+    np.testing.assert_allclose(vo.apply_rope(x, np.zeros(9), 1e4), x, rtol=0, atol=0)
+
+
+def test_rope_equals_complex_rotation():
+    # Pair (x_i, x_{i+hd/2}) as the complex number x_i + i*x_{i+hd/2}, rotated
+    # by exp(i * pos * base^(-2i/hd)).
+    rng = np.random.default_rng(4)
+    hd, pos = 16, np.array([0, 1, 5, 300])
+    x = rng.normal(size=(4, 2, hd))
+    c = x[..., : hd // 2] + 1j * x[..., hd // 2:]
+    freq = np.array([10000.0 ** (-2 * i / hd) for i in range(hd // 2)])
+    rot = c * np.exp(1j * pos[:, None, None] * freq[None, None, :])
+    ref = np.concatenate([rot.real, rot.imag], axis=-1)
+    np.testing.assert_allclose(vo.apply_rope(x, pos, 1e4), ref, rtol=1e-12, atol=1e-12)
+    # First pair at position 1 is rotated by exactly one radian.
+    e = np.zeros((1, 1, hd)); e[0, 0, 0] = 1.0
+    y = vo.apply_rope(e, np.array([1]), 1e4)
+    assert y[0, 0, 0] == pytest.approx(math.cos(1.0)) and y[0, 0, hd // 2] == pytest.approx(math.sin(1.0))
+
+
+def test_rope_scores_depend_only_on_relative_position():
+    rng = np.random.default_rng(5)
+    q, k = rng.normal(size=(1, 1, 32)), rng.normal(size=(1, 1, 32))
+    def score(m, n):
+        return float(np.sum(vo.apply_rope(q, np.array([m]), 1e4) * vo.apply_rope(k, np.array([n]), 1e4)))
+    for m, n, s in [(7, 3, 100), (40, 40, 11), (2, 250, 17)]:
+        assert score(m, n) == pytest.approx(score(m + s, n + s), rel=1e-10, abs=1e-10)
+    assert abs(score(10, 3) - score(3, 10)) > 1e-6   # but not symmetric in (m, n)
+
+
+# ---------------------------------------------------------------- attention
+def test_attention_matches_torch_sdpa_and_rows_sum_to_one():
+    rng = np.random.default_rng(6)
+    L, H, hd = 11, 3, 16
+    q, k, v = (rng.normal(size=(L, H, hd)) for _ in range(3))
+    o, p = vo.causal_attention(q, k, v, np.arange(L), np.arange(L), return_probs=True)
+    t = lambda a: torch.from_numpy(np.transpose(a, (1, 0, 2)))[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), is_causal=True)
+    np.testing.assert_allclose(o, np.transpose(ref[0].numpy(), (1, 0, 2)), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(p.sum(-1), 1.0, rtol=0, atol=1e-14)
+    assert np.all(p[:, np.arange(L)[:, None] < np.arange(L)[None, :]] == 0)
+    np.testing.assert_allclose(o[0], v[0], rtol=1e-14)          # first query sees only key 0
+
+
+def test_attention_with_cached_keys_equals_slice_of_full():
+    rng = np.random.default_rng(7)
+    L, H, hd = 9, 2, 8
+    q, k, v = (rng.normal(size=(L, H, hd)) for _ in range(3))
+    full = vo.causal_attention(q, k, v, np.arange(L), np.arange(L))
+    tail = vo.causal_attention(q[6:], k, v, np.arange(6, L), np.arange(L))
+    np.testing.assert_allclose(tail, full[6:], rtol=1e-13, atol=1e-14)
+
+
+# ---------------------------------------------------------------- whole decoder vs a library
+def _hf_model(cfg, w):
+    transformers = pytest.importorskip("transformers")
+    hc = transformers.LlamaConfig(
+        vocab_size=cfg.vocab, hidden_size=cfg.d_model, intermediate_size=cfg.d_ffn,
+        num_hidden_layers=cfg.n_layers, num_attention_heads=cfg.n_heads,
+        num_key_value_heads=cfg.n_heads, rms_norm_eps=cfg.rms_eps, rope_theta=cfg.rope_base,
+        max_position_embeddings=512, attention_bias=False, mlp_bias=False, tie_word_embeddings=False)
+    hc._attn_implementation = "eager"
+    m = transformers.LlamaForCausalLM(hc).double().eval()
+    sd = {"model.embed_tokens.weight": w["embed"], "lm_head.weight": w["lm_head"],
+          "model.norm.weight": w["final_norm"]}
+    names = {"attn_norm": "input_layernorm", "mlp_norm": "post_attention_layernorm",
+             "wq": "self_attn.q_proj", "wk": "self_attn.k_proj", "wv": "self_attn.v_proj",
+             "wo": "self_attn.o_proj", "wgate": "mlp.gate_proj", "wup": "mlp.up_proj",
+             "wdown": "mlp.down_proj"}
+    for i, lw in enumerate(w["layers"]):
+        for k, n in names.items():
+            sd[f"model.layers.{i}.{n}.weight"] = lw[k]
+    m.load_state_dict({k: v.double() for k, v in sd.items()}, strict=True)
+    inv = m.model.rotary_emb.inv_freq.double()
+    ref = torch.tensor([cfg.rope_base ** (-2 * i / cfg.head_dim) for i in range(cfg.head_dim // 2)],
+                       dtype=torch.float64)
+    torch.testing.assert_close(inv, ref, rtol=1e-6, atol=0)   # library uses the same RoPE frequencies
+    return m
+
+
+def test_decoder_matches_huggingface_llama(pin_setup):
+    """The composed decoder equals transformers' LlamaForCausalLM on the same
+    weights (its RMSNorm and RoPE run in fp32, hence the 1e-5 tolerance)."""
+    w, inp = pin_setup
+    m = _hf_model(PIN, w)
+    got = oracle.prefill_logits(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, mode="ideal")
+    a0 = PIN.action_begin
+    for b in range(inp.batch):
+        x0 = oracle.prefix_embeddings(PIN, vo.as_weights(w, PIN), inp.vis[b], inp.env_prompt(b))
+        with torch.no_grad():
+            ref = m(inputs_embeds=torch.from_numpy(x0)[None]).logits[0, -1, a0:].numpy()
+        np.testing.assert_allclose(got[b], ref, rtol=0, atol=2e-5 * np.abs(ref).max())
+
+
+def test_prompt_ids_equal_their_embedding_rows(pin_setup):
+    w, inp = pin_setup
+    W = vo.as_weights(w, PIN)
+    ids = inp.env_prompt(0)
+    vis_as_tokens = torch.cat([inp.vis[0], w["embed"][torch.as_tensor(ids[:2].astype(np.int64))]])
+    a = oracle.forward_rows(PIN, W, oracle.prefix_embeddings(PIN, W, vis_as_tokens, ids[2:]))
+    b = oracle.forward_rows(PIN, W, oracle.prefix_embeddings(PIN, W, inp.vis[0], ids))
+    np.testing.assert_array_equal(a, b)
+
+
+def test_zero_blocks_reduce_to_action_head_gemv():
+    cfg = PIN.replace(batch=2)
+    w = make_weights(cfg, seed=9)
+    for lw in w["layers"]:
+        lw["wo"].zero_(); lw["wdown"].zero_()
+    inp = make_inputs(cfg, seed=9)
+    z = oracle.prefill_logits(cfg, w, inp.vis, inp.prompt_ids, inp.prompt_lens, mode="ideal")
+    for b in range(2):
+        x_last = inp.vis[b, -1].double().numpy() if inp.prompt_lens[b] == 0 else \
+            w["embed"][int(inp.env_prompt(b)[-1])].double().numpy()
+        u = x_last / np.sqrt(np.mean(x_last ** 2) + cfg.rms_eps)
+        ref = w["lm_head"][cfg.action_begin:].double().numpy() @ u
+        np.testing.assert_allclose(z[b], ref, rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- KV cache and batching
+@pytest.mark.parametrize("mode", ["ideal", "bf16"])
+def test_kv_cached_decode_equals_full_forward(pin_setup, mode):
+    w, inp = pin_setup
+    r = oracle.rollout(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, inp.gumbel, 1.5, mode=mode)
+    tf = oracle.teacher_forced(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, r["tokens"], 1.5, mode=mode)
+    np.testing.assert_allclose(r["logits"], tf["logits"], rtol=0, atol=1e-11)
+    # PPO ratio of Eq. 2 is exactly 1 at theta = theta_old.
+    np.testing.assert_allclose(np.exp(tf["logp_sum"] - r["logp_sum"]), 1.0, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(tf["entropy"], r["entropy"], rtol=0, atol=1e-11)
+
+
+def test_environment_alone_equals_environment_in_ragged_batch(pin_setup):
+    w, inp = pin_setup
+    full = oracle.rollout(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, inp.gumbel, 1.0)
+    b = 1
+    one = oracle.rollout(PIN, w, inp.vis[b:b + 1], inp.env_prompt(b), inp.prompt_lens[b:b + 1],
+                         inp.gumbel[b:b + 1], 1.0)
+    np.testing.assert_array_equal(one["tokens"][0], full["tokens"][b])
+    np.testing.assert_array_equal(one["logits"][0], full["logits"][b])
+
+
+def test_contract_rounding_is_small_but_present(pin_setup):
+    w, inp = pin_setup
+    a = oracle.prefill_logits(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, mode="ideal")
+    b = oracle.prefill_logits(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, mode="bf16")
+    d = np.abs(a - b).max()
+    assert 1e-6 < d < 3e-2
+
+
+# ---------------------------------------------------------------- sampler and Eq. 1
+def test_sampler_closed_forms():
+    A = 256
+    z = np.zeros(A)
+    k, lp, ent, _ = vo.sample_bin(z, np.zeros(A), 1.5)
+    assert k == 0                                   # exact tie -> lowest index
+    assert lp == pytest.approx(-math.log(A), abs=1e-12) and ent == pytest.approx(math.log(A), abs=1e-12)
+    rng = np.random.default_rng(8)
+    z = rng.normal(size=A)
+    assert vo.sample_bin(z, np.zeros(A), 1.0)[0] == int(np.argmax(z))     # g = 0 -> argmax
+    g = np.zeros(A); g[17] = 100.0
+    assert vo.sample_bin(z, g, 1.5)[0] == 17
+    lps = np.array([vo.token_stats(z, j, 1.5)[0] for j in range(A)])
+    assert np.exp(lps).sum() == pytest.approx(1.0, abs=1e-12)
+    # log-probabilities are those of softmax(z / T): ratios follow exp((z_i - z_j)/T)
+    assert lps[3] - lps[9] == pytest.approx((z[3] - z[9]) / 1.5, abs=1e-12)
+    # entropy falls as temperature falls and tends to 0 for T -> 0
+    assert vo.token_stats(z, 0, 0.5)[1] < vo.token_stats(z, 0, 1.5)[1]
+    assert vo.token_stats(z, 0, 1e-3)[1] < 1e-6
+
+
+def test_gumbel_max_frequencies_follow_softmax():
+    """Chi-square test: Gumbel-max with the generator's noise draws bins with
+    probability softmax(z / T)."""
+    scipy_stats = pytest.importorskip("scipy.stats")
+    A, T, n = 256, 1.5, 14000 * 7
+    rng = np.random.default_rng(10)
+    z = rng.normal(size=A) * 1.3
+    g = gumbel_noise(PIN, 14000, seed=11).reshape(n, A)
+    counts = np.bincount([vo.sample_bin(z, g[i], T)[0] for i in range(n)], minlength=A)
+    p = np.exp(z / T - np.max(z / T)); p /= p.sum()
+    exp = n * p
+    keep = exp >= 5
+    obs, ex = counts[keep], exp[keep]
+    if not keep.all():                                  # pool the rare bins into one cell
+        obs, ex = np.append(obs, counts[~keep].sum()), np.append(ex, exp[~keep].sum())
+    assert scipy_stats.chisquare(obs, ex).pvalue > 1e-4
+
+
+def test_eq1_joint_distribution_normalises_by_enumeration():
+    """With 2 action bins and 7 tokens, the exp of Eq. 1's sum of token
+    log-probs over all 2^7 action sequences must add to 1: the token
+    log-probs are proper auto-regressive conditionals."""
+    cfg = PIN.replace(action_bins=2, batch=1)
+    w = make_weights(cfg, seed=12)
+    inp = make_inputs(cfg, seed=12)
+    W = vo.as_weights(w, cfg)
+    total = 0.0
+    for code in range(2 ** cfg.n_actions):
+        acts = [cfg.action_begin + ((code >> i) & 1) for i in range(cfg.n_actions)]
+        r = vo.teacher_forced_env(cfg, W, inp.vis[0], inp.env_prompt(0), acts, 1.5, "ideal")
+        total += math.exp(r["logp"].sum())
+    assert total == pytest.approx(1.0, abs=1e-12)
+
+
+def test_rollout_outputs_are_action_tokens_and_consistent(pin_setup):
+    w, inp = pin_setup
+    r = oracle.rollout(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, inp.gumbel, 1.5)
+    assert r["tokens"].shape == (inp.batch, PIN.n_actions)
+    assert np.all((r["tokens"] >= PIN.action_begin) & (r["tokens"] < PIN.vocab))
+    np.testing.assert_allclose(r["logp_sum"], r["logp"].sum(1), rtol=1e-14)
+    assert np.all(r["logp"] < 0) and np.all(r["entropy"] > 0) and np.all(r["margin"] >= 0)
+    # each token is the Gumbel-max choice of the logits at its step
+    for b in range(inp.batch):
+        for i in range(PIN.n_actions):
+            s = r["logits"][b, i] / 1.5 + inp.gumbel[b, i]
+            assert r["tokens"][b, i] - PIN.action_begin == int(np.argmax(s))
