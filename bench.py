@@ -1,0 +1,226 @@
+"""Throughput of batched VLA rollout inference on one MI355X.
+
+A step is one environment step of VLA-RL's rollout phase for a batch of
+environments: prefill of [256 visual embeddings ; prompt] through the
+OpenVLA-7B-shaped decoder, then the KV-cached decode of the 7 action tokens
+with Gumbel-max sampling over the 256 action bins and per-token log-probs.
+Inputs are synthetic and seeded (random-init bf16 weights, N(0,1) visual
+embeddings, uniform prompt ids, ragged prompt lengths), resident in HBM
+before the timed region.  The teacher-forced log-prob pass is timed in the
+same run and reported beside the step.
+
+Prints ONE JSON line.  `roofline` is the prefill GEMM (the dominant kernel),
+measured with HIP events on the launch stream during the timed steps;
+`roofline_decode` the decode GEMM, measured on a separate profiled decode.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(cfg, w, inp, layers, T):
+    """The oracle on the host cores: one environment (the shortest prefix of
+    the batch), prefill + 7-token KV-cached decode + log-probs over the first
+    `layers` decoder layers, scaled to all layers."""
+    import oracle
+    from paper_2505_18719_amd import inputs as I
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 0) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    b = int(np.argmin(inp.prompt_lens))
+    sub = cfg.replace(n_layers=layers)
+    wc = {k: w[k].cpu() for k in ("embed", "lm_head", "final_norm")}
+    wc["layers"] = [{k: t.cpu() for k, t in w["layers"][l].items()} for l in range(layers)]
+    W = oracle.as_weights(wc, sub, cache_layers=False)
+    t0 = time.perf_counter()
+    oracle.rollout(sub, W, inp.vis[b:b + 1].cpu(), inp.env_prompt(b), inp.prompt_lens[b:b + 1],
+                   inp.gumbel[b:b + 1], T, mode="bf16")
+    dt = time.perf_counter() - t0
+    t_env = dt * cfg.n_layers / layers
+    return {"value": 1.0 / t_env, "unit": "actions/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"1 environment (prefix {int(inp.prefix_lens[b])} tokens), prefill + 7-token decode + "
+                      f"log-probs over {layers} of {cfg.n_layers} layers in {dt:.1f} s, scaled x{cfg.n_layers / layers:g}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="openvla7b_b64_ragged")
+    ap.add_argument("--temperature", type=float, default=1.5)
+    ap.add_argument("--cpu-layers", type=int, default=8, help="decoder layers in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-teacher-forced", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2505_18719_amd import inputs as I
+    from paper_2505_18719_amd.vla import VlaModel
+
+    cfg = I.PRESETS[args.config]
+    B, T = cfg.batch, args.temperature
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    log(f"[bench] {cfg.name}: building weights and inputs")
+    w = I.make_weights(cfg, seed=0, device=dev)
+    model = VlaModel(cfg, w, max_batch=B, device=dev)
+    n_sets = max(1, min(args.steps + args.warmup, 4))
+    sets = []
+    for k in range(n_sets):
+        inp = I.make_inputs(cfg, seed=0, step=k, device=dev)
+        sets.append((inp, torch.from_numpy(inp.prompt_ids).to(dev), torch.from_numpy(inp.gumbel).to(dev)))
+    logits = torch.empty(B, cfg.action_bins, dtype=torch.float32, device=dev)
+    out = {"tokens": torch.empty(B, cfg.n_actions, dtype=torch.int32, device=dev),
+           "logp": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev),
+           "entropy": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev)}
+    stream = torch.cuda.current_stream(dev)
+
+    def step(k, ev=None):
+        inp, ids, g = sets[k % n_sets]
+        if ev:
+            ev[0].record(stream)
+        model.prefill(inp.vis, ids, inp.prompt_lens, out=logits)
+        if ev:
+            ev[1].record(stream)
+        model.decode_actions(g, T, batch=B, out=out)
+        if ev:
+            ev[2].record(stream)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    model.profile_begin(("prefill_gemm", "prefill_attn"))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = model.profile_end()
+    prefill_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    decode_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"[bench] {ms_per_step:.2f} ms/step (prefill {prefill_ms:.2f} ms, decode {decode_ms:.2f} ms)")
+
+    # decode kernels profiled on a separate step (events between the ~10^3
+    # decode launches would perturb the timed region)
+    inp0, ids0, g0 = sets[0]
+    model.prefill(inp0.vis, ids0, inp0.prompt_lens, out=logits)
+    model.profile_begin(("decode_gemm", "decode_attn"))
+    model.decode_actions(g0, T, batch=B, out=out)
+    dprof = model.profile_end()
+
+    # algorithmic work per step (the step's own inputs)
+    d, F, L = cfg.d_model, cfg.d_ffn, cfg.n_layers
+    layer_params = 4 * d * d + 3 * d * F
+    prefill_flops = decode_bytes = 0.0
+    for k in range(args.steps):
+        inp = sets[(args.warmup + k) % n_sets][0]
+        Lb = inp.prefix_lens.astype(np.float64)
+        prefill_flops += 2 * layer_params * L * Lb.sum() + 2 * d * L * (Lb * (Lb + 1)).sum() \
+            + 2 * d * cfg.action_bins * B
+        for t in range(1, cfg.n_actions):
+            decode_bytes += 2 * layer_params * L + 2 * cfg.action_bins * d \
+                + 4 * d * L * (Lb + t).sum() + 2 * d * B  # weights + head rows + KV + embeddings
+    prefill_flops /= args.steps
+    decode_bytes /= args.steps
+
+    pg = prof["prefill_gemm"]
+    g_ms = pg["ms"] / max(pg["launches"], 1)
+    g_tflops = pg["work"] / (pg["ms"] * 1e-3) / 1e12
+    dg = dprof["decode_gemm"]
+    dg_gbs = dg["work"] / (dg["ms"] * 1e-3) / 1e9
+    da = dprof["decode_attn"]
+    pa = prof["prefill_attn"]
+
+    result = {
+        "metric": "VLA actions/sec at 7B shape, batch 64; decode HBM GB/s; prefill MFMA util",
+        "value": B / (ms_per_step * 1e-3),
+        "unit": "actions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init bf16 weights ~N(0,0.02), N(0,1) visual embeddings, "
+                "uniform prompt ids, supplied Gumbel noise)",
+        "config": {"workload": f"{cfg.name}: OpenVLA-7B-shaped decoder (32 layers, d 4096, 32 heads, FFN 11008, "
+                               f"vocab 32064), batch {B}, 256 visual + prompt U[{cfg.prompt_min},{cfg.prompt_max}] "
+                               f"tokens, 7-token action decode with log-probs, T={T}",
+                   "global_batch": B, "seq_len": int(cfg.n_visual + cfg.prompt_max + cfg.n_actions),
+                   "parallelism": "single GPU"},
+        "action_tokens_per_s": B * cfg.n_actions / (ms_per_step * 1e-3),
+        "prefill_ms": prefill_ms,
+        "decode_ms": decode_ms,
+        "prefill_mfma_frac": prefill_flops / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "decode_hbm_gbs": decode_bytes / (decode_ms * 1e-3) / 1e9,
+        "decode_hbm_frac": decode_bytes / (decode_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+        "roofline": {"kernel": "gemm_bf16_kernel (prefill QKV/O/gate-up/down)", "bound": "mfma",
+                     "achieved": g_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": g_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_launch_ms": g_ms, "launches": pg["launches"]},
+        "roofline_decode": {"kernel": "skinny_kernel (decode QKV/O/gate-up/down)", "bound": "hbm",
+                            "achieved": dg_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": dg_gbs / PEAK_HBM_GBS, "traffic": None,
+                            "avg_launch_ms": dg["ms"] / max(dg["launches"], 1), "launches": dg["launches"]},
+        "kernels": {"prefill_attn_tflops": pa["work"] / max(pa["ms"], 1e-9) / 1e9,
+                    "prefill_attn_ms_per_step": pa["ms"] / args.steps,
+                    "prefill_gemm_ms_per_step": pg["ms"] / args.steps,
+                    "decode_attn_gbs": da["work"] / max(da["ms"], 1e-9) / 1e6,
+                    "decode_attn_ms": da["ms"], "decode_gemm_ms": dg["ms"]},
+    }
+
+    if not args.no_teacher_forced:
+        inp, ids, _ = sets[0]
+        acts = torch.from_numpy(I.stored_actions(cfg, B, seed=0)).to(dev)
+        model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(2):
+            model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tf_ms = e0.elapsed_time(e1) / 2
+        Lb = inp.prefix_lens.astype(np.float64) + cfg.n_actions
+        tf_flops = 2 * layer_params * L * Lb.sum() + 2 * d * L * (Lb * (Lb + 1)).sum()
+        result["teacher_forced"] = {"ms": tf_ms, "rows": int(Lb.sum()),
+                                    "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                    "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
+
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle CPU baseline ({args.cpu_layers} layers of one environment)")
+        result["cpu_baseline"] = cpu_baseline(cfg, w, sets[0][0], args.cpu_layers, T)
+    model.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

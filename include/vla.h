@@ -1,0 +1,188 @@
+/*
+ * vla.h -- C ABI of the MI355X (gfx950) batched VLA rollout-inference library.
+ *
+ * The library runs the policy step of VLA-RL's rollout phase (arXiv
+ * 2505.18719, Alg. 1 and Sec. 3.3): for a batch of environments it prefills
+ * [projected visual patch embeddings ; instruction prompt tokens] through an
+ * OpenVLA-style Llama-2 decoder (Sec. 3.1), then generates the |A| = 7 action
+ * tokens auto-regressively with a paged KV cache, sampling each token among
+ * the action bins (the last `action_bins` vocabulary ids, one bin per action
+ * dimension, Sec. 3.1) by Gumbel-max with caller-supplied noise, and returns
+ * the per-token log-probabilities whose sum is the action log-probability of
+ * Eq. 1, plus per-token entropies.  A teacher-forced entry point recomputes
+ * log-probabilities of stored action tokens, the numerator of the PPO ratio
+ * (Eq. 2).  Rollout runs in bf16 (Sec. 3.5, "Infrastructure"): weights and
+ * stored activations are bf16, accumulation and the residual stream fp32.
+ *
+ * Conventions
+ *  - Every pointer is a DEVICE pointer unless its name ends in `_host`.
+ *  - Streams are `hipStream_t` passed as `void*` (NULL = the default stream).
+ *    All work is enqueued asynchronously on that stream; outputs are valid
+ *    once the stream has been synchronised.  No call synchronises the host
+ *    with the device except `vla_read_device_flags`.
+ *  - The library never allocates device memory: the caller provides one
+ *    workspace of `vla_workspace_size` bytes and owns every buffer.
+ *  - Matrices are row-major.  Linear weights are `[out_features, in_features]`.
+ *  - Every call returns a status (0 = success, negative = error) and sets a
+ *    thread-local message readable with `vla_last_error`.  No C++ exception
+ *    crosses this boundary.
+ *  - A model handle is not thread-safe; use one handle per stream.
+ */
+#ifndef VLA_H_
+#define VLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define VLA_OK 0
+#define VLA_EINVAL -1        /* null pointer, non-positive size, bad temperature, ... */
+#define VLA_ESHAPE -2        /* batch > max_batch or a sequence longer than max_seq */
+#define VLA_EWORKSPACE -3    /* workspace smaller than vla_workspace_size() or misaligned */
+#define VLA_EHIP -4          /* a HIP runtime call failed; the message holds HIP's text */
+#define VLA_ESTATE -6        /* decode without a matching prefill on this handle */
+#define VLA_EUNSUPPORTED -7  /* configuration outside what the kernels implement */
+
+/* device-side flags (see vla_read_device_flags) */
+#define VLA_FLAG_BAD_PROMPT_ID 1u   /* a prompt id outside [0, vocab): a zero row was used */
+#define VLA_FLAG_BAD_ACTION 2u      /* a teacher-forced token outside the action range: scored as NaN */
+
+/* Decoder shape and capacity.
+ *   d_model = n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0;
+ *   d_ffn % 16 == 0; 1 <= action_bins <= 256; action_begin + action_bins <= vocab;
+ *   1 <= n_actions <= 16; max_seq <= 320 (prefix + n_actions rows of one env);
+ *   page_size == 16; 1 <= max_batch <= 512. */
+typedef struct vla_config {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t d_ffn;
+  int32_t vocab;
+  int32_t action_bins;   /* number of action bins (256 for OpenVLA) */
+  int32_t action_begin;  /* vocabulary id of bin 0 (vocab - action_bins for OpenVLA) */
+  int32_t n_actions;     /* action tokens per environment step, |A| = 7 (Eq. 1) */
+  int32_t n_visual;      /* visual patch embeddings per observation (256) */
+  float rope_base;       /* rotary base, 10000 */
+  float rms_eps;         /* RMSNorm epsilon, 1e-6 */
+  int32_t max_batch;     /* largest batch passed to any call on the handle */
+  int32_t max_seq;       /* longest sequence: n_visual + prompt + n_actions */
+  int32_t page_size;     /* KV-cache page size in tokens (16) */
+} vla_config;
+
+/* Decoder weights, all bf16 device memory, read only during vla_create.
+ * Per-layer entries are HOST arrays of n_layers device pointers. */
+typedef struct vla_weights {
+  const void* embed;              /* [vocab, d_model] token embedding */
+  const void* lm_head;            /* [vocab, d_model] output projection (untied) */
+  const void* final_norm;         /* [d_model] RMSNorm gain */
+  const void* const* attn_norm;   /* [d_model] per layer */
+  const void* const* wq;          /* [d_model, d_model] per layer */
+  const void* const* wk;          /* [d_model, d_model] */
+  const void* const* wv;          /* [d_model, d_model] */
+  const void* const* wo;          /* [d_model, d_model] */
+  const void* const* mlp_norm;    /* [d_model] */
+  const void* const* wgate;       /* [d_ffn, d_model] */
+  const void* const* wup;         /* [d_ffn, d_model] */
+  const void* const* wdown;       /* [d_model, d_ffn] */
+} vla_weights;
+
+typedef struct vla_model vla_model;  /* opaque handle */
+
+/* Bytes of device workspace a model with this configuration needs: repacked
+ * weights, the paged KV pool for max_batch * max_seq tokens, activations and
+ * split-K partials.  Returns VLA_EINVAL / VLA_EUNSUPPORTED for a bad config. */
+int vla_workspace_size(const vla_config* cfg, size_t* bytes_host);
+
+/* Validate `cfg`, lay out `workspace` (256-byte aligned, >= vla_workspace_size
+ * bytes, owned by the caller and kept alive until vla_destroy) and repack the
+ * weights into it on `stream`: fused [Wq;Wk;Wv] with the rotary pairs of each
+ * head arranged for the fused RoPE epilogue, interleaved [Wgate;Wup], the
+ * action-bin rows of the LM head, fp32 norm gains and a rotary table computed
+ * on the host in double precision.  The caller may free `weights` once
+ * `stream` has completed.  On success *out receives the handle. */
+int vla_create(const vla_config* cfg, const vla_weights* weights, void* workspace,
+               size_t workspace_bytes, void* stream, vla_model** out);
+
+/* Prefill (Alg. 1, the policy-generation step, first half): for environment b
+ * the sequence is its n_visual rows of `vis_emb` followed by the embedding
+ * rows of its prompt ids, at positions 0 .. L_b-1 with L_b = n_visual +
+ * prompt_lens_host[b] (causal attention over the whole prefix, no special
+ * tokens).  Environments are packed without padding (ragged prefill) and each
+ * gets its own KV-cache pages.
+ *   vis_emb          bf16 [batch, n_visual, d_model]
+ *   prompt_ids       int32 [sum(prompt_lens_host)], environment b's ids follow env b-1's
+ *   prompt_lens_host int32 [batch] on the host, each >= 0, L_b + n_actions <= max_seq
+ *   action_logits    fp32 [batch, action_bins] out: logits of the action bins at
+ *                    the last prefix row (raw, before temperature)
+ * The handle keeps the KV cache and these logits for vla_decode_actions. */
+int vla_prefill(vla_model* m, int32_t batch, const void* vis_emb, const int32_t* prompt_ids,
+                const int32_t* prompt_lens_host, float* action_logits, void* stream);
+
+/* Decode the n_actions action tokens of the batch prefilled last (Alg. 1,
+ * policy generation and the sum of token log-probabilities, Eq. 1).  Token i
+ * is bin k_i = argmax_j (z_ij / T + g_ij) (lowest j on exact ties), i.e. a
+ * draw from softmax(z_i / T) over the action bins, where z_i are the logits
+ * at position L_b - 1 + i; tokens 0 .. n_actions-2 are fed back through the
+ * KV-cached decoder.
+ *   batch        must equal the last vla_prefill's batch (else VLA_ESTATE)
+ *   gumbel       fp32 [batch, n_actions, action_bins] standard Gumbel noise g
+ *   temperature  T > 0 (VLA-RL samples at T = 1.5)
+ *   tokens       int32 [batch, n_actions] out: vocabulary ids action_begin + k_i
+ *   logp         fp32 [batch, n_actions] out: log softmax(z_i / T)[k_i]
+ *   entropy      fp32 [batch, n_actions] out, or NULL: entropy of softmax(z_i / T)
+ *   step_logits  fp32 [batch, n_actions, action_bins] out, or NULL: z_i
+ * The decode consumes the prefill state: a second call needs a new prefill. */
+int vla_decode_actions(vla_model* m, int32_t batch, const float* gumbel, float temperature,
+                       int32_t* tokens, float* logp, float* entropy, float* step_logits,
+                       void* stream);
+
+/* Teacher-forced pass (numerator of the PPO ratio, Eq. 2): one causal forward
+ * over [visual ; prompt ; the n_actions given action tokens] per environment,
+ * with no KV reuse, scoring token i by the logits at row L_b - 1 + i.
+ *   vis_emb, prompt_ids, prompt_lens_host  as in vla_prefill
+ *   action_tokens  int32 [batch, n_actions] vocabulary ids in
+ *                  [action_begin, action_begin + action_bins); others raise
+ *                  VLA_FLAG_BAD_ACTION and are scored as NaN
+ *   logp, entropy  fp32 [batch, n_actions] out (entropy may be NULL)
+ *   logits         fp32 [batch, n_actions, action_bins] out, or NULL
+ * Overwrites the handle's prefill state (a later decode needs a new prefill). */
+int vla_token_logprobs(vla_model* m, int32_t batch, const void* vis_emb, const int32_t* prompt_ids,
+                       const int32_t* prompt_lens_host, const int32_t* action_tokens,
+                       float temperature, float* logp, float* entropy, float* logits, void* stream);
+
+/* Synchronise `stream`, return the OR of VLA_FLAG_* raised by kernels since
+ * the last read into *flags_host, and clear them. */
+int vla_read_device_flags(vla_model* m, void* stream, uint32_t* flags_host);
+
+/* Live kernel timing.  vla_profile_begin(m, mask) starts recording a pair of
+ * HIP events on the launch stream around every kernel launch of the selected
+ * categories (bit i of `mask` selects category i) together with the
+ * launch's algorithmic work (flops for VLA_PROF_PREFILL_*, HBM bytes for
+ * VLA_PROF_DECODE_*: weights, activations and KV read once, no split-K
+ * partials).  vla_profile_end waits for the recorded events and, for each
+ * category, writes the summed kernel time in milliseconds, the summed work
+ * and the number of launches into arrays of VLA_PROF_CATEGORIES entries, then
+ * stops recording.  At most 16384 launches are recorded per begin/end. */
+#define VLA_PROF_PREFILL_GEMM 0
+#define VLA_PROF_PREFILL_ATTN 1
+#define VLA_PROF_DECODE_GEMM 2
+#define VLA_PROF_DECODE_ATTN 3
+#define VLA_PROF_CATEGORIES 4
+int vla_profile_begin(vla_model* m, uint32_t mask);
+int vla_profile_end(vla_model* m, double* ms_host, double* work_host, int64_t* launches_host);
+
+/* Release the handle (not the caller's workspace).  Safe on NULL. */
+void vla_destroy(vla_model* m);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* vla_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_H_ */

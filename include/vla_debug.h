@@ -1,0 +1,43 @@
+/*
+ * vla_debug.h -- test hooks of libvla.so: single kernels of the rollout path
+ * exposed for kernel-level parity tests.  Not part of the rollout API; same
+ * conventions as vla.h (device pointers, async on `stream`, status codes).
+ */
+#ifndef VLA_DEBUG_H_
+#define VLA_DEBUG_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Prefill MFMA GEMM: C[M, N] fp32 = A[M, K] bf16 (row stride lda) * W[N, K]^T bf16.
+ * Requires K % 64 == 0, N % 64 == 0, lda % 8 == 0. */
+int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, float* C,
+                   void* stream);
+
+/* Decode split-K GEMM: C[M, N] fp32 = A * W^T for M <= 128, using `splits`
+ * K slices whose partial sums go to `scratch` (splits * M * N floats).
+ * Requires N % 64 == 0, K % 32 == 0. */
+int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t splits,
+                     float* scratch, float* C, void* stream);
+
+/* Sampler on given logits z[B, A] at step `step` of gumbel[B, n_actions, A]:
+ * writes tokens / logp / entropy / logits at [b, step] exactly as
+ * vla_decode_actions does.  `next_tok` receives the sampled vocabulary ids. */
+int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, int32_t step, int32_t action_begin,
+                     const float* gumbel, float temperature, int32_t* tokens, int32_t* next_tok, float* logp,
+                     float* entropy, float* logits_out, void* stream);
+
+/* Copy `bytes` of an internal buffer of the handle to `dst` (device):
+ * which = 0 residual x fp32 [rows, d], 1 rotated q bf16 [rows, d], 2 / 3 the K / V
+ * page pool of `layer` (bf16, page layouts of the KV cache), 4 the bf16
+ * activation buffer [rows, d]. */
+struct vla_model;
+int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_DEBUG_H_ */

@@ -315,8 +315,10 @@ def rollout(cfg, w, vis, prompt_ids, prompt_lens, gumbel, temperature: float,
             feed_tokens: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
     """Batched rollout of Alg. 1's policy step over the selected environments.
 
-    Returns tokens int32 [n, 7], logp / entropy / margin [n, 7], logits [n, 7, A]
-    and ``logp_sum`` [n] (the action log-probability of Eq. 1).
+    ``feed_tokens``, if given, is indexed by environment id ([B, 7] for the
+    whole batch).  Returns tokens int32 [n, 7], logp / entropy / margin
+    [n, 7], logits [n, 7, A] and ``logp_sum`` [n] (the action log-probability
+    of Eq. 1) for the n selected environments.
     """
     W = as_weights(w, cfg)
     prompts = _split_prompts(prompt_ids, prompt_lens)

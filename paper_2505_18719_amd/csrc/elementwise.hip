@@ -1,0 +1,333 @@
+// Memory-bound kernels of the VLA rollout path on gfx950: input assembly,
+// RMSNorm (one wave per row, fp32 statistics), the consumers of the decode
+// GEMM's split-K partials (residual add + RMSNorm, SwiGLU, RoPE + KV append,
+// logits), and one-time weight repacking.  All loads and stores are 16-byte
+// vectors where the layout allows.
+#include "common.h"
+#include "kernels.h"
+
+namespace vla {
+
+namespace {
+
+// ------------------------------------------------------------------ embed
+// x^0 rows of each environment: n_visual projected visual embeddings, then the
+// embedding rows of its prompt ids, then (teacher-forced pass) its actions.
+__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+  const int row = blockIdx.x;
+  const int env = a.row_env[row], pos = a.row_pos[row];
+  const bf16_t* src;
+  if (pos < a.n_visual) {
+    src = a.vis + ((size_t)env * a.n_visual + pos) * a.d;
+  } else {
+    int id;
+    if (pos < a.env_prefix[env]) id = a.prompt_ids[a.env_prompt_off[env] + pos - a.n_visual];
+    else id = a.actions[env * a.n_actions + pos - a.env_prefix[env]];
+    if (id < 0 || id >= a.vocab) {
+      if (threadIdx.x == 0) atomicOr(a.flags, 1u);
+      src = nullptr;
+    } else {
+      src = a.emb + (size_t)id * a.d;
+    }
+  }
+  float* dst = a.x + (size_t)row * a.d;
+  for (int c = threadIdx.x * 8; c < a.d; c += 256 * 8) {
+    float f[8];
+    if (src) unpack8(*reinterpret_cast<const uint4*>(src + c), f);
+    else
+#pragma unroll
+      for (int i = 0; i < 8; ++i) f[i] = 0.f;
+    reinterpret_cast<float4*>(dst + c)[0] = make_float4(f[0], f[1], f[2], f[3]);
+    reinterpret_cast<float4*>(dst + c)[1] = make_float4(f[4], f[5], f[6], f[7]);
+  }
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// One wave per row: u = bf16(x * rsqrt(mean(x^2) + eps) * g).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
+                                                      const int32_t* __restrict__ rows,
+                                                      const float* __restrict__ g, float eps,
+                                                      bf16_t* __restrict__ u, int ldu, int M, int d) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= M) return;
+  const int src = rows ? rows[i] : i;
+  const float* xr = x + (size_t)src * ldx;
+  float ss = 0.f;
+  for (int c = lane * 4; c < d; c += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  const float r = rsqrtf(ss / (float)d + eps);
+  bf16_t* ur = u + (size_t)i * ldu;
+  for (int c = lane * 4; c < d; c += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + c);
+    const float4 w = *reinterpret_cast<const float4*>(g + c);
+    uint2 o;
+    o.x = pack2bf(v.x * r * w.x, v.y * r * w.y);
+    o.y = pack2bf(v.z * r * w.z, v.w * r * w.w);
+    *reinterpret_cast<uint2*>(ur + c) = o;
+  }
+}
+
+// Block-wide sum over 256 threads.
+__device__ __forceinline__ float block_sum256(float v, float* sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  return sh[0] + sh[1] + sh[2] + sh[3];
+}
+
+constexpr int kMaxPerThread = 32;  // d <= 8192
+
+__global__ __launch_bounds__(256) void embed_token_norm_kernel(const int32_t* tok, const bf16_t* emb, float* x,
+                                                               bf16_t* u, const float* g, float eps, int d,
+                                                               int vocab, uint32_t* flags) {
+  __shared__ float sh[4];
+  const int b = blockIdx.x;
+  int id = tok[b];
+  const bool ok = id >= 0 && id < vocab;
+  if (!ok && threadIdx.x == 0) atomicOr(flags, 1u);
+  float v[kMaxPerThread];
+  float ss = 0.f;
+  int n = 0;
+  for (int c = threadIdx.x; c < d; c += 256, ++n) {
+    v[n] = ok ? bf2f(emb[(size_t)id * d + c]) : 0.f;
+    ss += v[n] * v[n];
+  }
+  ss = block_sum256(ss, sh);
+  const float r = rsqrtf(ss / (float)d + eps);
+  n = 0;
+  for (int c = threadIdx.x; c < d; c += 256, ++n) {
+    x[(size_t)b * d + c] = v[n];
+    u[(size_t)b * d + c] = f2bf(v[n] * r * g[c]);
+  }
+}
+
+__global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* __restrict__ part, int splits,
+                                                                   float* __restrict__ x, bf16_t* __restrict__ u,
+                                                                   const float* __restrict__ g, float eps, int M,
+                                                                   int d) {
+  __shared__ float sh[4];
+  const int m = blockIdx.x;
+  float v[kMaxPerThread];
+  float ss = 0.f;
+  int n = 0;
+  for (int c = threadIdx.x; c < d; c += 256, ++n) {
+    float acc = 0.f;
+    for (int s = 0; s < splits; ++s) acc += part[((size_t)s * M + m) * d + c];
+    v[n] = x[(size_t)m * d + c] + acc;
+    ss += v[n] * v[n];
+  }
+  ss = block_sum256(ss, sh);
+  const float r = rsqrtf(ss / (float)d + eps);
+  n = 0;
+  for (int c = threadIdx.x; c < d; c += 256, ++n) {
+    x[(size_t)m * d + c] = v[n];
+    u[(size_t)m * d + c] = f2bf(v[n] * r * g[c]);
+  }
+}
+
+// Interleaved gate/up columns: gate j at 64*(j/32) + j%32, up j 32 further.
+__global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restrict__ part, int splits,
+                                                            bf16_t* __restrict__ h, int ldh, int M, int Fp) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int m = blockIdx.y;
+  if (j >= Fp) return;
+  const int N = 2 * Fp;
+  const int cg = 64 * (j >> 5) + (j & 31);
+  float gs = 0.f, us = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    const float* p = part + ((size_t)s * M + m) * N;
+    gs += p[cg];
+    us += p[cg + 32];
+  }
+  h[(size_t)m * ldh + j] = f2bf(gs / (1.f + expf(-gs)) * us);
+}
+
+__global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict__ part, int splits,
+                                                         float* __restrict__ z, int M, int N, int ldp) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)M * N) return;
+  const size_t m = i / N, n = i % N;
+  float acc = 0.f;
+  for (int s = 0; s < splits; ++s) acc += part[((size_t)s * M + m) * ldp + n];
+  z[i] = acc;
+}
+
+// One thread per rotary pair of q and k, and per pair of v features.
+__global__ __launch_bounds__(256) void decode_qkv_kernel(DecodeQkvArgs a) {
+  const int b = blockIdx.y;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int d = a.d, hd = a.head_dim, half = hd / 2, H = a.n_heads;
+  if (t >= 3 * (d / 2)) return;
+  const int region = t / (d / 2);
+  const int p = t - region * (d / 2);            // pair index within the region
+  const int head = p / half, e = p % half;       // e in [0, half)
+  const int N = 3 * d;
+  // permuted columns of the pair (see the prefill GEMM's RoPE epilogue)
+  const int blk = e / 32, c = e % 32;
+  int col1, col2;
+  if (region < 2) {
+    col1 = region * d + head * hd + 64 * blk + c;
+    col2 = col1 + 32;
+  } else {  // v keeps the natural order: features e and e + half
+    col1 = 2 * d + head * hd + e;
+    col2 = col1 + half;
+  }
+  float x1 = 0.f, x2 = 0.f;
+  for (int s = 0; s < a.splits; ++s) {
+    const float* pr = a.part + ((size_t)s * a.B + b) * N;
+    x1 += pr[col1];
+    x2 += pr[col2];
+  }
+  const int pos = a.env_prefix[b] + a.step - 1;
+  if (region == 0) {
+    const float2 cs = a.rope[pos * half + e];
+    bf16_t* qr = a.q + (size_t)b * d + head * hd;
+    qr[e] = f2bf(x1 * cs.x - x2 * cs.y);
+    qr[e + half] = f2bf(x1 * cs.y + x2 * cs.x);
+    return;
+  }
+  const int page = a.page_table[b * a.max_pages + pos / kPage];
+  const int slot = pos % kPage;
+  if (region == 1) {
+    const float2 cs = a.rope[pos * half + e];
+    bf16_t* kr = a.kv.k + (((size_t)page * H + head) * kPage + slot) * hd;
+    kr[e] = f2bf(x1 * cs.x - x2 * cs.y);
+    kr[e + half] = f2bf(x1 * cs.y + x2 * cs.x);
+  } else {
+    bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + slot;
+    vb[(size_t)e * kPage] = f2bf(x1);
+    vb[(size_t)(e + half) * kPage] = f2bf(x2);
+  }
+}
+
+// ------------------------------------------------------------------ repacking
+// q/k rows of each head reordered so that each 64-row block holds rotary
+// pairs 32 rows apart: block b = rows [32b, 32b+32) then [half+32b, half+32b+32).
+__global__ __launch_bounds__(256) void repack_qk_kernel(bf16_t* dst, const bf16_t* src, int d, int hd) {
+  const int r = blockIdx.x;  // destination row
+  const int head = r / hd, p = r % hd, half = hd / 2;
+  const int blk = p / 64, c = p % 64;
+  const int orig = head * hd + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32);
+  for (int k = threadIdx.x * 8; k < d; k += 256 * 8)
+    *reinterpret_cast<uint4*>(dst + (size_t)r * d + k) = *reinterpret_cast<const uint4*>(src + (size_t)orig * d + k);
+}
+
+// [gate; up] interleaved in blocks of 32 rows, zero rows past F.
+__global__ __launch_bounds__(256) void repack_gate_up_kernel(bf16_t* dst, const bf16_t* gate, const bf16_t* up,
+                                                             int F, int d) {
+  const int r = blockIdx.x;
+  const int j = 32 * (r / 64) + (r % 32);
+  const bf16_t* src = (j < F) ? ((r % 64) < 32 ? gate : up) + (size_t)j * d : nullptr;
+  for (int k = threadIdx.x * 8; k < d; k += 256 * 8)
+    *reinterpret_cast<uint4*>(dst + (size_t)r * d + k) =
+        src ? *reinterpret_cast<const uint4*>(src + k) : make_uint4(0, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(256) void pad_cols_kernel(bf16_t* dst, const bf16_t* src, int cols, int cols_p) {
+  const int r = blockIdx.x;
+  for (int c = threadIdx.x; c < cols_p; c += 256)
+    dst[(size_t)r * cols_p + c] = c < cols ? src[(size_t)r * cols + c] : (bf16_t)0;
+}
+
+__global__ void bf16_to_f32_kernel(float* dst, const bf16_t* src, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = bf2f(src[i]);
+}
+
+__global__ void fill_zero_kernel(uint4* dst, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256)
+    dst[i] = make_uint4(0, 0, 0, 0);
+}
+
+}  // namespace
+
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.d % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_kernel, dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps, bf16_t* u,
+                          int ldu, int M, int d, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (d % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float* x, bf16_t* u, const float* g,
+                                   float eps, int B, int d, int vocab, uint32_t* flags, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (d > 256 * kMaxPerThread) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_token_norm_kernel, dim3(B), dim3(256), 0, s, tok, emb, x, u, g, eps, d, vocab, flags);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u, const float* g,
+                                       float eps, int M, int d, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (d > 256 * kMaxPerThread) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(256), 0, s, part, splits, x, u, g, eps, M, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_swiglu(const float* part, int splits, bf16_t* h, int ldh, int M, int Fp, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((Fp + 255) / 256, M), dim3(256), 0, s, part, splits, h, ldh, M, Fp);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_sum(const float* part, int splits, float* z, int M, int N, int ldp, hipStream_t s) {
+  const size_t n = (size_t)M * N;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, splits, z, M, N,
+                     ldp);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s) {
+  if (a.B <= 0) return hipSuccess;
+  const int threads = 3 * (a.d / 2);
+  hipLaunchKernelGGL(decode_qkv_kernel, dim3((threads + 255) / 256, a.B), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack_qk(bf16_t* dst, const bf16_t* src, int d, int hd, hipStream_t s) {
+  hipLaunchKernelGGL(repack_qk_kernel, dim3(d), dim3(256), 0, s, dst, src, d, hd);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack_gate_up(bf16_t* dst, const bf16_t* gate, const bf16_t* up, int F, int Fp, int d,
+                                 hipStream_t s) {
+  hipLaunchKernelGGL(repack_gate_up_kernel, dim3(2 * Fp), dim3(256), 0, s, dst, gate, up, F, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_pad_cols(bf16_t* dst, const bf16_t* src, int rows, int cols, int cols_p, hipStream_t s) {
+  hipLaunchKernelGGL(pad_cols_kernel, dim3(rows), dim3(256), 0, s, dst, src, cols, cols_p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s) {
+  hipLaunchKernelGGL(bf16_to_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if (bytes % 16 != 0) return hipErrorInvalidValue;
+  const size_t n16 = bytes / 16;
+  size_t blocks = (n16 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<uint4*>(dst), n16);
+  return hipGetLastError();
+}
+
+}  // namespace vla

@@ -1,0 +1,184 @@
+// Launch interface of the gfx950 kernels (host side).  Every launcher takes
+// plain device pointers and a stream and returns the launch's hipError_t.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vla {
+
+typedef uint16_t bf16_t;
+
+// Paged KV cache of one layer.  K pages are [page][head][slot][head_dim]
+// (each key row contiguous); V pages are stored transposed,
+// [page][head][head_dim][slot], so that 8 consecutive keys of one feature are
+// one 16-byte load for the attention P*V products.  page_size is 16 tokens.
+constexpr int kPage = 16;
+
+struct KvCache {
+  bf16_t* k;
+  bf16_t* v;
+};
+
+// Per-row metadata of a packed ragged batch (device arrays).
+struct RowMeta {
+  const int32_t* row_pos;     // [M] position of the row inside its environment
+  const int32_t* row_env;     // [M] environment of the row
+  const int32_t* page_table;  // [B, max_pages] physical page of each 16-token block
+  int max_pages;
+};
+
+// Prefill GEMM, C = A * W^T with A [M, K] bf16 (row stride lda) and W [N, K]
+// bf16, fp32 accumulation on MFMA, and one of these epilogues:
+enum GemmEpilogue {
+  kEpiStoreF32 = 0,  // C[m, n] = acc                         (fp32, ldc)
+  kEpiResidual = 1,  // C[m, n] += acc                        (fp32 residual stream, ldc)
+  kEpiSwiGlu = 2,    // H[m, j] = bf16(silu(gate) * up)  for W = interleaved [gate; up] blocks of 32 rows
+  kEpiQkvRope = 3,   // rotate q, k by RoPE, store q bf16 [M, d] and K/V into the page pool
+};
+
+struct GemmArgs {
+  const bf16_t* A;
+  int lda;
+  const bf16_t* W;
+  int M, N, K;
+  float* C;
+  int ldc;
+  bf16_t* H;
+  int ldh;
+  // kEpiQkvRope
+  bf16_t* q;
+  int ldq;
+  KvCache kv;
+  RowMeta meta;
+  const float2* rope;  // [pos][head_dim / 2] (cos, sin)
+  int d_model, n_heads, head_dim;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s);
+
+// Skinny split-K GEMM for decode: part[s, m, n] = sum over the s-th K slice of
+// A[m, k] * W[n, k], for M <= 128 rows.  Requires N % 64 == 0, K % 32 == 0.
+struct SkinnyArgs {
+  const bf16_t* A;
+  int lda;
+  int M;
+  const bf16_t* W;
+  int N, K;
+  float* part;  // [splits, M, N]
+  int splits;
+};
+int skinny_splits(int M, int N, int K, int max_splits);
+hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t s);
+
+// Elementwise / reduction kernels
+struct EmbedArgs {
+  float* x;                     // [M, d] out
+  const bf16_t* emb;            // [vocab, d]
+  const bf16_t* vis;            // [B, n_visual, d]
+  const int32_t* prompt_ids;    // packed
+  const int32_t* actions;       // [B, n_actions] or null
+  const int32_t* row_pos;
+  const int32_t* row_env;
+  const int32_t* env_prefix;    // [B] L_b
+  const int32_t* env_prompt_off;// [B]
+  int M, d, n_visual, n_actions, vocab;
+  uint32_t* flags;
+};
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+
+// u[i] = bf16(rmsnorm(x[rows ? rows[i] : i]) * g), i < M
+hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps,
+                          bf16_t* u, int ldu, int M, int d, hipStream_t s);
+
+// Decode step input: x[b] = emb[tok[b]], u[b] = bf16(rmsnorm(x[b]) * g)
+hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float* x, bf16_t* u,
+                                   const float* g, float eps, int B, int d, int vocab,
+                                   uint32_t* flags, hipStream_t s);
+
+// x[m] += sum_s part[s, m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d)
+hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u,
+                                       const float* g, float eps, int M, int d, hipStream_t s);
+
+// h[m, j] = bf16(silu(sum gate) * sum up) from interleaved partial columns
+hipError_t launch_reduce_swiglu(const float* part, int splits, bf16_t* h, int ldh, int M, int Fp,
+                                hipStream_t s);
+
+// z[m, n] = sum_s part[s, m, n] for n < N; partial rows have stride ldp >= N
+hipError_t launch_reduce_sum(const float* part, int splits, float* z, int M, int N, int ldp, hipStream_t s);
+
+// Decode: sum QKV partials, RoPE at position env_prefix[b] + step - 1, store q
+// and append K/V of the new token to the page pool.
+struct DecodeQkvArgs {
+  const float* part;
+  int splits;
+  bf16_t* q;
+  KvCache kv;
+  const int32_t* page_table;
+  int max_pages;
+  const int32_t* env_prefix;
+  int step;  // 1-based decode step: token position = env_prefix[b] + step - 1
+  const float2* rope;
+  int B, d, n_heads, head_dim;
+};
+hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s);
+
+// Attention
+struct PrefillAttnArgs {
+  const bf16_t* q;  // [M, d]
+  bf16_t* o;        // [M, d]
+  KvCache kv;
+  const int32_t* page_table;
+  int max_pages;
+  const int32_t* env_row0;    // [B] first packed row of env b
+  const int32_t* env_len;     // [B] rows of env b in this pass
+  const int32_t* qblocks;     // [n_qblocks, 2] (env, first query row)
+  int n_qblocks, d, n_heads, head_dim;
+  float scale;
+};
+hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
+
+struct DecodeAttnArgs {
+  const bf16_t* q;  // [B, d]
+  bf16_t* o;        // [B, d]
+  KvCache kv;
+  const int32_t* page_table;
+  int max_pages;
+  const int32_t* env_prefix;
+  int step;  // keys 0 .. env_prefix[b] + step - 1
+  int B, d, n_heads, head_dim;
+  float scale;
+};
+hipError_t launch_attn_decode(const DecodeAttnArgs& a, hipStream_t s);
+
+// Sampler over the action bins (one wave per row).
+struct SamplerArgs {
+  const float* z;          // [rows, A] logits
+  int A;
+  float inv_t;             // unused; the kernel divides by temperature
+  float temperature;
+  // sampling mode (gumbel != null): row b, step i
+  const float* gumbel;     // [B, n_actions, A]
+  int step, n_actions, action_begin;
+  int32_t* tokens;         // [B, n_actions]
+  int32_t* next_tok;       // [B]
+  // teacher-forced mode (gumbel == null): row r = b * n_actions + i scores given[r]
+  const int32_t* given;    // [rows]
+  float* logp;             // sampling: [B, n_actions] at step; TF: [rows]
+  float* entropy;          // same layout, may be null
+  float* logits_out;       // same layout times A, may be null
+  int rows;
+  uint32_t* flags;
+};
+hipError_t launch_sampler(const SamplerArgs& a, hipStream_t s);
+
+// Weight repacking (one-time, at create)
+hipError_t launch_repack_qk(bf16_t* dst, const bf16_t* src, int d, int head_dim, hipStream_t s);
+hipError_t launch_repack_gate_up(bf16_t* dst, const bf16_t* gate, const bf16_t* up, int F, int Fp,
+                                 int d, hipStream_t s);
+hipError_t launch_pad_cols(bf16_t* dst, const bf16_t* src, int rows, int cols, int cols_p,
+                           hipStream_t s);
+hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
+hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
+
+}  // namespace vla

@@ -1,0 +1,672 @@
+// Host runtime of the VLA library: C ABI, argument validation, workspace
+// layout, one-time weight repacking, ragged-batch metadata and page tables,
+// and the launch sequences of prefill, KV-cached action decode and the
+// teacher-forced pass.  No device memory is allocated here: every buffer is a
+// slice of the caller's workspace.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "vla.h"
+
+using namespace vla;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define VLA_CK(expr)                                                                        \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess) return fail(VLA_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kMaxSplits = 16;
+constexpr int kSkinnyRows = 128;
+constexpr int kQBlock = 64;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int round_up(int v, int a) { return (v + a - 1) / a * a; }
+
+// Sizes derived from a configuration.
+struct Dims {
+  int d, H, hd, F, Fp, A, Ap, V, L, nact, nvis;
+  int Bmax, Smax, max_pages, n_pages;
+  size_t Mmax;      // packed rows of the largest pass
+  int Nmax;         // widest skinny GEMM
+  int qblk_max;
+  size_t meta_ints;
+};
+
+int check_config(const vla_config* c, Dims* o) {
+  if (!c) return fail(VLA_EINVAL, "cfg is NULL");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_heads < 1 || c->head_dim < 1 || c->d_ffn < 1 || c->vocab < 1 ||
+      c->action_bins < 1 || c->n_actions < 1 || c->n_visual < 0 || c->max_batch < 1 || c->max_seq < 1)
+    return fail(VLA_EINVAL, "config has a non-positive size");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(VLA_EUNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->d_model != c->n_heads * c->head_dim) return fail(VLA_EINVAL, "d_model != n_heads * head_dim");
+  if (c->d_model > 8192) return fail(VLA_EUNSUPPORTED, "d_model must be <= 8192");
+  if (c->action_bins > 256) return fail(VLA_EUNSUPPORTED, "action_bins must be <= 256");
+  if (c->action_begin < 0 || c->action_begin + c->action_bins > c->vocab)
+    return fail(VLA_EINVAL, "action range outside the vocabulary");
+  if (c->n_actions > 16) return fail(VLA_EUNSUPPORTED, "n_actions must be <= 16");
+  if (c->page_size != kPage) return fail(VLA_EUNSUPPORTED, "page_size must be 16");
+  if (c->max_seq > 320) return fail(VLA_EUNSUPPORTED, "max_seq must be <= 320");
+  if (c->max_seq < c->n_visual + c->n_actions + (c->n_visual == 0 ? 1 : 0))
+    return fail(VLA_EINVAL, "max_seq smaller than n_visual + n_actions");
+  if (c->max_batch > 512) return fail(VLA_EUNSUPPORTED, "max_batch must be <= 512");
+  if (!(c->rope_base > 1.f) || !(c->rms_eps >= 0.f)) return fail(VLA_EINVAL, "bad rope_base or rms_eps");
+  Dims& D = *o;
+  D.d = c->d_model;
+  D.H = c->n_heads;
+  D.hd = c->head_dim;
+  D.F = c->d_ffn;
+  D.Fp = round_up(c->d_ffn, 64);
+  D.A = c->action_bins;
+  D.Ap = round_up(c->action_bins, 64);
+  D.V = c->vocab;
+  D.L = c->n_layers;
+  D.nact = c->n_actions;
+  D.nvis = c->n_visual;
+  D.Bmax = c->max_batch;
+  D.Smax = c->max_seq;
+  D.max_pages = (c->max_seq + kPage - 1) / kPage;
+  D.n_pages = D.max_pages * D.Bmax;
+  D.Mmax = (size_t)D.Bmax * D.Smax;
+  D.Nmax = std::max(std::max(3 * D.d, 2 * D.Fp), D.Ap);
+  D.qblk_max = D.Bmax * ((D.Smax + kQBlock - 1) / kQBlock);
+  D.meta_ints = 2 * D.Mmax + 4 * (size_t)D.Bmax + (size_t)D.Bmax * D.max_pages + 2 * (size_t)D.qblk_max +
+                (size_t)D.Bmax * D.nact;
+  return VLA_OK;
+}
+
+// Workspace layout; with base == nullptr only the size is computed.
+struct Layout {
+  size_t off = 0;
+  char* base = nullptr;
+  template <class T>
+  T* take(size_t count) {
+    off = align_up(off, 256);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+struct LayerW {
+  bf16_t *wqkv, *wo, *wgu, *wd;
+  float *attn_norm, *mlp_norm;
+};
+
+}  // namespace
+
+struct vla_model {
+  vla_config cfg;
+  Dims D;
+  bf16_t* emb;
+  bf16_t* lm_act;  // [Ap, d], rows past A are zero
+  float* final_norm;
+  std::vector<LayerW> lw;
+  std::vector<KvCache> kv;
+  float2* rope;
+  float* x;
+  bf16_t* u;
+  bf16_t* q;
+  bf16_t* h;
+  float* part;
+  float* logits_pre;  // [Bmax, A]
+  float* logits_dec;  // [Bmax, A]
+  float* logits_tf;   // [Bmax * nact, A]
+  bf16_t* u_head;     // [Bmax * nact, d]
+  int32_t* next_tok;  // [Bmax]
+  uint32_t* flags;
+  int32_t* meta_dev;
+  int32_t* meta_host;  // pinned staging
+  hipEvent_t meta_event;
+  bool meta_pending;
+  // device views into meta_dev
+  int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *page_table, *qblocks, *head_rows;
+  // decode state
+  int state_batch;
+  bool state_valid;
+  std::vector<int> prefix_host;  // L_b of the last prefill
+  float scale;
+  // live profiling
+  struct ProfSlot {
+    hipEvent_t a, b;
+    int cat;
+    double work;
+  };
+  std::vector<ProfSlot> prof;
+  int prof_used;
+  uint32_t prof_mask;
+};
+
+namespace {
+
+void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
+  vla_model tmp;
+  vla_model& M = m ? *m : tmp;
+  M.emb = L.take<bf16_t>((size_t)D.V * D.d);
+  M.lm_act = L.take<bf16_t>((size_t)D.Ap * D.d);
+  M.final_norm = L.take<float>(D.d);
+  M.lw.resize(n_layers);
+  M.kv.resize(n_layers);
+  for (int l = 0; l < n_layers; ++l) {
+    LayerW& w = M.lw[l];
+    w.wqkv = L.take<bf16_t>((size_t)3 * D.d * D.d);
+    w.wo = L.take<bf16_t>((size_t)D.d * D.d);
+    w.wgu = L.take<bf16_t>((size_t)2 * D.Fp * D.d);
+    w.wd = L.take<bf16_t>((size_t)D.d * D.Fp);
+    w.attn_norm = L.take<float>(D.d);
+    w.mlp_norm = L.take<float>(D.d);
+  }
+  const size_t kv_elems = (size_t)D.n_pages * D.H * kPage * D.hd;
+  for (int l = 0; l < n_layers; ++l) {
+    M.kv[l].k = L.take<bf16_t>(kv_elems);
+    M.kv[l].v = L.take<bf16_t>(kv_elems);
+  }
+  M.rope = L.take<float2>((size_t)D.Smax * (D.hd / 2));
+  M.x = L.take<float>(D.Mmax * D.d);
+  M.u = L.take<bf16_t>(D.Mmax * D.d);
+  M.q = L.take<bf16_t>(D.Mmax * D.d);
+  M.h = L.take<bf16_t>(D.Mmax * D.Fp);
+  M.part = L.take<float>((size_t)kMaxSplits * kSkinnyRows * D.Nmax);
+  M.logits_pre = L.take<float>((size_t)D.Bmax * D.A);
+  M.logits_dec = L.take<float>((size_t)D.Bmax * D.A);
+  M.logits_tf = L.take<float>((size_t)D.Bmax * D.nact * D.A);
+  M.u_head = L.take<bf16_t>((size_t)D.Bmax * D.nact * D.d);
+  M.next_tok = L.take<int32_t>(D.Bmax);
+  M.flags = L.take<uint32_t>(4);
+  M.meta_dev = L.take<int32_t>(D.meta_ints);
+  L.off = align_up(L.off, 256);
+}
+
+size_t kv_region_bytes(const Dims& D, int n_layers) {
+  return align_up((size_t)D.n_pages * D.H * kPage * D.hd * sizeof(bf16_t), 256) * 2 * n_layers;
+}
+
+void set_meta_views(vla_model* m, int32_t* base) {
+  const Dims& D = m->D;
+  int32_t* p = base;
+  m->row_pos = p; p += D.Mmax;
+  m->row_env = p; p += D.Mmax;
+  m->env_row0 = p; p += D.Bmax;
+  m->env_len = p; p += D.Bmax;
+  m->env_prefix = p; p += D.Bmax;
+  m->env_prompt_off = p; p += D.Bmax;
+  m->page_table = p; p += (size_t)D.Bmax * D.max_pages;
+  m->qblocks = p; p += 2 * (size_t)D.qblk_max;
+  m->head_rows = p;
+}
+
+// Index of a view inside the meta block (same for host staging and device).
+template <class T>
+size_t meta_index(const vla_model* m, const T* view) {
+  return (size_t)(view - m->meta_dev);
+}
+
+RowMeta row_meta(const vla_model* m) { return RowMeta{m->row_pos, m->row_env, m->page_table, m->D.max_pages}; }
+
+constexpr int kProfSlots = 16384;
+
+// Start event of a profiled launch; returns the slot or -1 when not recorded.
+int prof_start(vla_model* m, int cat, hipStream_t s) {
+  if (!(m->prof_mask & (1u << cat)) || m->prof_used >= (int)m->prof.size()) return -1;
+  const int i = m->prof_used++;
+  m->prof[i].cat = cat;
+  m->prof[i].work = 0.0;
+  (void)hipEventRecord(m->prof[i].a, s);
+  return i;
+}
+
+void prof_stop(vla_model* m, int slot, double work, hipStream_t s) {
+  if (slot < 0) return;
+  m->prof[slot].work = work;
+  (void)hipEventRecord(m->prof[slot].b, s);
+}
+
+// Profiled launch wrapper: evaluates `launch` between the two events.
+#define PROF_LAUNCH(cat, work, launch)              \
+  do {                                              \
+    const int slot_ = prof_start(m, (cat), s);      \
+    VLA_CK(launch);                                 \
+    prof_stop(m, slot_, (work), s);                 \
+  } while (0)
+
+double gemm_flops(double M, double N, double K) { return 2.0 * M * N * K; }
+// algorithmic HBM bytes of a decode GEMM: the weights once plus the activations in
+double skinny_bytes(double N, double K, double M) { return 2.0 * N * K + 2.0 * M * K; }
+
+// Skinny GEMM over up to kSkinnyRows rows, followed by the logits reduction.
+int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t s) {
+  const Dims& D = m->D;
+  for (int r0 = 0; r0 < R; r0 += kSkinnyRows) {
+    const int rows = std::min(kSkinnyRows, R - r0);
+    SkinnyArgs sa{u + (size_t)r0 * D.d, D.d, rows, m->lm_act, D.Ap, D.d, m->part, 0};
+    sa.splits = skinny_splits(rows, D.Ap, D.d, kMaxSplits);
+    VLA_CK(launch_skinny(sa, s));
+    VLA_CK(launch_reduce_sum(m->part, sa.splits, logits + (size_t)r0 * D.A, rows, D.A, D.Ap, s));
+  }
+  return VLA_OK;
+}
+
+// Shared forward over a packed ragged batch: prefill (actions == nullptr) or
+// teacher-forced (each environment's rows extended by its action tokens).
+int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, const int32_t* lens_host,
+            const int32_t* actions, hipStream_t s, int* out_rows) {
+  const Dims& D = m->D;
+  const bool tf = actions != nullptr;
+  std::vector<int> prefix(B), rows(B);
+  size_t M = 0;
+  int nq = 0;
+  for (int b = 0; b < B; ++b) {
+    if (lens_host[b] < 0) return fail(VLA_EINVAL, "negative prompt length");
+    prefix[b] = D.nvis + lens_host[b];
+    if (prefix[b] < 1) return fail(VLA_EINVAL, "empty sequence (n_visual + prompt length == 0)");
+    if (prefix[b] + D.nact > D.Smax) return fail(VLA_ESHAPE, "n_visual + prompt + n_actions exceeds max_seq");
+    rows[b] = prefix[b] + (tf ? D.nact : 0);
+    M += rows[b];
+    nq += (rows[b] + kQBlock - 1) / kQBlock;
+  }
+  // host metadata -> pinned staging -> one async upload
+  if (m->meta_pending) {
+    VLA_CK(hipEventSynchronize(m->meta_event));
+    m->meta_pending = false;
+  }
+  int32_t* h = m->meta_host;
+  int32_t* hp = h + meta_index(m, m->row_pos);
+  int32_t* he = h + meta_index(m, m->row_env);
+  int32_t* hr0 = h + meta_index(m, m->env_row0);
+  int32_t* hl = h + meta_index(m, m->env_len);
+  int32_t* hpre = h + meta_index(m, m->env_prefix);
+  int32_t* hpo = h + meta_index(m, m->env_prompt_off);
+  int32_t* hpt = h + meta_index(m, m->page_table);
+  int32_t* hq = h + meta_index(m, m->qblocks);
+  int32_t* hh = h + meta_index(m, m->head_rows);
+  size_t r = 0;
+  int po = 0, qi = 0;
+  for (int b = 0; b < B; ++b) {
+    hr0[b] = (int32_t)r;
+    hl[b] = rows[b];
+    hpre[b] = prefix[b];
+    hpo[b] = po;
+    po += lens_host[b];
+    for (int t = 0; t < rows[b]; ++t, ++r) {
+      hp[r] = t;
+      he[r] = b;
+    }
+    // pages of env b are interleaved with the other environments' pages
+    const int np = (prefix[b] + D.nact + kPage - 1) / kPage;
+    for (int p = 0; p < D.max_pages; ++p) hpt[(size_t)b * D.max_pages + p] = p < np ? p * B + b : 0;
+    for (int q0 = 0; q0 < rows[b]; q0 += kQBlock, ++qi) {
+      hq[2 * qi] = b;
+      hq[2 * qi + 1] = q0;
+    }
+    if (tf) {
+      for (int i = 0; i < D.nact; ++i) hh[b * D.nact + i] = hr0[b] + prefix[b] - 1 + i;
+    } else {
+      hh[b] = hr0[b] + prefix[b] - 1;
+    }
+  }
+  VLA_CK(hipMemcpyAsync(m->meta_dev, m->meta_host, D.meta_ints * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  VLA_CK(hipEventRecord(m->meta_event, s));
+  m->meta_pending = true;
+
+  const int Mi = (int)M;
+  // causal attention flops of one layer: q.k and p.v over (t + 1) keys per row
+  double attn_flops = 0.0;
+  for (int b = 0; b < B; ++b) attn_flops += 2.0 * D.d * (double)rows[b] * (rows[b] + 1);
+  EmbedArgs ea{m->x, m->emb, static_cast<const bf16_t*>(vis), prompt_ids, actions, m->row_pos, m->row_env,
+               m->env_prefix, m->env_prompt_off, Mi, D.d, D.nvis, D.nact, D.V, m->flags};
+  VLA_CK(launch_embed(ea, s));
+  const float eps = m->cfg.rms_eps;
+  VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s));
+  for (int l = 0; l < D.L; ++l) {
+    const LayerW& w = m->lw[l];
+    GemmArgs g{};
+    g.A = m->u; g.lda = D.d; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
+    g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
+    g.d_model = D.d; g.n_heads = D.H; g.head_dim = D.hd;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 3.0 * D.d, D.d), launch_gemm(g, kEpiQkvRope, s));
+    PrefillAttnArgs pa{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, m->qblocks,
+                       nq, D.d, D.H, D.hd, m->scale};
+    PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, attn_flops, launch_attn_prefill(pa, s));
+    GemmArgs go{};
+    go.A = m->u; go.lda = D.d; go.W = w.wo; go.M = Mi; go.N = D.d; go.K = D.d; go.C = m->x; go.ldc = D.d;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.d), launch_gemm(go, kEpiResidual, s));
+    VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, w.mlp_norm, eps, m->u, D.d, Mi, D.d, s));
+    GemmArgs gg{};
+    gg.A = m->u; gg.lda = D.d; gg.W = w.wgu; gg.M = Mi; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = m->h; gg.ldh = D.Fp;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
+    GemmArgs gd{};
+    gd.A = m->h; gd.lda = D.Fp; gd.W = w.wd; gd.M = Mi; gd.N = D.d; gd.K = D.Fp; gd.C = m->x; gd.ldc = D.d;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
+    if (l + 1 < D.L) VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s));
+  }
+  const int R = tf ? B * D.nact : B;
+  VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s));
+  *out_rows = R;
+  return VLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vla_workspace_size(const vla_config* cfg, size_t* bytes) {
+  Dims D;
+  int rc = check_config(cfg, &D);
+  if (rc) return rc;
+  if (!bytes) return fail(VLA_EINVAL, "bytes_host is NULL");
+  Layout L;
+  plan(L, nullptr, D, cfg->n_layers);
+  *bytes = L.off;
+  return VLA_OK;
+}
+
+int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, size_t ws_bytes, void* stream,
+               vla_model** out) {
+  Dims D;
+  int rc = check_config(cfg, &D);
+  if (rc) return rc;
+  if (!w || !out || !workspace) return fail(VLA_EINVAL, "NULL weights, workspace or out");
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo ||
+      !w->mlp_norm || !w->wgate || !w->wup || !w->wdown)
+    return fail(VLA_EINVAL, "a weight pointer is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->mlp_norm[l] || !w->wgate[l] ||
+        !w->wup[l] || !w->wdown[l])
+      return fail(VLA_EINVAL, "a per-layer weight pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return fail(VLA_EWORKSPACE, "workspace not 256-byte aligned");
+  Layout L;
+  L.base = static_cast<char*>(workspace);
+  vla_model* m = new vla_model();
+  m->cfg = *cfg;
+  m->D = D;
+  plan(L, m, D, cfg->n_layers);
+  if (L.off > ws_bytes) {
+    delete m;
+    return fail(VLA_EWORKSPACE, "workspace smaller than vla_workspace_size()");
+  }
+  m->scale = 1.0f / std::sqrt((float)D.hd);
+  set_meta_views(m, m->meta_dev);
+  m->meta_pending = false;
+  m->state_batch = 0;
+  m->state_valid = false;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto cleanup = [&](int code) {
+    if (m->meta_host) (void)hipHostFree(m->meta_host);
+    delete m;
+    return code;
+  };
+  m->meta_host = nullptr;
+  if (hipHostMalloc(reinterpret_cast<void**>(&m->meta_host), D.meta_ints * sizeof(int32_t), hipHostMallocDefault) !=
+      hipSuccess)
+    return cleanup(fail(VLA_EHIP, "hipHostMalloc of the metadata staging buffer failed"));
+  std::memset(m->meta_host, 0, D.meta_ints * sizeof(int32_t));
+  if (hipEventCreateWithFlags(&m->meta_event, hipEventDisableTiming) != hipSuccess)
+    return cleanup(fail(VLA_EHIP, "hipEventCreate failed"));
+
+  auto ck = [&](hipError_t e, const char* what) -> int {
+    if (e == hipSuccess) return VLA_OK;
+    return fail(VLA_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+  };
+#define CREATE_CK(expr)                      \
+  do {                                       \
+    int r_ = ck((expr), #expr);              \
+    if (r_) {                                \
+      (void)hipEventDestroy(m->meta_event);  \
+      return cleanup(r_);                    \
+    }                                        \
+  } while (0)
+
+  const bf16_t* emb = static_cast<const bf16_t*>(w->embed);
+  const bf16_t* lm = static_cast<const bf16_t*>(w->lm_head);
+  CREATE_CK(hipMemcpyAsync(m->emb, emb, (size_t)D.V * D.d * 2, hipMemcpyDeviceToDevice, s));
+  CREATE_CK(launch_fill_zero(m->lm_act, align_up((size_t)D.Ap * D.d * 2, 16), s));
+  CREATE_CK(hipMemcpyAsync(m->lm_act, lm + (size_t)cfg->action_begin * D.d, (size_t)D.A * D.d * 2,
+                           hipMemcpyDeviceToDevice, s));
+  CREATE_CK(launch_bf16_to_f32(m->final_norm, static_cast<const bf16_t*>(w->final_norm), D.d, s));
+  for (int l = 0; l < D.L; ++l) {
+    LayerW& lw = m->lw[l];
+    CREATE_CK(launch_repack_qk(lw.wqkv, static_cast<const bf16_t*>(w->wq[l]), D.d, D.hd, s));
+    CREATE_CK(launch_repack_qk(lw.wqkv + (size_t)D.d * D.d, static_cast<const bf16_t*>(w->wk[l]), D.d, D.hd, s));
+    CREATE_CK(hipMemcpyAsync(lw.wqkv + (size_t)2 * D.d * D.d, w->wv[l], (size_t)D.d * D.d * 2,
+                             hipMemcpyDeviceToDevice, s));
+    CREATE_CK(hipMemcpyAsync(lw.wo, w->wo[l], (size_t)D.d * D.d * 2, hipMemcpyDeviceToDevice, s));
+    CREATE_CK(launch_repack_gate_up(lw.wgu, static_cast<const bf16_t*>(w->wgate[l]),
+                                    static_cast<const bf16_t*>(w->wup[l]), D.F, D.Fp, D.d, s));
+    CREATE_CK(launch_pad_cols(lw.wd, static_cast<const bf16_t*>(w->wdown[l]), D.d, D.F, D.Fp, s));
+    CREATE_CK(launch_bf16_to_f32(lw.attn_norm, static_cast<const bf16_t*>(w->attn_norm[l]), D.d, s));
+    CREATE_CK(launch_bf16_to_f32(lw.mlp_norm, static_cast<const bf16_t*>(w->mlp_norm[l]), D.d, s));
+  }
+  // zeroed KV pool: masked keys of a partly filled page then multiply finite values
+  CREATE_CK(launch_fill_zero(m->kv[0].k, kv_region_bytes(D, D.L), s));
+  CREATE_CK(launch_fill_zero(m->flags, 16, s));
+  // rotary table: angle = pos * base^(-2i/hd), evaluated in double precision
+  std::vector<float2> rope((size_t)D.Smax * (D.hd / 2));
+  for (int p = 0; p < D.Smax; ++p)
+    for (int i = 0; i < D.hd / 2; ++i) {
+      const double ang = (double)p * std::pow((double)cfg->rope_base, -2.0 * i / D.hd);
+      rope[(size_t)p * (D.hd / 2) + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+    }
+  CREATE_CK(hipMemcpyAsync(m->rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
+  CREATE_CK(hipStreamSynchronize(s));
+#undef CREATE_CK
+  *out = m;
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_prefill(vla_model* m, int32_t B, const void* vis, const int32_t* ids, const int32_t* lens_host,
+                float* logits, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (B < 0) return fail(VLA_EINVAL, "negative batch");
+  if (B > m->D.Bmax) return fail(VLA_ESHAPE, "batch > max_batch");
+  m->state_valid = false;
+  if (B == 0) {
+    m->state_batch = 0;
+    m->state_valid = true;
+    return VLA_OK;
+  }
+  if (!lens_host || !logits || (m->D.nvis > 0 && !vis)) return fail(VLA_EINVAL, "NULL argument");
+  long long np = 0;
+  for (int b = 0; b < B; ++b) np += lens_host[b];
+  if (np > 0 && !ids) return fail(VLA_EINVAL, "prompt_ids is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int R = 0;
+  int rc = forward(m, B, vis, ids, lens_host, nullptr, s, &R);
+  if (rc) return rc;
+  rc = head_logits(m, m->u_head, R, m->logits_pre, s);
+  if (rc) return rc;
+  VLA_CK(hipMemcpyAsync(logits, m->logits_pre, (size_t)B * m->D.A * sizeof(float), hipMemcpyDeviceToDevice, s));
+  m->prefix_host.assign(B, 0);
+  for (int b = 0; b < B; ++b) m->prefix_host[b] = m->D.nvis + lens_host[b];
+  m->state_batch = B;
+  m->state_valid = true;
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, int32_t* tokens, float* logp,
+                       float* entropy, float* step_logits, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (!m->state_valid || B != m->state_batch) return fail(VLA_ESTATE, "decode needs a prefill of the same batch");
+  if (B == 0) {
+    m->state_valid = false;
+    return VLA_OK;
+  }
+  if (!gumbel || !tokens || !logp) return fail(VLA_EINVAL, "NULL argument");
+  if (!(T > 0.f) || !std::isfinite(T)) return fail(VLA_EINVAL, "temperature must be finite and > 0");
+  const Dims& D = m->D;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  m->state_valid = false;
+  const float eps = m->cfg.rms_eps;
+  for (int i = 0; i < D.nact; ++i) {
+    const float* z = m->logits_pre;
+    if (i > 0) {
+      VLA_CK(launch_embed_token_norm(m->next_tok, m->emb, m->x, m->u, m->lw[0].attn_norm, eps, B, D.d, D.V, m->flags,
+                                     s));
+      // KV bytes read by one layer's decode attention at this step (K and V rows of every key)
+      double kv_bytes = 0.0;
+      for (int b = 0; b < B; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + i);
+      for (int l = 0; l < D.L; ++l) {
+        const LayerW& w = m->lw[l];
+        SkinnyArgs sq{m->u, D.d, B, w.wqkv, 3 * D.d, D.d, m->part, 0};
+        sq.splits = skinny_splits(B, sq.N, sq.K, kMaxSplits);
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, s));
+        DecodeQkvArgs qa{m->part, sq.splits, m->q, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, m->rope,
+                         B, D.d, D.H, D.hd};
+        VLA_CK(launch_decode_qkv(qa, s));
+        DecodeAttnArgs da{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, B, D.d, D.H, D.hd,
+                          m->scale};
+        PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
+        SkinnyArgs so{m->u, D.d, B, w.wo, D.d, D.d, m->part, 0};
+        so.splits = skinny_splits(B, so.N, so.K, kMaxSplits);
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, s));
+        VLA_CK(launch_reduce_residual_norm(m->part, so.splits, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
+        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part, 0};
+        sg.splits = skinny_splits(B, sg.N, sg.K, kMaxSplits);
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, s));
+        VLA_CK(launch_reduce_swiglu(m->part, sg.splits, m->h, D.Fp, B, D.Fp, s));
+        SkinnyArgs sd{m->h, D.Fp, B, w.wd, D.d, D.Fp, m->part, 0};
+        sd.splits = skinny_splits(B, sd.N, sd.K, kMaxSplits);
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, s));
+        const float* gnext = (l + 1 < D.L) ? m->lw[l + 1].attn_norm : m->final_norm;
+        VLA_CK(launch_reduce_residual_norm(m->part, sd.splits, m->x, m->u, gnext, eps, B, D.d, s));
+      }
+      int rc = head_logits(m, m->u, B, m->logits_dec, s);
+      if (rc) return rc;
+      z = m->logits_dec;
+    }
+    SamplerArgs sa{};
+    sa.z = z; sa.A = D.A; sa.temperature = T; sa.gumbel = gumbel; sa.step = i; sa.n_actions = D.nact;
+    sa.action_begin = m->cfg.action_begin; sa.tokens = tokens; sa.next_tok = m->next_tok; sa.logp = logp;
+    sa.entropy = entropy; sa.logits_out = step_logits; sa.rows = B; sa.flags = m->flags;
+    VLA_CK(launch_sampler(sa, s));
+  }
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_token_logprobs(vla_model* m, int32_t B, const void* vis, const int32_t* ids, const int32_t* lens_host,
+                       const int32_t* actions, float T, float* logp, float* entropy, float* logits, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (B < 0) return fail(VLA_EINVAL, "negative batch");
+  if (B > m->D.Bmax) return fail(VLA_ESHAPE, "batch > max_batch");
+  m->state_valid = false;
+  if (B == 0) return VLA_OK;
+  if (!lens_host || !actions || !logp || (m->D.nvis > 0 && !vis)) return fail(VLA_EINVAL, "NULL argument");
+  if (!(T > 0.f) || !std::isfinite(T)) return fail(VLA_EINVAL, "temperature must be finite and > 0");
+  long long np = 0;
+  for (int b = 0; b < B; ++b) np += lens_host[b];
+  if (np > 0 && !ids) return fail(VLA_EINVAL, "prompt_ids is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int R = 0;
+  int rc = forward(m, B, vis, ids, lens_host, actions, s, &R);
+  if (rc) return rc;
+  rc = head_logits(m, m->u_head, R, m->logits_tf, s);
+  if (rc) return rc;
+  SamplerArgs sa{};
+  sa.z = m->logits_tf; sa.A = m->D.A; sa.temperature = T; sa.gumbel = nullptr; sa.given = actions;
+  sa.action_begin = m->cfg.action_begin; sa.logp = logp; sa.entropy = entropy; sa.logits_out = logits; sa.rows = R;
+  sa.flags = m->flags;
+  VLA_CK(launch_sampler(sa, s));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_read_device_flags(vla_model* m, void* stream, uint32_t* flags_host) {
+  if (!m || !flags_host) return fail(VLA_EINVAL, "NULL argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint32_t v = 0;
+  VLA_CK(hipMemcpyAsync(&v, m->flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  VLA_CK(hipStreamSynchronize(s));
+  VLA_CK(launch_fill_zero(m->flags, 16, s));
+  VLA_CK(hipStreamSynchronize(s));
+  *flags_host = v;
+  return VLA_OK;
+}
+
+int vla_profile_begin(vla_model* m, uint32_t mask) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (m->prof.empty()) {
+    m->prof.resize(kProfSlots);
+    for (auto& p : m->prof) {
+      VLA_CK(hipEventCreate(&p.a));
+      VLA_CK(hipEventCreate(&p.b));
+    }
+  }
+  m->prof_used = 0;
+  m->prof_mask = mask;
+  return VLA_OK;
+}
+
+int vla_profile_end(vla_model* m, double* ms, double* work, int64_t* launches) {
+  if (!m || !ms || !work || !launches) return fail(VLA_EINVAL, "NULL argument");
+  for (int c = 0; c < VLA_PROF_CATEGORIES; ++c) {
+    ms[c] = 0.0;
+    work[c] = 0.0;
+    launches[c] = 0;
+  }
+  if (m->prof_used > 0) VLA_CK(hipEventSynchronize(m->prof[m->prof_used - 1].b));
+  for (int i = 0; i < m->prof_used; ++i) {
+    float t = 0.f;
+    VLA_CK(hipEventElapsedTime(&t, m->prof[i].a, m->prof[i].b));
+    const int c = m->prof[i].cat;
+    ms[c] += t;
+    work[c] += m->prof[i].work;
+    launches[c] += 1;
+  }
+  m->prof_used = 0;
+  m->prof_mask = 0;
+  return VLA_OK;
+}
+
+void vla_destroy(vla_model* m) {
+  if (!m) return;
+  for (auto& p : m->prof) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  if (m->meta_pending) (void)hipEventSynchronize(m->meta_event);
+  (void)hipEventDestroy(m->meta_event);
+  if (m->meta_host) (void)hipHostFree(m->meta_host);
+  delete m;
+}
+
+const char* vla_last_error(void) { return g_err.c_str(); }
+
+int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream) {
+  if (!m || !dst || layer < 0 || layer >= m->D.L) return fail(VLA_EINVAL, "bad argument");
+  const Dims& D = m->D;
+  const void* src = nullptr;
+  size_t avail = 0;
+  const size_t kv = (size_t)D.n_pages * D.H * kPage * D.hd * sizeof(bf16_t);
+  switch (which) {
+    case 0: src = m->x; avail = D.Mmax * D.d * sizeof(float); break;
+    case 1: src = m->q; avail = D.Mmax * D.d * sizeof(bf16_t); break;
+    case 2: src = m->kv[layer].k; avail = kv; break;
+    case 3: src = m->kv[layer].v; avail = kv; break;
+    case 4: src = m->u; avail = D.Mmax * D.d * sizeof(bf16_t); break;
+    default: return fail(VLA_EINVAL, "unknown buffer");
+  }
+  if (bytes > avail) return fail(VLA_EINVAL, "read larger than the buffer");
+  VLA_CK(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream)));
+  return VLA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,259 @@
+"""ctypes binding of ``libvla.so`` (argument marshalling only).
+
+Every step of the rollout path runs in the HIP library; this module only
+passes device pointers of torch tensors, the current HIP stream and host
+arrays through the C ABI of ``include/vla.h``.  Importing it fails loudly if
+the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvla.so")
+
+VLA_OK = 0
+STATUS = {-1: "VLA_EINVAL", -2: "VLA_ESHAPE", -3: "VLA_EWORKSPACE", -4: "VLA_EHIP", -6: "VLA_ESTATE",
+          -7: "VLA_EUNSUPPORTED"}
+FLAG_BAD_PROMPT_ID = 1
+FLAG_BAD_ACTION = 2
+
+EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
+           "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy", "vla_last_error")
+PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
+DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_sample", "vla_debug_read")
+
+
+class VlaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "d_model", "n_heads", "head_dim", "d_ffn", "vocab",
+                                              "action_bins", "action_begin", "n_actions", "n_visual")] + \
+               [("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float)] + \
+               [(n, ctypes.c_int32) for n in ("max_batch", "max_seq", "page_size")]
+
+
+_PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+class _Weights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p), ("final_norm", ctypes.c_void_p)] + \
+               [(n, _PP) for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wgate", "wup", "wdown")]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it is missing: there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    i32, vp, f32 = ctypes.c_int32, ctypes.c_void_p, ctypes.c_float
+    lib.vla_workspace_size.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(ctypes.c_size_t)]
+    lib.vla_create.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(_Weights), vp, ctypes.c_size_t, vp,
+                               ctypes.POINTER(vp)]
+    lib.vla_prefill.argtypes = [vp, i32, vp, vp, vp, vp, vp]
+    lib.vla_decode_actions.argtypes = [vp, i32, vp, f32, vp, vp, vp, vp, vp]
+    lib.vla_token_logprobs.argtypes = [vp, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp]
+    lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.vla_profile_begin.argtypes = [vp, ctypes.c_uint32]
+    lib.vla_profile_end.argtypes = [vp, vp, vp, vp]
+    lib.vla_destroy.argtypes = [vp]
+    lib.vla_destroy.restype = None
+    lib.vla_last_error.restype = ctypes.c_char_p
+    lib.vla_debug_gemm.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp]
+    lib.vla_debug_skinny.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
+    lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
+    lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
+    for name in EXPORTS + DEBUG_EXPORTS:
+        if name not in ("vla_destroy", "vla_last_error"):
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(code: int) -> None:
+    if code != VLA_OK:
+        raise VlaError(code, _lib.vla_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    return ctypes.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def make_config(cfg, max_batch: Optional[int] = None, max_seq: Optional[int] = None) -> _Config:
+    return _Config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ffn, cfg.vocab, cfg.action_bins,
+                   cfg.action_begin, cfg.n_actions, cfg.n_visual, cfg.rope_base, cfg.rms_eps,
+                   cfg.batch if max_batch is None else max_batch, cfg.max_seq if max_seq is None else max_seq,
+                   cfg.page_size)
+
+
+def workspace_bytes(cfg, max_batch: Optional[int] = None, max_seq: Optional[int] = None) -> int:
+    lib = load_library()
+    c = make_config(cfg, max_batch, max_seq)
+    n = ctypes.c_size_t()
+    _check(lib.vla_workspace_size(ctypes.byref(c), ctypes.byref(n)))
+    return n.value
+
+
+class VlaModel:
+    """A model handle over a caller-owned workspace (a torch uint8 tensor)."""
+
+    def __init__(self, cfg, weights: Dict[str, object], max_batch: Optional[int] = None,
+                 max_seq: Optional[int] = None, device="cuda"):
+        self.lib = load_library()
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.c_cfg = make_config(cfg, max_batch, max_seq)
+        n = ctypes.c_size_t()
+        _check(self.lib.vla_workspace_size(ctypes.byref(self.c_cfg), ctypes.byref(n)))
+        self.workspace = torch.empty(n.value, dtype=torch.uint8, device=self.device)
+        L = cfg.n_layers
+        arrays = {}
+        for k in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wgate", "wup", "wdown"):
+            arr = (ctypes.c_void_p * L)(*[_ptr(weights["layers"][i][k]).value for i in range(L)])
+            arrays[k] = arr
+        self._keep = arrays
+        w = _Weights(_ptr(weights["embed"]), _ptr(weights["lm_head"]), _ptr(weights["final_norm"]),
+                     *[ctypes.cast(arrays[k], _PP) for k in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm",
+                                                              "wgate", "wup", "wdown")])
+        h = ctypes.c_void_p()
+        _check(self.lib.vla_create(ctypes.byref(self.c_cfg), ctypes.byref(w), _ptr(self.workspace),
+                                   ctypes.c_size_t(n.value), _stream(self.device), ctypes.byref(h)))
+        self.handle = h
+
+    # --------------------------------------------------------------- rollout
+    def prefill(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
+                out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        lens = np.ascontiguousarray(prompt_lens, dtype=np.int32)
+        B = int(lens.shape[0])
+        if out is None:
+            out = torch.empty(B, self.cfg.action_bins, dtype=torch.float32, device=self.device)
+        _check(self.lib.vla_prefill(self.handle, B, _ptr(vis), _ptr(prompt_ids),
+                                    lens.ctypes.data_as(ctypes.c_void_p), _ptr(out), _stream(self.device)))
+        self._last_batch = B
+        return out
+
+    def decode_actions(self, gumbel: torch.Tensor, temperature: float, batch: Optional[int] = None,
+                       with_logits: bool = True, out: Optional[Dict[str, torch.Tensor]] = None
+                       ) -> Dict[str, torch.Tensor]:
+        B = self._last_batch if batch is None else batch
+        na, A = self.cfg.n_actions, self.cfg.action_bins
+        if out is None:
+            out = {"tokens": torch.empty(B, na, dtype=torch.int32, device=self.device),
+                   "logp": torch.empty(B, na, dtype=torch.float32, device=self.device),
+                   "entropy": torch.empty(B, na, dtype=torch.float32, device=self.device)}
+            if with_logits:
+                out["logits"] = torch.empty(B, na, A, dtype=torch.float32, device=self.device)
+        _check(self.lib.vla_decode_actions(self.handle, B, _ptr(gumbel), float(temperature), _ptr(out["tokens"]),
+                                           _ptr(out["logp"]), _ptr(out.get("entropy")), _ptr(out.get("logits")),
+                                           _stream(self.device)))
+        return out
+
+    def token_logprobs(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
+                       actions: torch.Tensor, temperature: float, with_logits: bool = True
+                       ) -> Dict[str, torch.Tensor]:
+        lens = np.ascontiguousarray(prompt_lens, dtype=np.int32)
+        B = int(lens.shape[0])
+        na, A = self.cfg.n_actions, self.cfg.action_bins
+        out = {"logp": torch.empty(B, na, dtype=torch.float32, device=self.device),
+               "entropy": torch.empty(B, na, dtype=torch.float32, device=self.device)}
+        if with_logits:
+            out["logits"] = torch.empty(B, na, A, dtype=torch.float32, device=self.device)
+        _check(self.lib.vla_token_logprobs(self.handle, B, _ptr(vis), _ptr(prompt_ids),
+                                           lens.ctypes.data_as(ctypes.c_void_p), _ptr(actions), float(temperature),
+                                           _ptr(out["logp"]), _ptr(out["entropy"]), _ptr(out.get("logits")),
+                                           _stream(self.device)))
+        return out
+
+    def read_flags(self) -> int:
+        v = ctypes.c_uint32()
+        _check(self.lib.vla_read_device_flags(self.handle, _stream(self.device), ctypes.byref(v)))
+        return v.value
+
+    def profile_begin(self, categories=PROF_CATEGORIES) -> None:
+        mask = 0
+        for c in categories:
+            mask |= 1 << PROF_CATEGORIES.index(c)
+        _check(self.lib.vla_profile_begin(self.handle, mask))
+
+    def profile_end(self) -> Dict[str, dict]:
+        """Per category: summed kernel ms, summed algorithmic work (flops or
+        bytes) and launch count of the launches recorded since profile_begin."""
+        n = len(PROF_CATEGORIES)
+        ms, work = (ctypes.c_double * n)(), (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check(self.lib.vla_profile_end(self.handle, ms, work, cnt))
+        return {c: {"ms": ms[i], "work": work[i], "launches": int(cnt[i])} for i, c in enumerate(PROF_CATEGORIES)}
+
+    def debug_read(self, which: int, layer: int, out: torch.Tensor) -> torch.Tensor:
+        _check(self.lib.vla_debug_read(self.handle, which, layer, _ptr(out), out.numel() * out.element_size(),
+                                       _stream(self.device)))
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            torch.cuda.current_stream(self.device).synchronize()
+            self.lib.vla_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------------------ test hooks
+def debug_gemm(A: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
+    lib = load_library()
+    M, K = A.shape
+    N = W.shape[0]
+    C = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    _check(lib.vla_debug_gemm(_ptr(A), K, _ptr(W), M, N, K, _ptr(C), _stream(A.device)))
+    return C
+
+
+def debug_skinny(A: torch.Tensor, W: torch.Tensor, splits: int) -> torch.Tensor:
+    lib = load_library()
+    M, K = A.shape
+    N = W.shape[0]
+    scratch = torch.empty(splits * M * N, dtype=torch.float32, device=A.device)
+    C = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    _check(lib.vla_debug_skinny(_ptr(A), K, _ptr(W), M, N, K, splits, _ptr(scratch), _ptr(C), _stream(A.device)))
+    return C
+
+
+def debug_sample(z: torch.Tensor, gumbel: torch.Tensor, step: int, temperature: float, action_begin: int):
+    lib = load_library()
+    B, A = z.shape
+    na = gumbel.shape[1]
+    dev = z.device
+    tokens = torch.full((B, na), -1, dtype=torch.int32, device=dev)
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    logp = torch.full((B, na), float("nan"), dtype=torch.float32, device=dev)
+    ent = torch.full((B, na), float("nan"), dtype=torch.float32, device=dev)
+    logits = torch.zeros(B, na, A, dtype=torch.float32, device=dev)
+    _check(lib.vla_debug_sample(_ptr(z), B, A, na, step, action_begin, _ptr(gumbel), float(temperature),
+                                _ptr(tokens), _ptr(nxt), _ptr(logp), _ptr(ent), _ptr(logits), _stream(dev)))
+    return {"tokens": tokens, "next": nxt, "logp": logp, "entropy": ent, "logits": logits}

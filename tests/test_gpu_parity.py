@@ -1,0 +1,161 @@
+"""End-to-end parity of the HIP rollout path with the CPU oracle on the same
+seeded inputs: prefill logits, KV-cached action decode (tokens, log-probs,
+entropies, per-step logits) and the teacher-forced pass, plus the invariants
+that need no oracle (batch-composition invariance, determinism, decode ==
+teacher-forced forward)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import LOGIT_TOL, LOGP_TOL, Setup, compare_rollout, log
+from paper_2505_18719_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+# tiny decoder with ragged prompts (0 .. 40 tokens) so one pass spans several
+# tiles and a ragged tail
+TINY_RAGGED = inputs.TINY.replace(name="tiny_ragged", batch=5, prompt_min=0, prompt_max=40)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Setup(inputs.TINY, seed=0)
+
+
+@pytest.fixture(scope="module")
+def tiny_ragged():
+    return Setup(TINY_RAGGED, seed=1, gain_jitter=True)
+
+
+def _rollout(S, inp, dev, T):
+    m = S.model
+    z0 = m.prefill(dev["vis"], dev["ids"], inp.prompt_lens)
+    out = m.decode_actions(dev["gumbel"], T)
+    torch.cuda.synchronize()
+    return z0, out
+
+
+@pytest.mark.parametrize("T", [1.0, 1.5])
+def test_tiny_rollout_matches_oracle(tiny, T):
+    inp, dev = tiny.inputs(seed=0)
+    z0, out = _rollout(tiny, inp, dev, T)
+    st = compare_rollout(tiny.cfg, tiny.W, inp, out, T, label=f"tiny T={T}")
+    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["dent"] <= LOGP_TOL
+    assert st["mismatches"] == 0
+    np.testing.assert_array_equal(z0.cpu().numpy(), out["logits"][:, 0].cpu().numpy())
+    toks = out["tokens"].cpu().numpy()
+    assert ((toks >= tiny.cfg.action_begin) & (toks < tiny.cfg.vocab)).all()
+    ideal = compare_rollout(tiny.cfg, tiny.W, inp, out, T, mode="ideal", label=f"tiny T={T}")
+    assert ideal["dlogit"] <= LOGIT_TOL and ideal["dlogp"] <= LOGP_TOL
+
+
+def test_ragged_prompts_with_gains_match_oracle(tiny_ragged):
+    S = tiny_ragged
+    inp, dev = S.inputs(seed=3, prompt_lens=[0, 40, 7, 33, 16])
+    z0, out = _rollout(S, inp, dev, 1.5)
+    st = compare_rollout(S.cfg, S.W, inp, out, 1.5, label="tiny ragged")
+    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
+
+
+def test_teacher_forced_matches_oracle_and_decode(tiny_ragged):
+    S = tiny_ragged
+    inp, dev = S.inputs(seed=4, prompt_lens=[3, 40, 0, 21, 9])
+    _, out = _rollout(S, inp, dev, 1.5)
+    acts = out["tokens"].clone()
+    tf = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, 1.5)
+    torch.cuda.synchronize()
+    ref = oracle.teacher_forced(S.cfg, S.W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens,
+                                acts.cpu().numpy(), 1.5)
+    dl = np.abs(tf["logits"].cpu().numpy() - ref["logits"]).max()
+    dp = np.abs(tf["logp"].cpu().numpy() - ref["logp"]).max()
+    log(f"[teacher-forced] max|dlogit|={dl:.3e} max|dlogp|={dp:.3e}")
+    assert dl <= LOGIT_TOL and dp <= LOGP_TOL
+    # PPO ratio of Eq. 2 at theta = theta_old: the teacher-forced pass and the
+    # rollout score the same tokens alike
+    ratio = torch.exp(tf["logp"].sum(1) - out["logp"].sum(1)).cpu().numpy()
+    dd = np.abs(tf["logits"].cpu().numpy() - out["logits"].cpu().numpy()).max()
+    log(f"[decode vs teacher-forced on GPU] max|dlogit|={dd:.3e} ratio range=({ratio.min():.6f}, {ratio.max():.6f})")
+    assert dd <= 1e-2 and np.abs(ratio - 1).max() <= 1e-2
+
+
+def test_teacher_forced_random_actions(tiny):
+    inp, dev = tiny.inputs(seed=5)
+    acts = inputs.stored_actions(tiny.cfg, inp.batch, seed=5)
+    tf = tiny.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, torch.from_numpy(acts).cuda(), 1.0)
+    torch.cuda.synchronize()
+    ref = oracle.teacher_forced(tiny.cfg, tiny.W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, acts, 1.0)
+    dp = np.abs(tf["logp"].cpu().numpy() - ref["logp"]).max()
+    de = np.abs(tf["entropy"].cpu().numpy() - ref["entropy"]).max()
+    log(f"[teacher-forced stored actions] max|dlogp|={dp:.3e} max|dH|={de:.3e}")
+    assert dp <= LOGP_TOL and de <= LOGP_TOL
+
+
+def test_batch_composition_invariance_and_determinism(tiny_ragged):
+    """An environment decodes bit-identically alone and inside a ragged batch
+    (the large-batch failure that motivates batch decoding), and runs repeat
+    bit-exactly."""
+    S = tiny_ragged
+    inp, dev = S.inputs(seed=6, prompt_lens=[12, 0, 40, 5, 27])
+    _, full = _rollout(S, inp, dev, 1.5)
+    full = {k: v.clone() for k, v in full.items()}
+    _, again = _rollout(S, inp, dev, 1.5)
+    for k in full:
+        assert torch.equal(full[k], again[k]), k
+    b = 2
+    off = int(inp.prompt_lens[:b].sum())
+    ids1 = dev["ids"][off:off + int(inp.prompt_lens[b])].contiguous()
+    S.model.prefill(dev["vis"][b:b + 1].contiguous(), ids1, inp.prompt_lens[b:b + 1])
+    one = S.model.decode_actions(dev["gumbel"][b:b + 1].contiguous(), 1.5)
+    torch.cuda.synchronize()
+    for k in full:
+        assert torch.equal(one[k][0], full[k][b]), k
+
+
+def test_edge_cases_and_errors(tiny):
+    from paper_2505_18719_amd.vla import VlaError
+    m = tiny.model
+    inp, dev = tiny.inputs(seed=7)
+    # decode without a prefill of the same batch
+    m.prefill(dev["vis"], dev["ids"], inp.prompt_lens)
+    with pytest.raises(VlaError, match="VLA_ESTATE"):
+        m.decode_actions(dev["gumbel"][:2].contiguous(), 1.0, batch=2)
+    # batch larger than max_batch
+    big = np.full(tiny.cfg.batch + 1, 4, dtype=np.int32)
+    with pytest.raises(VlaError, match="VLA_ESHAPE"):
+        m.prefill(dev["vis"], dev["ids"], big)
+    # prompt too long for max_seq
+    with pytest.raises(VlaError, match="VLA_ESHAPE"):
+        m.prefill(dev["vis"], dev["ids"], np.array([100, 1, 1, 1], dtype=np.int32))
+    # empty batch is a no-op
+    z = m.prefill(dev["vis"], dev["ids"], np.zeros(0, dtype=np.int32))
+    assert z.shape == (0, tiny.cfg.action_bins)
+    # out-of-range prompt id: flagged, zero embedding row, no fault
+    bad = dev["ids"].clone()
+    bad[3] = tiny.cfg.vocab + 5
+    m.prefill(dev["vis"], bad, inp.prompt_lens)
+    assert m.read_flags() & 1
+    assert m.read_flags() == 0
+    # action token outside the action bins in the teacher-forced pass -> NaN + flag
+    acts = torch.full((inp.batch, tiny.cfg.n_actions), tiny.cfg.action_begin, dtype=torch.int32, device="cuda")
+    acts[1, 4] = 5
+    tf = m.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, 1.0)
+    assert torch.isnan(tf["logp"][1, 4]).item() and not torch.isnan(tf["logp"][0]).any().item()
+    assert m.read_flags() & 2
+    with pytest.raises(VlaError, match="VLA_EINVAL"):
+        m.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, 0.0)
+
+
+def test_mid_rollout_and_teacher_forced_match_oracle():
+    """Mid decoder (8 layers, d 1024, batch 16): 7-token decode plus the
+    teacher-forced pass over the full 295-token sequences."""
+    S = Setup(inputs.MID, seed=0)
+    inp, dev = S.inputs(seed=0)
+    z0, out = _rollout(S, inp, dev, 1.5)
+    st = compare_rollout(S.cfg, S.W, inp, out, 1.5, label="mid")
+    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
+    tf = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, out["tokens"].clone(), 1.5)
+    torch.cuda.synchronize()
+    dd = np.abs(tf["logp"].cpu().numpy() - st["ref"]["logp"]).max()
+    log(f"[mid teacher-forced] max|dlogp| vs oracle={dd:.3e}")
+    assert dd <= LOGP_TOL

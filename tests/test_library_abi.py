@@ -1,0 +1,74 @@
+"""Host-side checks of the C-ABI library (no GPU needed): it loads, exports
+every function its headers declare, and validates configurations and
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2505_18719_amd import inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def vla():
+    from paper_2505_18719_amd import vla as binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2505_18719_amd import build
+        build.build(verbose=False)
+    binding.load_library()
+    return binding
+
+
+def _declared_functions():
+    names = set()
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            txt = open(os.path.join(ROOT, "include", f)).read()
+            names |= set(re.findall(r"^(?:int|void|const char\*|size_t)\s+(vla_\w+)\(", txt, re.M))
+    return sorted(names)
+
+
+def test_headers_declare_the_rollout_entry_points():
+    names = _declared_functions()
+    for n in ("vla_prefill", "vla_decode_actions", "vla_token_logprobs", "vla_create", "vla_workspace_size",
+              "vla_destroy", "vla_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(vla):
+    lib = vla.load_library()
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_workspace_size_and_config_validation(vla):
+    lib = vla.load_library()
+    n = ctypes.c_size_t()
+    c = vla.make_config(inputs.L7B_B64, max_batch=64)
+    assert lib.vla_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0
+    # repacked weights (~13.2 GB incl. embedding) + KV pool for 64 x 320 tokens (~10.7 GB) + activations
+    assert 20e9 < n.value < 40e9
+    bad = [dict(head_dim_override=96), dict(max_seq=400), dict(action_bins=300), dict(max_batch=0),
+           dict(n_actions=0), dict(page_size=8)]
+    for b in bad:
+        c = vla.make_config(inputs.TINY)
+        for k, v in b.items():
+            setattr(c, "head_dim" if k == "head_dim_override" else k, v)
+        rc = lib.vla_workspace_size(ctypes.byref(c), ctypes.byref(n))
+        assert rc in (-1, -7), (b, rc)
+        assert lib.vla_last_error().decode()
+    assert lib.vla_workspace_size(None, ctypes.byref(n)) == -1
+
+
+def test_create_rejects_null_arguments_before_device_work(vla):
+    lib = vla.load_library()
+    c = vla.make_config(inputs.TINY)
+    h = ctypes.c_void_p()
+    assert lib.vla_create(ctypes.byref(c), None, None, 0, None, ctypes.byref(h)) == -1
+    assert "NULL" in lib.vla_last_error().decode()
+    assert lib.vla_prefill(None, 1, None, None, None, None, None) == -1
+    assert lib.vla_decode_actions(None, 1, None, 1.0, None, None, None, None, None) == -1
+    lib.vla_destroy(None)
