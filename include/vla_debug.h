@@ -37,6 +37,11 @@ int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, in
 struct vla_model;
 int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream);
 
+/* Make later prefill / teacher-forced passes run only the first `n_layers`
+ * decoder layers (0 restores all), so that the residual after any layer can
+ * be read with vla_debug_read for layer-by-layer parity. */
+int vla_debug_set_layer_limit(struct vla_model* m, int32_t n_layers);
+
 #ifdef __cplusplus
 }
 #endif

@@ -142,6 +142,7 @@ struct vla_model {
   int state_batch;
   bool state_valid;
   std::vector<int> prefix_host;  // L_b of the last prefill
+  int layer_limit;               // test hook: run only the first layer_limit layers (0 = all)
   float scale;
   // live profiling
   struct ProfSlot {
@@ -334,7 +335,8 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   VLA_CK(launch_embed(ea, s));
   const float eps = m->cfg.rms_eps;
   VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s));
-  for (int l = 0; l < D.L; ++l) {
+  const int n_layers = m->layer_limit > 0 ? std::min(m->layer_limit, D.L) : D.L;
+  for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     GemmArgs g{};
     g.A = m->u; g.lda = D.d; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
@@ -649,6 +651,12 @@ void vla_destroy(vla_model* m) {
 }
 
 const char* vla_last_error(void) { return g_err.c_str(); }
+
+int vla_debug_set_layer_limit(vla_model* m, int32_t n_layers) {
+  if (!m || n_layers < 0) return fail(VLA_EINVAL, "bad argument");
+  m->layer_limit = n_layers;
+  return VLA_OK;
+}
 
 int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream) {
   if (!m || !dst || layer < 0 || layer >= m->D.L) return fail(VLA_EINVAL, "bad argument");

@@ -25,7 +25,8 @@ FLAG_BAD_ACTION = 2
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
            "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy", "vla_last_error")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
-DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_sample", "vla_debug_read")
+DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_sample", "vla_debug_read",
+                 "vla_debug_set_layer_limit")
 
 
 class VlaError(RuntimeError):
@@ -77,6 +78,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_debug_skinny.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
     lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
     lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
+    lib.vla_debug_set_layer_limit.argtypes = [vp, i32]
     for name in EXPORTS + DEBUG_EXPORTS:
         if name not in ("vla_destroy", "vla_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -210,6 +212,9 @@ class VlaModel:
         _check(self.lib.vla_debug_read(self.handle, which, layer, _ptr(out), out.numel() * out.element_size(),
                                        _stream(self.device)))
         return out
+
+    def debug_layer_limit(self, n_layers: int) -> None:
+        _check(self.lib.vla_debug_set_layer_limit(self.handle, n_layers))
 
     def close(self) -> None:
         if getattr(self, "handle", None):
