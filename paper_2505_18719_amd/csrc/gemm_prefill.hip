@@ -2,14 +2,17 @@
 // fp32 accumulation, with fused epilogues (residual add, SwiGLU, RoPE + paged
 // KV append).
 //
-// Tiling: a 512-thread workgroup (8 wave64s, 2 per SIMD) owns a 256 x 256
-// output tile; each wave owns 128 x 64 of it as 4 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16.  K advances in steps of 64 through a two-stage
-// LDS ring (2 x 64 KB) whose 16-byte chunks are XOR-swizzled by row so that
-// the MFMA operand reads (ds_read_b128, 32 rows x one chunk column) are
-// bank-conflict free.  Workgroup ids are remapped so that the tiles one XCD
-// runs are contiguous in a grouped (8 tile-rows) order, which keeps A panels
-// and W panels resident in that XCD's L2.
+// Tiling: a 256-thread workgroup (4 wave64s, one per SIMD) owns a 256 x 256
+// output tile; each wave owns 128 x 128 of it as 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane, held in AGPRs),
+// which halves the LDS operand traffic per MFMA compared with 128 x 64 wave
+// tiles.  K advances in steps of 64 through two LDS stages of 64 KB filled by
+// direct global -> LDS loads (global_load_lds_dwordx4, no VGPR round trip),
+// issued one stage ahead of the MFMAs that consume the other.  16-byte chunks
+// are XOR-swizzled by row so that the MFMA operand reads (ds_read_b128, 32
+// rows x one chunk column) spread over the LDS banks.  Workgroup ids are
+// remapped so that the tiles one XCD runs are contiguous in a grouped (8
+// tile-rows) order, which keeps A panels and W panels resident in that XCD's L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -18,9 +21,12 @@ namespace vla {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 512;
-constexpr int CH = BK / 8;  // 16-byte chunks per tile row
+constexpr int NT = 256;       // 4 waves, 2 x 2, each owning 128 x 128 of the tile
+constexpr int CH = BK / 8;    // 16-byte chunks per tile row
 constexpr int GROUP_M = 8;
+
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+typedef __attribute__((address_space(1))) const void gbl_ptr_t;
 
 __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_n, int& tm, int& tn) {
   // XCD-aware remap: the hardware deals workgroups round-robin to 8 XCDs.
@@ -36,165 +42,216 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
   tn = r / gm;
 }
 
+// Direct global -> LDS copy of 16 bytes per lane; lane i of the wave writes
+// bytes [16 i, 16 i + 16) after the wave-uniform LDS base.
+__device__ __forceinline__ void g2lds16(const bf16_t* g, uint4* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((gbl_ptr_t*)g, (lds_ptr_t*)lds_wave_base, 16, 0, 0);
+}
+
+// Each wave copies 8 blocks of 8 rows x 128 bytes of the A tile and of the W
+// tile.  Lane i of a block covers row 8b + i/8 and stores physical chunk i%8,
+// which holds logical K chunk (i%8) ^ (row%8): the XOR swizzle that makes the
+// 32-row MFMA operand reads conflict free.
+struct Loader {
+  const bf16_t* a;
+  const bf16_t* w;
+  int aoff[8], woff[8];  // element offsets of this lane's rows (rows clamped to M-1 / N-1)
+};
+
+__device__ __forceinline__ void issue_tile(const Loader& ld, int k0, uint4* sa, uint4* sw, int wave) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int blk = wave * 8 + j;
+    g2lds16(ld.a + ld.aoff[j] + k0, sa + blk * 64);
+    g2lds16(ld.w + ld.woff[j] + k0, sw + blk * 64);
+  }
+}
+
+__device__ __forceinline__ void load_frags(const uint4* sa, const uint4* sw, int ks, int wm, int wn, int lane,
+                                           bf16x8 (&af)[4], bf16x8 (&bw)[4]) {
+  const int l31 = lane & 31, c = 2 * ks + (lane >> 5);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wm * 128 + i * 32 + l31;
+    af[i] = as_bf16x8(sa[row * CH + (c ^ (row & 7))]);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = wn * 128 + j * 32 + l31;
+    bw[j] = as_bf16x8(sw[row * CH + (c ^ (row & 7))]);
+  }
+}
+
+// 4 k-steps of 16 on one LDS stage; the operand fragments of k-step ks+1 are
+// read while the 16 MFMAs of k-step ks run.
+__device__ __forceinline__ void compute_tile(const uint4* sa, const uint4* sw, f32x16 (&acc)[4][4], int wm, int wn,
+                                             int lane) {
+  bf16x8 af[2][4], bw[2][4];
+  load_frags(sa, sw, 0, wm, wn, lane, af[0], bw[0]);
+#pragma unroll
+  for (int ks = 0; ks < BK / 16; ++ks) {
+    if (ks + 1 < BK / 16) load_frags(sa, sw, ks + 1, wm, wn, lane, af[(ks + 1) & 1], bw[(ks + 1) & 1]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[ks & 1][i], bw[ks & 1][j], acc[i][j]);
+  }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds[2][2][BM * CH];
+  __shared__ uint4 lds[2][2][BM * CH];  // [stage][A / W][256 rows x 8 chunks]
 
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int M = a.M, N = a.N, K = a.K;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 1, wn = wave & 1;
 
-  // global -> LDS assignment: 4 passes of 64 rows, 8 threads per 128-byte row
-  const int lrow = tid >> 3, lchunk = tid & 7;
-  const bf16_t* ag[4];
-  const bf16_t* wg[4];
-  int so[4];
+  Loader ld;
+  ld.a = a.A;
+  ld.w = a.W;
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int r = p * 64 + lrow;
-    ag[p] = a.A + (size_t)min(m0 + r, M - 1) * a.lda + lchunk * 8;
-    wg[p] = a.W + (size_t)min(n0 + r, N - 1) * K + lchunk * 8;
-    so[p] = r * CH + (lchunk ^ (r & 7));
+  for (int j = 0; j < 8; ++j) {
+    const int row = (wave * 8 + j) * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ (lane >> 3);
+    ld.aoff[j] = min(m0 + row, M - 1) * a.lda + chunk * 8;
+    ld.woff[j] = min(n0 + row, N - 1) * K + chunk * 8;
   }
 
-  uint4 ra[4], rb[4];
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    ra[p] = *reinterpret_cast<const uint4*>(ag[p]);
-    rb[p] = *reinterpret_cast<const uint4*>(wg[p]);
-  }
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    lds[0][0][so[p]] = ra[p];
-    lds[0][1][so[p]] = rb[p];
-  }
-  __syncthreads();
-
-  f32x16 acc[4][2];
+  f32x16 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = K / BK;
-  const int l31 = lane & 31, lhi = lane >> 5;
+  issue_tile(ld, 0, lds[0][0], lds[0][1], wave);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int koff = (kt + 1) * BK;
+    // copy the next K step into the other stage (the last iteration re-copies
+    // its own step into the unused stage, keeping the body one basic block)
+    issue_tile(ld, min(kt + 1, nk - 1) * BK, lds[cur ^ 1][0], lds[cur ^ 1][1], wave);
+    compute_tile(lds[cur][0], lds[cur][1], acc, wm, wn, lane);
+    // schedule: the 16 copies first, the first k-step's 8 operand reads, then
+    // one operand read of the next k-step per two MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        ra[p] = *reinterpret_cast<const uint4*>(ag[p] + koff);
-        rb[p] = *reinterpret_cast<const uint4*>(wg[p] + koff);
-      }
+    for (int t = 0; t < 24; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int c = 2 * ks + lhi;
-      bf16x8 af[4], bw[2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + i * 32 + l31;
-        af[i] = as_bf16x8(lds[cur][0][row * CH + (c ^ (row & 7))]);
-      }
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = wn * 64 + j * 32 + l31;
-        bw[j] = as_bf16x8(lds[cur][1][row * CH + (c ^ (row & 7))]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(af[i], bw[j], acc[i][j]);
-    }
-    if (more) {
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        lds[cur ^ 1][0][so[p]] = ra[p];
-        lds[cur ^ 1][1][so[p]] = rb[p];
-      }
-    }
-    __syncthreads();
+    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the next stage have landed
+    __syncthreads();                 // ... and everyone's; the current stage is free again
   }
 
   // ---------------------------------------------------------------- epilogue
-  // acc[i][j][r] holds row wm*128 + i*32 + 8*(r/4) + 4*lhi + r%4 and column
-  // wn*64 + j*32 + l31 of the tile.
-  const int c0 = n0 + wn * 64;
-  if (c0 >= N) return;
-  if constexpr (EPI == kEpiStoreF32 || EPI == kEpiResidual) {
+  // The LDS stages are free after the last barrier; each wave stages its
+  // 128 x 128 accumulator tile through its own 32 KB of them, 64 columns at a
+  // time, and then writes the epilogue's outputs with contiguous stores.
+  // acc[i][j][r] holds row i*32 + 8*(r/4) + 4*lhi + r%4 and column j*32 + l31
+  // of the wave tile; in LDS the float4 chunk q of row rl sits at q ^ (rl%16).
+  float* st = reinterpret_cast<float*>(lds[wave >> 1][wave & 1]);
+  const int l31 = lane & 31, lhi = lane >> 5;
+  const int wrow0 = m0 + wm * 128;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int c0 = n0 + wn * 128 + h * 64;   // first column of this 64-column group
+    if (c0 >= N) break;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
-        if (row >= M) continue;
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = c0 + j * 32 + l31;
-          if (col >= N) continue;
-          float* p = a.C + (size_t)row * a.ldc + col;
-          if constexpr (EPI == kEpiResidual) *p += acc[i][j][r];
-          else *p = acc[i][j][r];
+        for (int r = 0; r < 16; ++r) {
+          const int rl = i * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+          const int cl = jj * 32 + l31;
+          st[rl * 64 + (((cl >> 2) ^ (rl & 15)) << 2) + (cl & 3)] = acc[i][2 * h + jj][r];
         }
-      }
-  } else if constexpr (EPI == kEpiSwiGlu) {
-    // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
-    const int jj = c0 / 2 + l31;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
-        if (row >= M) continue;
-        const float g = acc[i][0][r], u = acc[i][1][r];
-        a.H[(size_t)row * a.ldh + jj] = f2bf(g / (1.f + expf(-g)) * u);
-      }
-  } else {  // kEpiQkvRope
-    const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
-    const int region = c0 / d;
-    const int cc0 = c0 - region * d;
-    const int head = cc0 / hd;
-    const int blk = (cc0 % hd) / 64;
-    // q and k rows were permuted per head so that columns c and c+32 of this
-    // 64-column block are the rotary pair (32*blk + c, half + 32*blk + c).
-    const int ai = 32 * blk + l31;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
-        if (row >= M) continue;
-        const int pos = a.meta.row_pos[row];
-        const float x1 = acc[i][0][r], x2 = acc[i][1][r];
-        if (region == 0) {
-          const float2 cs = a.rope[pos * half + ai];
-          bf16_t* qr = a.q + (size_t)row * a.ldq + head * hd;
-          qr[ai] = f2bf(x1 * cs.x - x2 * cs.y);
-          qr[half + ai] = f2bf(x1 * cs.y + x2 * cs.x);
-        } else {
-          const int env = a.meta.row_env[row];
-          const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
-          const int slot = pos % kPage;
-          if (region == 1) {
-            const float2 cs = a.rope[pos * half + ai];
-            bf16_t* kr = a.kv.k + (((size_t)page * H + head) * kPage + slot) * hd;
-            kr[ai] = f2bf(x1 * cs.x - x2 * cs.y);
-            kr[half + ai] = f2bf(x1 * cs.y + x2 * cs.x);
+    __builtin_amdgcn_s_waitcnt(0);
+    if constexpr (EPI == kEpiStoreF32 || EPI == kEpiResidual) {
+      const int q = lane & 15;
+      for (int it = 0; it < 32; ++it) {
+        const int rl = it * 4 + (lane >> 4);
+        const int row = wrow0 + rl;
+        const float4 v = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
+        if (row < M) {
+          float4* p = reinterpret_cast<float4*>(a.C + (size_t)row * a.ldc + c0 + 4 * q);
+          if constexpr (EPI == kEpiResidual) {
+            const float4 o = *p;
+            *p = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
           } else {
-            const int i1 = cc0 % hd + l31;
-            bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + slot;
-            vb[(size_t)i1 * kPage] = f2bf(x1);
-            vb[(size_t)(i1 + 32) * kPage] = f2bf(x2);
+            *p = v;
           }
         }
       }
+    } else {
+      // pair epilogues: chunk q (< 8) of the group pairs with chunk q + 8
+      const int q = lane & 7;
+      for (int it = 0; it < 16; ++it) {
+        const int rl = it * 8 + (lane >> 3);
+        const int row = wrow0 + rl;
+        const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
+        const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
+        if (row >= M) continue;
+        const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
+        if constexpr (EPI == kEpiSwiGlu) {
+          // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
+          float o[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
+          *reinterpret_cast<uint2*>(a.H + (size_t)row * a.ldh + c0 / 2 + 4 * q) =
+              make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
+        } else {  // kEpiQkvRope
+          const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
+          const int region = c0 / d;
+          const int cc0 = c0 - region * d;
+          const int head = cc0 / hd;
+          const int blk = (cc0 % hd) / 64;
+          const int pos = a.meta.row_pos[row];
+          if (region < 2) {
+            // q and k rows were permuted per head so that columns c and c+32 of
+            // this 64-column group are the rotary pair (32*blk + c, half + 32*blk + c)
+            const int ai = 32 * blk + 4 * q;
+            float o1[4], o2[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const float2 cs = a.rope[pos * half + ai + t];
+              o1[t] = x1[t] * cs.x - x2[t] * cs.y;
+              o2[t] = x1[t] * cs.y + x2[t] * cs.x;
+            }
+            bf16_t* dst;
+            if (region == 0) {
+              dst = a.q + (size_t)row * a.ldq + head * hd;
+            } else {
+              const int env = a.meta.row_env[row];
+              const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
+              dst = a.kv.k + (((size_t)page * H + head) * kPage + pos % kPage) * hd;
+            }
+            *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
+            *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
+          } else {
+            const int env = a.meta.row_env[row];
+            const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
+            bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + pos % kPage;
+            const int i1 = cc0 % hd + 4 * q;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              vb[(size_t)(i1 + t) * kPage] = f2bf(x1[t]);
+              vb[(size_t)(i1 + t + 32) * kPage] = f2bf(x2[t]);
+            }
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
   }
 }
 
