@@ -52,8 +52,9 @@ extern "C" {
 #define VLA_FLAG_BAD_ACTION 2u      /* a teacher-forced token outside the action range: scored as NaN */
 
 /* Decoder shape and capacity.
- *   d_model = n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0;
- *   d_ffn % 16 == 0; 1 <= action_bins <= 256; action_begin + action_bins <= vocab;
+ *   d_model = n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0,
+ *   d_model <= 8192; d_ffn >= 1 (padded internally to a multiple of 64);
+ *   1 <= action_bins <= 256; action_begin + action_bins <= vocab;
  *   1 <= n_actions <= 16; max_seq <= 320 (prefix + n_actions rows of one env);
  *   page_size == 16; 1 <= max_batch <= 512. */
 typedef struct vla_config {

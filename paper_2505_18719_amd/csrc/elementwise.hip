@@ -113,39 +113,30 @@ __global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* 
                                                                    int d) {
   __shared__ float sh[4];
   const int m = blockIdx.x;
+  const int n = d / 256;  // elements per thread (d % 256 == 0)
   float v[kMaxPerThread];
-  float ss = 0.f;
-  int n = 0;
-  for (int c = threadIdx.x; c < d; c += 256, ++n) {
-    float acc = 0.f;
-    for (int s = 0; s < splits; ++s) acc += part[((size_t)s * M + m) * d + c];
-    v[n] = x[(size_t)m * d + c] + acc;
-    ss += v[n] * v[n];
+#pragma unroll
+  for (int i = 0; i < kMaxPerThread; ++i)
+    if (i < n) v[i] = x[(size_t)m * d + threadIdx.x + 256 * i];
+  for (int s = 0; s < splits; ++s) {
+    const float* p = part + ((size_t)s * M + m) * d + threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < kMaxPerThread; ++i)
+      if (i < n) v[i] += p[256 * i];
   }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPerThread; ++i)
+    if (i < n) ss += v[i] * v[i];
   ss = block_sum256(ss, sh);
   const float r = rsqrtf(ss / (float)d + eps);
-  n = 0;
-  for (int c = threadIdx.x; c < d; c += 256, ++n) {
-    x[(size_t)m * d + c] = v[n];
-    u[(size_t)m * d + c] = f2bf(v[n] * r * g[c]);
-  }
-}
-
-// Interleaved gate/up columns: gate j at 64*(j/32) + j%32, up j 32 further.
-__global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restrict__ part, int splits,
-                                                            bf16_t* __restrict__ h, int ldh, int M, int Fp) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  const int m = blockIdx.y;
-  if (j >= Fp) return;
-  const int N = 2 * Fp;
-  const int cg = 64 * (j >> 5) + (j & 31);
-  float gs = 0.f, us = 0.f;
-  for (int s = 0; s < splits; ++s) {
-    const float* p = part + ((size_t)s * M + m) * N;
-    gs += p[cg];
-    us += p[cg + 32];
-  }
-  h[(size_t)m * ldh + j] = f2bf(gs / (1.f + expf(-gs)) * us);
+#pragma unroll
+  for (int i = 0; i < kMaxPerThread; ++i)
+    if (i < n) {
+      const int c = threadIdx.x + 256 * i;
+      x[(size_t)m * d + c] = v[i];
+      u[(size_t)m * d + c] = f2bf(v[i] * r * g[c]);
+    }
 }
 
 __global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict__ part, int splits,
@@ -273,14 +264,8 @@ hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float*
 hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u, const float* g,
                                        float eps, int M, int d, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (d > 256 * kMaxPerThread) return hipErrorInvalidValue;
+  if (d > 256 * kMaxPerThread || d % 256 != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(256), 0, s, part, splits, x, u, g, eps, M, d);
-  return hipGetLastError();
-}
-
-hipError_t launch_reduce_swiglu(const float* part, int splits, bf16_t* h, int ldh, int M, int Fp, hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((Fp + 255) / 256, M), dim3(256), 0, s, part, splits, h, ldh, M, Fp);
   return hipGetLastError();
 }
 

@@ -42,6 +42,12 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
   tn = r / gm;
 }
 
+// Physical position of logical 16-byte chunk c of tile row r is c ^ swz(r).
+// A 32-row operand read (one chunk column) then touches distinct banks for
+// every 8 consecutive rows and for every 16 consecutive rows split by parity,
+// i.e. it is conflict free whether the LDS serves 8 or 16 lanes per cycle.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
 // Direct global -> LDS copy of 16 bytes per lane; lane i of the wave writes
 // bytes [16 i, 16 i + 16) after the wave-uniform LDS base.
 __device__ __forceinline__ void g2lds16(const bf16_t* g, uint4* lds_wave_base) {
@@ -50,8 +56,7 @@ __device__ __forceinline__ void g2lds16(const bf16_t* g, uint4* lds_wave_base) {
 
 // Each wave copies 8 blocks of 8 rows x 128 bytes of the A tile and of the W
 // tile.  Lane i of a block covers row 8b + i/8 and stores physical chunk i%8,
-// which holds logical K chunk (i%8) ^ (row%8): the XOR swizzle that makes the
-// 32-row MFMA operand reads conflict free.
+// which holds logical K chunk (i%8) ^ swz(row).
 struct Loader {
   const bf16_t* a;
   const bf16_t* w;
@@ -73,12 +78,12 @@ __device__ __forceinline__ void load_frags(const uint4* sa, const uint4* sw, int
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = wm * 128 + i * 32 + l31;
-    af[i] = as_bf16x8(sa[row * CH + (c ^ (row & 7))]);
+    af[i] = as_bf16x8(sa[row * CH + (c ^ swz(row))]);
   }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int row = wn * 128 + j * 32 + l31;
-    bw[j] = as_bf16x8(sw[row * CH + (c ^ (row & 7))]);
+    bw[j] = as_bf16x8(sw[row * CH + (c ^ swz(row))]);
   }
 }
 
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int row = (wave * 8 + j) * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ (lane >> 3);
+    const int chunk = (lane & 7) ^ swz(row);
     ld.aoff[j] = min(m0 + row, M - 1) * a.lda + chunk * 8;
     ld.woff[j] = min(n0 + row, N - 1) * K + chunk * 8;
   }
@@ -139,13 +144,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
     issue_tile(ld, min(kt + 1, nk - 1) * BK, lds[cur ^ 1][0], lds[cur ^ 1][1], wave);
     compute_tile(lds[cur][0], lds[cur][1], acc, wm, wn, lane);
     // schedule: the 16 copies first, the first k-step's 8 operand reads, then
-    // one operand read of the next k-step per two MFMAs
+    // in each k-step the next step's 8 operand reads interleaved with its
+    // first 8 MFMAs, so that 8 more MFMAs cover their latency
     __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
-    for (int t = 0; t < 24; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    for (int ks = 0; ks < 3; ++ks) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
     __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the next stage have landed

@@ -57,8 +57,12 @@ struct GemmArgs {
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s);
 
-// Skinny split-K GEMM for decode: part[s, m, n] = sum over the s-th K slice of
-// A[m, k] * W[n, k], for M <= 128 rows.  Requires N % 64 == 0, K % 32 == 0.
+// Skinny split-K GEMM for decode: C = A[M, K] * W[N, K]^T for M <= 128 rows.
+// Requires N % 64 == 0, K % 32 == 0.  kSkinnyPartial writes the fp32 partial
+// sum of K slice s to part[s, m, n]; kSkinnySwiGlu (one slice only) treats W
+// as interleaved [gate; up] blocks of 32 rows and writes
+// h[m, j] = bf16(silu(gate_j) * up_j).
+enum SkinnyEpilogue { kSkinnyPartial = 0, kSkinnySwiGlu = 1 };
 struct SkinnyArgs {
   const bf16_t* A;
   int lda;
@@ -67,9 +71,11 @@ struct SkinnyArgs {
   int N, K;
   float* part;  // [splits, M, N]
   int splits;
+  bf16_t* h;    // kSkinnySwiGlu output [M, ldh]
+  int ldh;
 };
 int skinny_splits(int M, int N, int K, int max_splits);
-hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t s);
+hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t s, SkinnyEpilogue epi = kSkinnyPartial);
 
 // Elementwise / reduction kernels
 struct EmbedArgs {
@@ -99,10 +105,6 @@ hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float*
 // x[m] += sum_s part[s, m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d)
 hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u,
                                        const float* g, float eps, int M, int d, hipStream_t s);
-
-// h[m, j] = bf16(silu(sum gate) * sum up) from interleaved partial columns
-hipError_t launch_reduce_swiglu(const float* part, int splits, bf16_t* h, int ldh, int M, int Fp,
-                                hipStream_t s);
 
 // z[m, n] = sum_s part[s, m, n] for n < N; partial rows have stride ldp >= N
 hipError_t launch_reduce_sum(const float* part, int splits, float* z, int M, int N, int ldp, hipStream_t s);

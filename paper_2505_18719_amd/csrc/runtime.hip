@@ -57,7 +57,8 @@ int check_config(const vla_config* c, Dims* o) {
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(VLA_EUNSUPPORTED, "head_dim must be 64 or 128");
   if (c->d_model != c->n_heads * c->head_dim) return fail(VLA_EINVAL, "d_model != n_heads * head_dim");
-  if (c->d_model > 8192) return fail(VLA_EUNSUPPORTED, "d_model must be <= 8192");
+  if (c->d_model > 8192 || c->d_model % 256 != 0)
+    return fail(VLA_EUNSUPPORTED, "d_model must be a multiple of 256, at most 8192");
   if (c->action_bins > 256) return fail(VLA_EUNSUPPORTED, "action_bins must be <= 256");
   if (c->action_begin < 0 || c->action_begin + c->action_bins > c->vocab)
     return fail(VLA_EINVAL, "action range outside the vocabulary");
@@ -540,10 +541,8 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
         so.splits = skinny_splits(B, so.N, so.K, kMaxSplits);
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, s));
         VLA_CK(launch_reduce_residual_norm(m->part, so.splits, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
-        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part, 0};
-        sg.splits = skinny_splits(B, sg.N, sg.K, kMaxSplits);
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, s));
-        VLA_CK(launch_reduce_swiglu(m->part, sg.splits, m->h, D.Fp, B, D.Fp, s));
+        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part, 1, m->h, D.Fp};
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, s, kSkinnySwiGlu));
         SkinnyArgs sd{m->h, D.Fp, B, w.wd, D.d, D.Fp, m->part, 0};
         sd.splits = skinny_splits(B, sd.N, sd.K, kMaxSplits);
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, s));

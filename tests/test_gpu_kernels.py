@@ -47,7 +47,7 @@ def test_prefill_gemm_7b_shape_sampled_rows():
 
 
 @pytest.mark.parametrize("M", [1, 7, 16, 33, 64, 128])
-@pytest.mark.parametrize("N,K,splits", [(256, 4096, 16), (1024, 704, 3), (768, 256, 1)])
+@pytest.mark.parametrize("N,K,splits", [(256, 4096, 16), (1024, 704, 3), (768, 256, 1), (4096, 11008, 4)])
 def test_decode_skinny_gemm_matches_float64(M, N, K, splits):
     from paper_2505_18719_amd import vla
     A, W = _rand_bf16((M, K), 5 + M), _rand_bf16((N, K), 6, 0.02)
