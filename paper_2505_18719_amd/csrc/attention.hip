@@ -1,13 +1,11 @@
 // Causal attention over the paged KV cache on gfx950.
 //
 // Prefill: one 256-thread workgroup per (64-query block of one environment,
-// head); each wave owns 16 queries.  Scores S = Q K^T / sqrt(hd) come from
-// v_mfma_f32_16x16x32_bf16 with the key rows read straight from their pages;
-// a whole score row (<= 320 keys, the longest sequence of one environment)
-// stays in registers, so the softmax is exact (true row maximum, no online
-// rescaling).  P goes through LDS into the MFMA A-operand layout and P*V runs
-// as two bf16 MFMAs (P = P_hi + P_lo) against the transposed V pages, which
-// keeps P at ~16 significant bits.
+// head); each wave owns 16 queries.  K and V^T are staged through LDS one
+// 32-key chunk at a time (double-buffered, one copy per workgroup), scores
+// are computed transposed so that P stays in registers in the layout the
+// P*V MFMA consumes, and a whole score row (<= 320 keys, the longest sequence
+// of one environment) stays in registers, so the softmax is exact.
 //
 // Decode: one workgroup per (environment, head) and one query; scores and
 // P*V in fp32 on the vector ALUs, streaming K rows and transposed V pages with
@@ -20,120 +18,193 @@ namespace vla {
 namespace {
 
 constexpr int kMaxKeyTiles = 20;  // 320 keys
-constexpr int kPRow = kMaxKeyTiles * 16 + 4;
+constexpr int kMaxChunks = kMaxKeyTiles / 2;  // 32-key chunks
+
+// One 32-key chunk of one head staged in LDS.  K rows keep the page layout
+// (key-major, HD contiguous) with a 16-byte pad per row; V^T rows (one per
+// feature, 16 keys of one page) get a 16-byte pad too.  The pads put the 16
+// rows read by one MFMA operand load on distinct bank groups.
+template <int HD>
+struct AttnChunk {
+  static constexpr int KROW = HD * 2 + 16;       // bytes per key row
+  static constexpr int VROW = 48;                // bytes per feature row (16 keys + pad)
+  static constexpr int KBYTES = 32 * KROW;
+  static constexpr int VBYTES = 2 * HD * VROW;
+};
+
+// Copy chunk c (pages 2c, 2c+1 of this environment) of head `head` from the
+// page pool into registers: each thread moves 16-byte pieces of both pages of
+// K and of V^T (coalesced: a page of one head is contiguous).
+template <int HD>
+struct ChunkRegs {
+  static constexpr int PER = (2 * 16 * HD * 2) / (256 * 16);  // 16-byte pieces per thread per tensor
+  uint4 k[PER], v[PER];
+};
 
 template <int HD>
+__device__ __forceinline__ void chunk_load(ChunkRegs<HD>& r, const bf16_t* kpool, const bf16_t* vpool,
+                                           const int32_t* pt, int c, int H, int head, bool kv_k, bool kv_v) {
+  constexpr int PIECES_PER_PAGE = 16 * HD * 2 / 16;
+#pragma unroll
+  for (int i = 0; i < ChunkRegs<HD>::PER; ++i) {
+    const int piece = threadIdx.x + 256 * i;
+    const int pl = piece / PIECES_PER_PAGE, off = piece % PIECES_PER_PAGE;
+    const size_t base = ((size_t)pt[2 * c + pl] * H + head) * (16 * HD);
+    if (kv_k) r.k[i] = *reinterpret_cast<const uint4*>(kpool + base + off * 8);
+    if (kv_v) r.v[i] = *reinterpret_cast<const uint4*>(vpool + base + off * 8);
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void chunk_store(const ChunkRegs<HD>& r, char* kl, char* vl, bool kv_k, bool kv_v) {
+  constexpr int PIECES_PER_PAGE = 16 * HD * 2 / 16;
+#pragma unroll
+  for (int i = 0; i < ChunkRegs<HD>::PER; ++i) {
+    const int piece = threadIdx.x + 256 * i;
+    const int pl = piece / PIECES_PER_PAGE, off = piece % PIECES_PER_PAGE;
+    if (kv_k) {  // K page: [slot][HD]
+      const int slot = off / (HD / 8), j = off % (HD / 8);
+      *reinterpret_cast<uint4*>(kl + (pl * 16 + slot) * AttnChunk<HD>::KROW + j * 16) = r.k[i];
+    }
+    if (kv_v) {  // V^T page: [HD][16 slots]
+      const int f = off / 2, half = off % 2;
+      *reinterpret_cast<uint4*>(vl + (pl * HD + f) * AttnChunk<HD>::VROW + half * 16) = r.v[i];
+    }
+  }
+}
+
+// Prefill attention, one workgroup per (64-query block of one environment,
+// head), 16 queries per wave.  Scores are computed transposed, S^T = K Q^T,
+// with the keys of each 32-key chunk assigned to MFMA rows so that the lane
+// group g ends up holding keys 8g .. 8g+7 of the chunk for its query: exactly
+// the B-operand fragment of P^T in O^T = V^T P^T.  P therefore never leaves
+// registers; it enters the MFMA as P_hi + P_lo (two bf16 products, ~16
+// significant bits).  The whole score row of a query (<= 320 keys) is kept,
+// so the softmax is exact (true maximum, no online rescaling).
+template <int HD>
 __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
-  __shared__ float pl[4][16][kPRow];
+  using C = AttnChunk<HD>;
+  __shared__ __attribute__((aligned(16))) char klds[2][C::KBYTES];
+  __shared__ __attribute__((aligned(16))) char vlds[2][C::VBYTES];
   const int item = blockIdx.x, head = blockIdx.y;
   const int env = a.qblocks[2 * item], q0 = a.qblocks[2 * item + 1];
   const int L = a.env_len[env], row0 = a.env_row0[env];
   const int H = a.n_heads;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, g = lane >> 4;
-  const int qw = q0 + wave * 16;
+  const int qw = q0 + wave * 16;                 // first query of this wave
   const int kend = min(L, q0 + 64);
-  const int nkt = (kend + 15) / 16;
+  const int nch = (kend + 31) / 32;
   const int32_t* pt = a.page_table + env * a.max_pages;
 
   constexpr int KS = HD / 32;
-  uint4 qf[KS];
+  uint4 qf[KS];  // B operand: query r16, features 32 ks + 8g .. +8
   {
-    const int qrow = min(qw + r16, L - 1);
-    const bf16_t* qp = a.q + (size_t)(row0 + qrow) * a.d + head * HD + 8 * g;
+    const bf16_t* qp = a.q + (size_t)(row0 + min(qw + r16, L - 1)) * a.d + head * HD + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const uint4*>(qp + ks * 32);
   }
+  // MFMA row i of tile t (0: A, 1: B) of a chunk is key 8*(i/4) + 4t + i%4
+  const int krowA = 8 * (r16 >> 2) + (r16 & 3);
 
+  // ---- pass 1: scores
   f32x4 sc[kMaxKeyTiles];
 #pragma unroll
-  for (int kt = 0; kt < kMaxKeyTiles; ++kt) {
-    sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (kt < nkt) {
-      const int page = pt[kt];
-      const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + r16) * HD + 8 * g;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        sc[kt] = mfma16(as_bf16x8(qf[ks]), as_bf16x8(*reinterpret_cast<const uint4*>(kp + ks * 32)), sc[kt]);
-    }
-  }
-
-  // lane holds queries qw + 4g + r (r < 4) against key kt*16 + r16
-  float mx[4], sum[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) mx[r] = -INFINITY;
-#pragma unroll
-  for (int kt = 0; kt < kMaxKeyTiles; ++kt) {
-    if (kt < nkt) {
-      const int key = kt * 16 + r16;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int qpos = qw + 4 * g + r;
-        const float v = (key <= qpos && key < L) ? sc[kt][r] * a.scale : -INFINITY;
-        sc[kt][r] = v;
-        mx[r] = fmaxf(mx[r], v);
-      }
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    mx[r] = group16_max(mx[r]);
-    sum[r] = 0.f;
-  }
-#pragma unroll
-  for (int kt = 0; kt < kMaxKeyTiles; ++kt) {
-    if (kt < nkt) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = (sc[kt][r] == -INFINITY) ? 0.f : expf(sc[kt][r] - mx[r]);
-        sum[r] += p;
-        pl[wave][4 * g + r][kt * 16 + r16] = p;
-      }
-    }
-  }
-  if (nkt & 1) {  // zero the unused half of the last 32-key chunk
-#pragma unroll
-    for (int r = 0; r < 4; ++r) pl[wave][4 * g + r][nkt * 16 + r16] = 0.f;
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) sum[r] = group16_sum(sum[r]);
+  for (int t = 0; t < kMaxKeyTiles; ++t) sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkRegs<HD> cr;
+  chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, 0, H, head, true, false);
+  chunk_store<HD>(cr, klds[0], nullptr, true, false);
   __syncthreads();
+#pragma unroll
+  for (int c = 0; c < kMaxChunks; ++c) {
+    if (c < nch) {
+      if (c + 1 < nch) chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, c + 1, H, head, true, false);
+      const char* kl = klds[c & 1];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const char* kr = kl + (krowA + 4 * t) * C::KROW + 16 * g;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          sc[2 * c + t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(kr + ks * 64)), as_bf16x8(qf[ks]),
+                                 sc[2 * c + t]);
+      }
+      if (c + 1 < nch) chunk_store<HD>(cr, klds[(c + 1) & 1], nullptr, true, false);
+      __syncthreads();
+    }
+  }
 
+  // lane holds S(query qw + r16, key 32c + 8g + 4t + r) in sc[2c + t][r]
+  const int qpos = qw + r16;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < kMaxChunks; ++c)
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = 32 * c + 8 * g + 4 * t + r;
+        const bool ok = c < nch && key <= qpos && key < L;
+        const float v = ok ? sc[2 * c + t][r] * a.scale : -INFINITY;
+        sc[2 * c + t][r] = v;
+        mx = fmaxf(mx, v);
+      }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  float sum = 0.f;
+#pragma unroll
+  for (int t = 0; t < kMaxKeyTiles; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = sc[t][r] == -INFINITY ? 0.f : expf(sc[t][r] - mx);
+      sc[t][r] = p;
+      sum += p;
+    }
+  sum += __shfl_xor(sum, 16, kWave);
+  sum += __shfl_xor(sum, 32, kWave);
+
+  // ---- pass 2: O^T = V^T P^T
   constexpr int NB = HD / 16;
   f32x4 o[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nch = (nkt + 1) / 2;
-  for (int ch = 0; ch < nch; ++ch) {
-    const float* pr = &pl[wave][r16][ch * 32 + 8 * g];
-    bf16x8 phi, plo;
+  chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, 0, H, head, false, true);
+  chunk_store<HD>(cr, nullptr, vlds[0], false, true);
+  __syncthreads();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float p = pr[j];
-      const __bf16 h = (__bf16)p;
-      phi[j] = h;
-      plo[j] = (__bf16)(p - (float)h);
-    }
-    const int tile = 2 * ch + (g >> 1);
-    const bool valid = tile < nkt;
-    const bf16_t* vp = a.kv.v + ((size_t)(valid ? pt[tile] : 0) * H + head) * HD * kPage + 8 * (g & 1);
+  for (int c = 0; c < kMaxChunks; ++c) {
+    if (c < nch) {
+      if (c + 1 < nch) chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, c + 1, H, head, false, true);
+      bf16x8 phi, plo;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const uint4 vv = valid ? *reinterpret_cast<const uint4*>(vp + (size_t)(nb * 16 + r16) * kPage)
-                             : make_uint4(0, 0, 0, 0);
-      o[nb] = mfma16(phi, as_bf16x8(vv), o[nb]);
-      o[nb] = mfma16(plo, as_bf16x8(vv), o[nb]);
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = sc[2 * c + t][r];
+          const __bf16 h = (__bf16)p;
+          phi[4 * t + r] = h;
+          plo[4 * t + r] = (__bf16)(p - (float)h);
+        }
+      // A operand: V^T row (feature nb*16 + r16), keys 8g .. 8g+7 of the chunk
+      const char* vl = vlds[c & 1] + (g >> 1) * HD * C::VROW + (g & 1) * 16;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint4 vv = *reinterpret_cast<const uint4*>(vl + (nb * 16 + r16) * C::VROW);
+        o[nb] = mfma16(as_bf16x8(vv), phi, o[nb]);
+        o[nb] = mfma16(as_bf16x8(vv), plo, o[nb]);
+      }
+      if (c + 1 < nch) chunk_store<HD>(cr, nullptr, vlds[(c + 1) & 1], false, true);
+      __syncthreads();
     }
   }
 
+  // o[nb][r] = O(query qw + r16, feature nb*16 + 4g + r)
+  if (qpos < L) {
+    const float inv = 1.f / sum;
+    bf16_t* op = a.o + (size_t)(row0 + qpos) * a.d + head * HD + 4 * g;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qpos = qw + 4 * g + r;
-    if (qpos >= L) continue;
-    const float inv = 1.f / sum[r];
-    bf16_t* op = a.o + (size_t)(row0 + qpos) * a.d + head * HD + r16;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) op[nb * 16] = f2bf(o[nb][r] * inv);
+    for (int nb = 0; nb < NB; ++nb)
+      *reinterpret_cast<uint2*>(op + nb * 16) =
+          make_uint2(pack2bf(o[nb][0] * inv, o[nb][1] * inv), pack2bf(o[nb][2] * inv, o[nb][3] * inv));
   }
 }
 

@@ -7,8 +7,9 @@
 // take interleaved 32-wide k-steps of that slice, so together they read each
 // weight row as one contiguous stream, and they combine their partial tiles
 // through LDS at the end.  Each lane loads its weight fragment straight from
-// global memory as 16-byte non-temporal loads; several k-steps are in flight
-// per wave.  The activations (<= 128 x K bf16) are read through L2, where
+// global memory as 16-byte loads; several k-steps are in flight per wave.
+// Each workgroup starts at a different point of its K range so that the
+// workgroups running at the same time spread their activation reads over L2.  The activations (<= 128 x K bf16) are read through L2, where
 // every workgroup of the GPU shares them; owning 64 columns amortises each
 // activation fragment over four weight fragments.
 //
@@ -49,36 +50,59 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a, int kslic
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // wave w takes k-steps kb + 32 * (NW * t + w)
-  int k = kb + 32 * wave;
-  for (; k + 32 * NW * (U - 1) < ke; k += 32 * NW * U) {
-    uint4 wv[U][4], av[U][MB];
+  // Wave w takes the k-steps kb + 32 * (NW * j + w), j < Tw, starting at a
+  // workgroup-dependent rotation so that concurrently running workgroups read
+  // different parts of the shared activations.  Batches of U k-steps are
+  // double-buffered in registers: batch b+1 is in flight while the MFMAs of
+  // batch b run.
+  const int T = (ke - kb + 31) / 32;
+  const int Tw = T > wave ? (T - wave + NW - 1) / NW : 0;
+  const int rot = Tw > 0 ? (int)((blockIdx.x * 37u + blockIdx.y * 11u) % (unsigned)Tw) : 0;
+  const int nbatch = Tw / U;
+  uint4 wv[2][U][4], av[2][U][MB];
+  auto kstep = [&](int j) {
+    j += rot;
+    j = j >= Tw ? j - Tw : j;
+    return kb + 32 * (NW * j + wave);
+  };
+  auto load = [&](int b, uint4 (&w)[U][4], uint4 (&x)[U][MB]) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      const int k = kstep(b * U + u);
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) wv[u][nb] = load_stream16(wp[nb] + k + 32 * NW * u);
+      for (int nb = 0; nb < 4; ++nb) w[u][nb] = *reinterpret_cast<const uint4*>(wp[nb] + k);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) av[u][mb] = *reinterpret_cast<const uint4*>(ap[mb] + k + 32 * NW * u);
+      for (int mb = 0; mb < MB; ++mb) x[u][mb] = *reinterpret_cast<const uint4*>(ap[mb] + k);
+    }
+  };
+  auto math = [&](const uint4 (&w)[U][4], const uint4 (&x)[U][MB]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          acc[mb][nb] = mfma16(as_bf16x8(av[u][mb]), as_bf16x8(wv[u][nb]), acc[mb][nb]);
+        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x[u][mb]), as_bf16x8(w[u][nb]), acc[mb][nb]);
+  };
+  if (nbatch > 0) load(0, wv[0], av[0]);
+  int b = 0;
+  for (; b + 2 <= nbatch; b += 2) {
+    load(b + 1, wv[1], av[1]);
+    math(wv[0], av[0]);
+    if (b + 2 < nbatch) load(b + 2, wv[0], av[0]);
+    math(wv[1], av[1]);
   }
-  for (; k < ke; k += 32 * NW) {
-    uint4 wv[4], av[MB];
+  if (b < nbatch) math(wv[0], av[0]);
+  for (int j = nbatch * U; j < Tw; ++j) {
+    const int k = kstep(j);
+    uint4 w1[4], x1[MB];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) wv[nb] = load_stream16(wp[nb] + k);
+    for (int nb = 0; nb < 4; ++nb) w1[nb] = *reinterpret_cast<const uint4*>(wp[nb] + k);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) av[mb] = *reinterpret_cast<const uint4*>(ap[mb] + k);
+    for (int mb = 0; mb < MB; ++mb) x1[mb] = *reinterpret_cast<const uint4*>(ap[mb] + k);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(av[mb]), as_bf16x8(wv[nb]), acc[mb][nb]);
+      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x1[mb]), as_bf16x8(w1[nb]), acc[mb][nb]);
   }
 
   // acc[mb][nb][r] is row mb*16 + 4g + r, column nb*16 + r16 of the tile
@@ -162,8 +186,8 @@ hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t st, SkinnyEpilogue epi
   const int mb = (a.M + 15) / 16;
   if (mb <= 1) return launch_mb<1, 4>(a, kslice, epi, st);
   if (mb <= 2) return launch_mb<2, 4>(a, kslice, epi, st);
-  if (mb <= 4) return launch_mb<4, 4>(a, kslice, epi, st);
-  return launch_mb<8, 2>(a, kslice, epi, st);
+  if (mb <= 4) return launch_mb<4, 2>(a, kslice, epi, st);
+  return launch_mb<8, 1>(a, kslice, epi, st);
 }
 
 }  // namespace vla
