@@ -6,11 +6,12 @@
 // output tile; each wave owns 128 x 128 of it as 4 x 4 blocks of
 // v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane, held in AGPRs),
 // which halves the LDS operand traffic per MFMA compared with 128 x 64 wave
-// tiles.  K advances in steps of 64 through two LDS stages of 64 KB filled by
-// direct global -> LDS loads (global_load_lds_dwordx4, no VGPR round trip),
-// issued one stage ahead of the MFMAs that consume the other.  16-byte chunks
-// are XOR-swizzled by row so that the MFMA operand reads (ds_read_b128, 32
-// rows x one chunk column) spread over the LDS banks.  Workgroup ids are
+// tiles.  K advances in steps of 32 through a ring of four 32 KB LDS stages
+// filled by direct global -> LDS loads (global_load_lds_dwordx4, no VGPR round
+// trip) issued three steps ahead, one copy instruction between MFMAs, so the
+// copies neither stall the MFMA issue in a burst nor have to land within one
+// step.  16-byte chunks are XOR-swizzled by row so that the MFMA operand
+// reads (ds_read_b128, 32 rows x one chunk column) spread over the LDS banks.  Workgroup ids are
 // remapped so that the tiles one XCD runs are contiguous in a grouped (8
 // tile-rows) order, which keeps A panels and W panels resident in that XCD's L2.
 #include "common.h"
@@ -20,9 +21,11 @@ namespace vla {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int NT = 256;       // 4 waves, 2 x 2, each owning 128 x 128 of the tile
-constexpr int CH = BK / 8;    // 16-byte chunks per tile row
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int NT = 256;        // 4 waves, 2 x 2, each owning 128 x 128 of the tile
+constexpr int CH = BK / 8;     // 16-byte chunks per tile row (64-byte rows)
+constexpr int NSTAGE = 4;      // LDS ring of K steps (4 x 32 KB)
+constexpr int AHEAD = 3;       // K steps in flight ahead of the one being consumed
 constexpr int GROUP_M = 8;
 
 typedef __attribute__((address_space(3))) void lds_ptr_t;
@@ -43,30 +46,35 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
 }
 
 // Physical position of logical 16-byte chunk c of tile row r is c ^ swz(r).
-// A 32-row operand read (one chunk column) then touches distinct banks for
-// every 8 consecutive rows and for every 16 consecutive rows split by parity,
+// A 32-row operand read (one chunk column of 64-byte rows) then hits distinct
+// bank groups for every 8 consecutive rows and for every 16 consecutive rows,
 // i.e. it is conflict free whether the LDS serves 8 or 16 lanes per cycle.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 
-// Direct global -> LDS copy of 16 bytes per lane; lane i of the wave writes
-// bytes [16 i, 16 i + 16) after the wave-uniform LDS base.
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane i of the wave writes bytes [16 i, 16 i + 16) after the wave-uniform LDS
+// address in M0.  Issued through inline assembly so that the compiler does
+// not treat the copy as an LDS store: it would otherwise wait for every copy
+// in flight (vmcnt(0)) before any later LDS read, serialising the copies that
+// run ahead; the kernel instead waits explicitly for the stage it consumes.
 __device__ __forceinline__ void g2lds16(const bf16_t* g, uint4* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((gbl_ptr_t*)g, (lds_ptr_t*)lds_wave_base, 16, 0, 0);
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)((lds_ptr_t*)lds_wave_base));
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(m0), "v"(g) : "memory", "m0");
 }
 
-// Each wave copies 8 blocks of 8 rows x 128 bytes of the A tile and of the W
-// tile.  Lane i of a block covers row 8b + i/8 and stores physical chunk i%8,
-// which holds logical K chunk (i%8) ^ swz(row).
+// Each wave copies 4 blocks of 16 rows x 64 bytes of the A tile and of the W
+// tile per K step.  Lane i of a block covers row 16b + i/4 and stores physical
+// chunk i%4, which holds logical K chunk (i%4) ^ swz(row).
 struct Loader {
   const bf16_t* a;
   const bf16_t* w;
-  int aoff[8], woff[8];  // element offsets of this lane's rows (rows clamped to M-1 / N-1)
+  int aoff[4], woff[4];  // element offsets of this lane's rows (rows clamped to M-1 / N-1)
 };
 
 __device__ __forceinline__ void issue_tile(const Loader& ld, int k0, uint4* sa, uint4* sw, int wave) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int blk = wave * 8 + j;
+  for (int j = 0; j < 4; ++j) {
+    const int blk = wave * 4 + j;
     g2lds16(ld.a + ld.aoff[j] + k0, sa + blk * 64);
     g2lds16(ld.w + ld.woff[j] + k0, sw + blk * 64);
   }
@@ -87,25 +95,20 @@ __device__ __forceinline__ void load_frags(const uint4* sa, const uint4* sw, int
   }
 }
 
-// 4 k-steps of 16 on one LDS stage; the operand fragments of k-step ks+1 are
-// read while the 16 MFMAs of k-step ks run.
-__device__ __forceinline__ void compute_tile(const uint4* sa, const uint4* sw, f32x16 (&acc)[4][4], int wm, int wn,
-                                             int lane) {
-  bf16x8 af[2][4], bw[2][4];
-  load_frags(sa, sw, 0, wm, wn, lane, af[0], bw[0]);
+__device__ __forceinline__ void mfma_rows(const bf16x8 (&af)[4], const bf16x8 (&bw)[4], f32x16 (&acc)[4][4],
+                                          int i0, int i1) {
 #pragma unroll
-  for (int ks = 0; ks < BK / 16; ++ks) {
-    if (ks + 1 < BK / 16) load_frags(sa, sw, ks + 1, wm, wn, lane, af[(ks + 1) & 1], bw[(ks + 1) & 1]);
+  for (int i = i0; i < i1; ++i)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[ks & 1][i], bw[ks & 1][j], acc[i][j]);
-  }
+    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bw[j], acc[i][j]);
 }
+
+// s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) >> 4) << 14) | (0xF << 8) | (0x7 << 4) | ((n) & 15))
 
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds[2][2][BM * CH];  // [stage][A / W][256 rows x 8 chunks]
+  __shared__ uint4 lds[NSTAGE][2][BM * CH];  // [stage][A / W][256 rows x 4 chunks]
 
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -118,9 +121,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   ld.a = a.A;
   ld.w = a.W;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int row = (wave * 8 + j) * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ swz(row);
+  for (int j = 0; j < 4; ++j) {
+    const int row = (wave * 4 + j) * 16 + (lane >> 2);
+    const int chunk = (lane & 3) ^ swz(row);
     ld.aoff[j] = min(m0 + row, M - 1) * a.lda + chunk * 8;
     ld.woff[j] = min(n0 + row, N - 1) * K + chunk * 8;
   }
@@ -133,34 +136,43 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Pipeline over K steps of 32 (two MFMA k-steps of 16).  Copies run AHEAD
+  // steps ahead through the 4-stage ring, one copy instruction between MFMAs;
+  // a step only waits for its own stage (the later copies stay in flight).
+  // The barrier that hands the next stage over sits inside the second k-step:
+  // the first operand fragments of the next stage are read while its last 8
+  // MFMAs run.  Each wave issues 8 copies per step.
   const int nk = K / BK;
-  issue_tile(ld, 0, lds[0][0], lds[0][1], wave);
+  bf16x8 fa[2][4], fb[2][4];
+#pragma unroll
+  for (int st = 0; st < AHEAD; ++st) issue_tile(ld, min(st, nk - 1) * BK, lds[st][0], lds[st][1], wave);
+  WAIT_VMCNT(8 * (AHEAD - 1));
+  __syncthreads();
+  load_frags(lds[0][0], lds[0][1], 0, wm, wn, lane, fa[0], fb[0]);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & (NSTAGE - 1);
+    const int nxt = (kt + 1) & (NSTAGE - 1);
+    const int fill = (kt + AHEAD) & (NSTAGE - 1);
+    // the stage being filled was read in step kt - 1, before the last barrier;
+    // past the end the last step is re-copied, keeping the count per step fixed
+    issue_tile(ld, min(kt + AHEAD, nk - 1) * BK, lds[fill][0], lds[fill][1], wave);
+    load_frags(lds[cur][0], lds[cur][1], 1, wm, wn, lane, fa[1], fb[1]);
+    mfma_rows(fa[0], fb[0], acc, 0, 4);
+    mfma_rows(fa[1], fb[1], acc, 0, 2);
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
+    WAIT_VMCNT(8 * (AHEAD - 1));   // this wave's copies of step kt+1 have landed
+    __syncthreads();               // ... and everyone's
+    load_frags(lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, fa[0], fb[0]);
+    mfma_rows(fa[1], fb[1], acc, 2, 4);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+  }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    // copy the next K step into the other stage (the last iteration re-copies
-    // its own step into the unused stage, keeping the body one basic block)
-    issue_tile(ld, min(kt + 1, nk - 1) * BK, lds[cur ^ 1][0], lds[cur ^ 1][1], wave);
-    compute_tile(lds[cur][0], lds[cur][1], acc, wm, wn, lane);
-    // schedule: the 16 copies first, the first k-step's 8 operand reads, then
-    // in each k-step the next step's 8 operand reads interleaved with its
-    // first 8 MFMAs, so that 8 more MFMAs cover their latency
-    __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-#pragma unroll
-    for (int ks = 0; ks < 3; ++ks) {
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the next stage have landed
-    __syncthreads();                 // ... and everyone's; the current stage is free again
-  }
 
   // ---------------------------------------------------------------- epilogue
   // The LDS stages are free after the last barrier; each wave stages its
@@ -168,7 +180,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   // time, and then writes the epilogue's outputs with contiguous stores.
   // acc[i][j][r] holds row i*32 + 8*(r/4) + 4*lhi + r%4 and column j*32 + l31
   // of the wave tile; in LDS the float4 chunk q of row rl sits at q ^ (rl%16).
-  float* st = reinterpret_cast<float*>(lds[wave >> 1][wave & 1]);
+  float* st = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (128 * 64);
   const int l31 = lane & 31, lhi = lane >> 5;
   const int wrow0 = m0 + wm * 128;
 #pragma unroll
