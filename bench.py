@@ -16,6 +16,7 @@ measured with HIP events on the launch stream during the timed steps;
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -26,6 +27,84 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+# HBM traffic (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a plain streaming
+# kernel of known size) is kept in a profile summary together with hashes of
+# the kernel sources it was taken on; it is reported only while they match.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_openvla7b_b64.md")
+TRAFFIC_SOURCES = {"prefill_gemm": ["gemm_prefill.hip", "common.h"],
+                   "decode_gemm": ["gemm_decode.hip", "common.h"]}
+TRAFFIC_KERNELS = {"prefill_gemm": "gemm_bf16_kernel", "decode_gemm": "skinny_kernel"}
+CALIB_ELEMS = 1 << 28       # bf16 elements of the calibration kernel: reads and writes 512 MiB
+
+
+def source_hash(names):
+    import hashlib
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2505_18719_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic():
+    """Measured HBM bytes per launch for each kernel whose sources are unchanged."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return {}
+    m = re.search(r"^traffic_json: (\{.*\})$", text, re.M)
+    if not m:
+        return {}
+    rec = json.loads(m.group(1))
+    return {k: v["bytes_per_launch"] for k, v in rec.items()
+            if k in TRAFFIC_SOURCES and v.get("source") == source_hash(TRAFFIC_SOURCES[k])}
+
+
+def summarise_traffic(fetch_dir, write_dir):
+    """Markdown summary of a FETCH_SIZE run and a WRITE_SIZE run (KiB per
+    dispatch), each scaled by what the counter reads for the calibration
+    kernel (torch.neg over CALIB_ELEMS bf16 elements)."""
+    import csv
+    import glob
+
+    def per_dispatch(d, counter):
+        rows = {}
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(path)):
+                if r["Counter_Name"] == counter:
+                    key = r["Dispatch_Id"]
+                    name, val = rows.get(key, (r["Kernel_Name"], 0.0))
+                    rows[key] = (name, val + float(r["Counter_Value"]))
+        return list(rows.values())
+
+    true_kib = CALIB_ELEMS * 2 / 1024.0
+    out, rec = [], {}
+    scale = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = per_dispatch(d, counter)
+        calib = [v for n, v in rows if "neg" in n]
+        if len(calib) != 1:
+            raise SystemExit(f"expected one calibration dispatch in {d}, found {len(calib)}")
+        scale[counter] = true_kib / calib[0]
+        out.append(f"| {counter} | calibration kernel reads {calib[0]:.0f} KiB for {true_kib:.0f} KiB | "
+                   f"scale {scale[counter]:.4f} |")
+        for k, kname in TRAFFIC_KERNELS.items():
+            vals = [v for n, v in rows if kname in n]
+            rec.setdefault(k, {"launches": len(vals), "source": source_hash(TRAFFIC_SOURCES[k])})
+            rec[k][counter] = float(np.mean(vals)) * scale[counter] * 1024.0 if vals else None
+    lines = ["| counter | calibration | factor |", "|---|---|---|"] + out + ["",
+             "| kernel | launches | fetch MB / launch | write MB / launch | HBM MB / launch |", "|---|---|---|---|---|"]
+    for k, v in rec.items():
+        if v["FETCH_SIZE"] is None or v["WRITE_SIZE"] is None:
+            continue
+        v["bytes_per_launch"] = v["FETCH_SIZE"] + v["WRITE_SIZE"]
+        lines.append(f"| {TRAFFIC_KERNELS[k]} | {v['launches']} | {v['FETCH_SIZE'] / 1e6:.2f} | "
+                     f"{v['WRITE_SIZE'] / 1e6:.2f} | {v['bytes_per_launch'] / 1e6:.2f} |")
+    rec = {k: v for k, v in rec.items() if "bytes_per_launch" in v}
+    lines += ["", "traffic_json: " + json.dumps(rec)]
+    return "\n".join(lines)
 
 
 def log(*a):
@@ -68,7 +147,14 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=8, help="decoder layers in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher-forced", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain streaming kernel of known size before timing (HBM counter calibration)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) as markdown and exit")
     args = ap.parse_args()
+    if args.traffic_from:
+        print(summarise_traffic(*args.traffic_from))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1", file=sys.stderr)
@@ -109,6 +195,12 @@ def main():
 
     for k in range(args.warmup):
         step(k)
+    if args.copy_calibration:
+        src = torch.ones(CALIB_ELEMS, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        del src, dst
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
 
@@ -149,6 +241,7 @@ def main():
     prefill_flops /= args.steps
     decode_bytes /= args.steps
 
+    traffic = load_traffic()
     pg = prof["prefill_gemm"]
     g_ms = pg["ms"] / max(pg["launches"], 1)
     g_tflops = pg["work"] / (pg["ms"] * 1e-3) / 1e12
@@ -184,11 +277,11 @@ def main():
         "decode_hbm_frac": decode_bytes / (decode_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
         "roofline": {"kernel": "gemm_bf16_kernel (prefill QKV/O/gate-up/down)", "bound": "mfma",
                      "achieved": g_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": g_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": g_tflops / PEAK_BF16_TFLOPS, "traffic": traffic.get("prefill_gemm"),
                      "avg_launch_ms": g_ms, "launches": pg["launches"]},
         "roofline_decode": {"kernel": "skinny_kernel (decode QKV/O/gate-up/down)", "bound": "hbm",
                             "achieved": dg_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                            "frac": dg_gbs / PEAK_HBM_GBS, "traffic": None,
+                            "frac": dg_gbs / PEAK_HBM_GBS, "traffic": traffic.get("decode_gemm"),
                             "avg_launch_ms": dg["ms"] / max(dg["launches"], 1), "launches": dg["launches"]},
         "kernels": {"prefill_attn_tflops": pa["work"] / max(pa["ms"], 1e-9) / 1e9,
                     "prefill_attn_ms_per_step": pa["ms"] / args.steps,
