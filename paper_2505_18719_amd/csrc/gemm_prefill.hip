@@ -6,14 +6,19 @@
 // output tile; each wave owns 128 x 128 of it as 4 x 4 blocks of
 // v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane, held in AGPRs),
 // which halves the LDS operand traffic per MFMA compared with 128 x 64 wave
-// tiles.  K advances in steps of 32 through a ring of four 32 KB LDS stages
-// filled by direct global -> LDS loads (global_load_lds_dwordx4, no VGPR round
-// trip) issued three steps ahead, one copy instruction between MFMAs, so the
-// copies neither stall the MFMA issue in a burst nor have to land within one
-// step.  16-byte chunks are XOR-swizzled by row so that the MFMA operand
-// reads (ds_read_b128, 32 rows x one chunk column) spread over the LDS banks.  Workgroup ids are
-// remapped so that the tiles one XCD runs are contiguous in a grouped (8
-// tile-rows) order, which keeps A panels and W panels resident in that XCD's L2.
+// tiles.  K advances in steps of 64 through two 64 KB LDS stages.
+//
+// The kernel is bound by how fast L2 delivers the A and W tiles to the CU
+// (128 flops per delivered byte at this tile size): the operand tiles are
+// brought in with plain 16-byte buffer loads into VGPRs, two K steps ahead,
+// and written to LDS one step ahead, so about 1.5 steps of loads are in flight
+// per CU; each wave load instruction reads 8 whole 128-byte rows.  Loads, LDS
+// writes, operand reads and MFMAs are interleaved one memory instruction per
+// MFMA in a pinned order.  16-byte chunks are XOR-swizzled by row so that the
+// MFMA operand reads (ds_read_b128, 32 rows x one chunk column) and the LDS
+// writes spread over the banks.  Workgroup ids are remapped so that the tiles
+// one XCD runs are contiguous in a grouped (8 tile-rows) order, which keeps A
+// panels and W panels resident in that XCD's L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -21,15 +26,11 @@ namespace vla {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int NT = 256;        // 4 waves, 2 x 2, each owning 128 x 128 of the tile
-constexpr int CH = BK / 8;     // 16-byte chunks per tile row (64-byte rows)
-constexpr int NSTAGE = 4;      // LDS ring of K steps (4 x 32 KB)
-constexpr int AHEAD = 3;       // K steps in flight ahead of the one being consumed
+constexpr int CH = BK / 8;     // 16-byte chunks per tile row (128-byte rows)
 constexpr int GROUP_M = 8;
 
-typedef __attribute__((address_space(3))) void lds_ptr_t;
-typedef __attribute__((address_space(1))) const void gbl_ptr_t;
 
 __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_n, int& tm, int& tn) {
   // XCD-aware remap: the hardware deals workgroups round-robin to 8 XCDs.
@@ -46,69 +47,34 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
 }
 
 // Physical position of logical 16-byte chunk c of tile row r is c ^ swz(r).
-// A 32-row operand read (one chunk column of 64-byte rows) then hits distinct
-// bank groups for every 8 consecutive rows and for every 16 consecutive rows,
-// i.e. it is conflict free whether the LDS serves 8 or 16 lanes per cycle.
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+// An operand read takes one chunk column of 16 consecutive rows per 16 lanes;
+// two 128-byte rows share a 256-byte bank row, so the chunk index must take 8
+// distinct values over the 8 rows of each parity: then the 16 reads hit 16
+// distinct 16-byte bank groups.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
-// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
-// lane i of the wave writes bytes [16 i, 16 i + 16) after the wave-uniform LDS
-// address in M0.  Issued through inline assembly so that the compiler does
-// not treat the copy as an LDS store: it would otherwise wait for every copy
-// in flight (vmcnt(0)) before any later LDS read, serialising the copies that
-// run ahead; the kernel instead waits explicitly for the stage it consumes.
-__device__ __forceinline__ void g2lds16(const bf16_t* g, uint4* lds_wave_base) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)((lds_ptr_t*)lds_wave_base));
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(m0), "v"(g) : "memory", "m0");
-}
+// nothing may be scheduled across this point
+#define PIN() __builtin_amdgcn_sched_barrier(0)
 
-// Each wave copies 4 blocks of 16 rows x 64 bytes of the A tile and of the W
-// tile per K step.  Lane i of a block covers row 16b + i/4 and stores physical
-// chunk i%4, which holds logical K chunk (i%4) ^ swz(row).
-struct Loader {
-  const bf16_t* a;
-  const bf16_t* w;
-  int aoff[4], woff[4];  // element offsets of this lane's rows (rows clamped to M-1 / N-1)
-};
+// Orders of the 16 MFMAs of one k-step over the 4 x 4 blocks of the wave
+// tile (row block i, column block j) and of the 8 operand reads that feed them
+// (o = 0 for A, 1 for W; block index).  Order 0 ("triangular") lets each MFMA
+// wait only for fragments read well before it; order 1 is row-major, so that
+// its first 8 MFMAs need only the first 6 reads (the k-step that straddles the
+// barrier).
+__device__ constexpr int kMfmaI[2][16] = {{0, 0, 1, 1, 0, 1, 2, 2, 2, 0, 1, 2, 3, 3, 3, 3},
+                                          {0, 0, 0, 0, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3}};
+__device__ constexpr int kMfmaJ[2][16] = {{0, 1, 0, 1, 2, 2, 0, 1, 2, 3, 3, 3, 0, 1, 2, 3},
+                                          {0, 1, 2, 3, 0, 1, 2, 3, 0, 1, 2, 3, 0, 1, 2, 3}};
+__device__ constexpr int kReadO[2][8] = {{0, 1, 0, 1, 0, 1, 0, 1}, {0, 0, 1, 1, 1, 1, 0, 0}};
+__device__ constexpr int kReadB[2][8] = {{0, 0, 1, 1, 2, 2, 3, 3}, {0, 1, 0, 1, 2, 3, 2, 3}};
 
-__device__ __forceinline__ void issue_tile(const Loader& ld, int k0, uint4* sa, uint4* sw, int wave) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int blk = wave * 4 + j;
-    g2lds16(ld.a + ld.aoff[j] + k0, sa + blk * 64);
-    g2lds16(ld.w + ld.woff[j] + k0, sw + blk * 64);
-  }
-}
-
-__device__ __forceinline__ void load_frags(const uint4* sa, const uint4* sw, int ks, int wm, int wn, int lane,
-                                           bf16x8 (&af)[4], bf16x8 (&bw)[4]) {
-  const int l31 = lane & 31, c = 2 * ks + (lane >> 5);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = wm * 128 + i * 32 + l31;
-    af[i] = as_bf16x8(sa[row * CH + (c ^ swz(row))]);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = wn * 128 + j * 32 + l31;
-    bw[j] = as_bf16x8(sw[row * CH + (c ^ swz(row))]);
-  }
-}
-
-__device__ __forceinline__ void mfma_rows(const bf16x8 (&af)[4], const bf16x8 (&bw)[4], f32x16 (&acc)[4][4],
-                                          int i0, int i1) {
-#pragma unroll
-  for (int i = i0; i < i1; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bw[j], acc[i][j]);
-}
-
-// s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
-#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) >> 4) << 14) | (0xF << 8) | (0x7 << 4) | ((n) & 15))
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds[NSTAGE][2][BM * CH];  // [stage][A / W][256 rows x 4 chunks]
+  __shared__ uint4 lds[2][2][BM * CH];  // [stage][A / W][256 rows x 8 chunks]
 
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -117,16 +83,21 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
-  Loader ld;
-  ld.a = a.A;
-  ld.w = a.W;
+  // Loads: per K step each thread brings 8 16-byte chunks of the A tile and 8
+  // of the W tile into VGPRs (row 32 j + tid / 8, chunk tid % 8: each wave
+  // instruction reads 8 whole 128-byte rows) and later writes them to LDS at
+  // physical chunk (tid % 8) ^ swz(row).
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
+  uint32_t voff[2][8];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = (wave * 4 + j) * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ swz(row);
-    ld.aoff[j] = min(m0 + row, M - 1) * a.lda + chunk * 8;
-    ld.woff[j] = min(n0 + row, N - 1) * K + chunk * 8;
+  for (int j = 0; j < 8; ++j) {
+    const int row = j * 32 + (tid >> 3);
+    voff[0][j] = (uint32_t)((min(m0 + row, M - 1) * a.lda + (tid & 7) * 8) * 2);
+    voff[1][j] = (uint32_t)((min(n0 + row, N - 1) * K + (tid & 7) * 8) * 2);
   }
+  // uint4 index of this thread's chunk in an operand tile (rows 32 j + tid / 8: + 256 j)
+  const int widx = (tid >> 3) * CH + ((tid & 7) ^ ((tid >> 4) & 7));
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -136,42 +107,116 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Pipeline over K steps of 32 (two MFMA k-steps of 16).  Copies run AHEAD
-  // steps ahead through the 4-stage ring, one copy instruction between MFMAs;
-  // a step only waits for its own stage (the later copies stay in flight).
-  // The barrier that hands the next stage over sits inside the second k-step:
-  // the first operand fragments of the next stage are read while its last 8
-  // MFMAs run.  Each wave issues 8 copies per step.
-  const int nk = K / BK;
-  bf16x8 fa[2][4], fb[2][4];
+  const int l31 = lane & 31;
+  int roff[2][4], rswz[2][4];
 #pragma unroll
-  for (int st = 0; st < AHEAD; ++st) issue_tile(ld, min(st, nk - 1) * BK, lds[st][0], lds[st][1], wave);
-  WAIT_VMCNT(8 * (AHEAD - 1));
-  __syncthreads();
-  load_frags(lds[0][0], lds[0][1], 0, wm, wn, lane, fa[0], fb[0]);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & (NSTAGE - 1);
-    const int nxt = (kt + 1) & (NSTAGE - 1);
-    const int fill = (kt + AHEAD) & (NSTAGE - 1);
-    // the stage being filled was read in step kt - 1, before the last barrier;
-    // past the end the last step is re-copied, keeping the count per step fixed
-    issue_tile(ld, min(kt + AHEAD, nk - 1) * BK, lds[fill][0], lds[fill][1], wave);
-    load_frags(lds[cur][0], lds[cur][1], 1, wm, wn, lane, fa[1], fb[1]);
-    mfma_rows(fa[0], fb[0], acc, 0, 4);
-    mfma_rows(fa[1], fb[1], acc, 0, 2);
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
-    WAIT_VMCNT(8 * (AHEAD - 1));   // this wave's copies of step kt+1 have landed
-    __syncthreads();               // ... and everyone's
-    load_frags(lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, fa[0], fb[0]);
-    mfma_rows(fa[1], fb[1], acc, 2, 4);
+  for (int i = 0; i < 4; ++i) {
+    const int ra = wm * 128 + i * 32 + l31, rw = wn * 128 + i * 32 + l31;
+    roff[0][i] = ra * CH;
+    roff[1][i] = BM * CH + rw * CH;
+    rswz[0][i] = swz(ra);
+    rswz[1][i] = swz(rw);
+  }
+  uint4* ring = &lds[0][0][0];
+  bf16x8 fr[2][2][4];
+  uint4 rg[2][16];  // register stages: [parity][A chunks 0-7, W chunks 0-7]
+  auto read = [&](int ord, int r, int st, int q) {
+    const int o = kReadO[ord][r], i = kReadB[ord][r];
+    const int c = (2 * q + (lane >> 5)) ^ rswz[o][i];
+    fr[q & 1][o][i] = as_bf16x8(ring[st * (2 * BM * CH) + roff[o][i] + c]);
+  };
+  auto mfma = [&](int ord, int t, int q) {
+    const int i = kMfmaI[ord][t], j = kMfmaJ[ord][t];
+    acc[i][j] = mfma32(fr[q & 1][0][i], fr[q & 1][1][j], acc[i][j]);
+  };
+  const int nk = K / BK;
+  // load chunk c (0..15: A 0-7, W 8-15) of K step ks into register stage p
+  auto gload = [&](int p, int c, int ks) {
+    const int o = c >> 3, j = c & 7;
+    rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(o ? rsW : rsA, voff[o][j], ks * BK * 2, 0));
+  };
+  auto lwrite = [&](int p, int c, int st) {
+    const int o = c >> 3, j = c & 7;
+    ring[st * (2 * BM * CH) + o * (BM * CH) + j * 256 + widx] = rg[p][c];
+  };
+
+  // Pipeline: step s's tiles are loaded into register stage s % 2 during step
+  // s - 2, written to LDS stage s % 2 during the second half of step s - 1,
+  // and consumed in step s.  One step of a wave is 64 MFMAs with one memory
+  // instruction after each:
+  //   k-step 0: + the 8 operand reads of k-step 1, + loads 0-7 of step kt+2
+  //   k-step 1: + the 8 operand reads of k-step 2, + loads 8-15 of step kt+2
+  //   k-step 2: + the 8 operand reads of k-step 3 (row-major order), + LDS writes 0-7 of step kt+1
+  //   k-step 3: MFMAs 0-7 + LDS writes 8-15 of step kt+1, barrier,
+  //             MFMAs 8-15 + the 8 operand reads of k-step 0 of step kt+1
+  // The order is pinned.  LDS stage (kt+1) % 2 was last read in step kt-1,
+  // before that step's barrier.
+  auto step = [&](int kt, int P) {
+    const int cur = P, nxt = P ^ 1;
+    const int k2 = min(kt + 2, nk - 1);
+    PIN();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        mfma(0, t, q);
+        read(0, t, cur, q + 1);
+        PIN();
+      }
+#pragma unroll
+      for (int t = 8; t < 16; ++t) {
+        mfma(0, t, q);
+        gload(P, 8 * q + t - 8, k2);
+        PIN();
+      }
+    }
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      mfma(0, t, 2);
+      read(1, t, cur, 3);
+      PIN();
     }
+#pragma unroll
+    for (int t = 8; t < 16; ++t) {
+      mfma(0, t, 2);
+      lwrite(nxt, t - 8, nxt);
+      PIN();
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      mfma(1, t, 3);
+      lwrite(nxt, t + 8, nxt);
+      PIN();
+    }
+    __syncthreads();
+    PIN();
+#pragma unroll
+    for (int t = 8; t < 16; ++t) {
+      mfma(1, t, 3);
+      read(0, t - 8, nxt, 0);
+      PIN();
+    }
+  };
+
+#pragma unroll
+  for (int c = 0; c < 16; ++c) gload(0, c, 0);
+#pragma unroll
+  for (int c = 0; c < 16; ++c) gload(1, c, min(1, nk - 1));
+#pragma unroll
+  for (int c = 0; c < 16; ++c) lwrite(0, c, 0);
+  __syncthreads();
+  PIN();
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    read(0, r, 0, 0);
+    PIN();
   }
-  __builtin_amdgcn_s_waitcnt(0);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, 0);
+    step(kt + 1, 1);
+  }
+  if (kt < nk) step(kt, 0);
   __syncthreads();
 
   // ---------------------------------------------------------------- epilogue
@@ -181,7 +226,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   // acc[i][j][r] holds row i*32 + 8*(r/4) + 4*lhi + r%4 and column j*32 + l31
   // of the wave tile; in LDS the float4 chunk q of row rl sits at q ^ (rl%16).
   float* st = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (128 * 64);
-  const int l31 = lane & 31, lhi = lane >> 5;
+  const int lhi = lane >> 5;
   const int wrow0 = m0 + wm * 128;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
