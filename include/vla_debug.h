@@ -17,10 +17,11 @@ extern "C" {
 int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, float* C,
                    void* stream);
 
-/* Decode split-K GEMM: C[M, N] fp32 = A * W^T for M <= 128, using `splits`
- * K slices whose partial sums go to `scratch` (splits * M * N floats).
- * Requires N % 64 == 0, K % 32 == 0. */
-int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t splits,
+/* Decode skinny GEMM: C[M, N] fp32 = A * W^T for M <= 128 on a persistent
+ * grid of at most `workgroups` workgroups; tile segments' partial sums go to
+ * `scratch` (16 * M * N floats).  Requires N % 64 == 0, K % 256 == 0,
+ * N * K < 2^30. */
+int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
                      float* scratch, float* C, void* stream);
 
 /* Sampler on given logits z[B, A] at step `step` of gumbel[B, n_actions, A]:

@@ -24,13 +24,14 @@ int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t
   return launch_gemm(g, kEpiStoreF32, static_cast<hipStream_t>(stream)) == hipSuccess ? VLA_OK : VLA_EHIP;
 }
 
-int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t splits,
+int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
                      float* scratch, float* C, void* stream) {
-  if (!A || !W || !C || !scratch || M < 0 || N <= 0 || K <= 0 || splits < 1) return VLA_EINVAL;
+  if (!A || !W || !C || !scratch || M < 0 || N <= 0 || K <= 0 || workgroups < 1) return VLA_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  SkinnyArgs a{static_cast<const bf16_t*>(A), lda, M, static_cast<const bf16_t*>(W), N, K, scratch, splits};
-  if (launch_skinny(a, s) != hipSuccess) return VLA_EHIP;
-  return launch_reduce_sum(scratch, splits, C, M, N, N, s) == hipSuccess ? VLA_OK : VLA_EHIP;
+  const SkinnyPlan p = skinny_plan(N, K, workgroups, 16);
+  SkinnyArgs a{static_cast<const bf16_t*>(A), lda, M, static_cast<const bf16_t*>(W), N, K, scratch};
+  if (launch_skinny(a, p, s) != hipSuccess) return VLA_EHIP;
+  return launch_reduce_sum(scratch, p, C, M, N, s) == hipSuccess ? VLA_OK : VLA_EHIP;
 }
 
 int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, int32_t step, int32_t action_begin,

@@ -107,7 +107,16 @@ __global__ __launch_bounds__(256) void embed_token_norm_kernel(const int32_t* to
   }
 }
 
-__global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* __restrict__ part, int splits,
+// Sum of the partial slots of column n of a skinny GEMM (N columns) at row m.
+__device__ __forceinline__ float skinny_sum(const float* __restrict__ part, const SkinnyPlan& p, int M, int N, int m,
+                                            int n) {
+  const int ns = skinny_slots(p, n >> 6);
+  float v = 0.f;
+  for (int s = 0; s < ns; ++s) v += part[((size_t)s * M + m) * N + n];
+  return v;
+}
+
+__global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* __restrict__ part, SkinnyPlan p,
                                                                    float* __restrict__ x, bf16_t* __restrict__ u,
                                                                    const float* __restrict__ g, float eps, int M,
                                                                    int d) {
@@ -118,12 +127,9 @@ __global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* 
 #pragma unroll
   for (int i = 0; i < kMaxPerThread; ++i)
     if (i < n) v[i] = x[(size_t)m * d + threadIdx.x + 256 * i];
-  for (int s = 0; s < splits; ++s) {
-    const float* p = part + ((size_t)s * M + m) * d + threadIdx.x;
 #pragma unroll
-    for (int i = 0; i < kMaxPerThread; ++i)
-      if (i < n) v[i] += p[256 * i];
-  }
+  for (int i = 0; i < kMaxPerThread; ++i)
+    if (i < n) v[i] += skinny_sum(part, p, M, d, m, threadIdx.x + 256 * i);
   float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < kMaxPerThread; ++i)
@@ -139,14 +145,23 @@ __global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* 
     }
 }
 
-__global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict__ part, int splits,
-                                                         float* __restrict__ z, int M, int N, int ldp) {
+__global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict__ part, SkinnyPlan p,
+                                                         float* __restrict__ z, int M, int N) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (size_t)M * N) return;
-  const size_t m = i / N, n = i % N;
-  float acc = 0.f;
-  for (int s = 0; s < splits; ++s) acc += part[((size_t)s * M + m) * ldp + n];
-  z[i] = acc;
+  const int m = (int)(i / N), n = (int)(i % N);
+  z[i] = skinny_sum(part, p, M, p.tiles * 64, m, n);
+}
+
+__global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restrict__ part, SkinnyPlan p,
+                                                            bf16_t* __restrict__ h, int ldh, int M, int F) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)M * F) return;
+  const int m = (int)(i / F), j = (int)(i % F);
+  const int N = p.tiles * 64;
+  const int cg = 64 * (j >> 5) + (j & 31);
+  const float gs = skinny_sum(part, p, M, N, m, cg), us = skinny_sum(part, p, M, N, m, cg + 32);
+  h[(size_t)m * ldh + j] = f2bf(gs / (1.f + expf(-gs)) * us);
 }
 
 // One thread per rotary pair of q and k, and per pair of v features.
@@ -169,12 +184,8 @@ __global__ __launch_bounds__(256) void decode_qkv_kernel(DecodeQkvArgs a) {
     col1 = 2 * d + head * hd + e;
     col2 = col1 + half;
   }
-  float x1 = 0.f, x2 = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const float* pr = a.part + ((size_t)s * a.B + b) * N;
-    x1 += pr[col1];
-    x2 += pr[col2];
-  }
+  const float x1 = skinny_sum(a.part, a.plan, a.B, N, b, col1);
+  const float x2 = skinny_sum(a.part, a.plan, a.B, N, b, col2);
   const int pos = a.env_prefix[b] + a.step - 1;
   if (region == 0) {
     const float2 cs = a.rope[pos * half + e];
@@ -261,19 +272,28 @@ hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float*
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u, const float* g,
+hipError_t launch_reduce_residual_norm(const float* part, const SkinnyPlan& p, float* x, bf16_t* u, const float* g,
                                        float eps, int M, int d, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (d > 256 * kMaxPerThread || d % 256 != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(256), 0, s, part, splits, x, u, g, eps, M, d);
+  if (d > 256 * kMaxPerThread || d % 256 != 0 || p.tiles * 64 != d) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(256), 0, s, part, p, x, u, g, eps, M, d);
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_sum(const float* part, int splits, float* z, int M, int N, int ldp, hipStream_t s) {
+hipError_t launch_reduce_sum(const float* part, const SkinnyPlan& p, float* z, int M, int N, hipStream_t s) {
   const size_t n = (size_t)M * N;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, splits, z, M, N,
-                     ldp);
+  if (N > p.tiles * 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, p, z, M, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* h, int ldh, int M, int F,
+                                hipStream_t s) {
+  const size_t n = (size_t)M * F;
+  if (n == 0) return hipSuccess;
+  if (2 * F > p.tiles * 64 || F % 32 != 0 || ldh < F) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, p, h, ldh, M, F);
   return hipGetLastError();
 }
 

@@ -2,21 +2,26 @@
 // environment), A [M, K] bf16, W [N, K] bf16, fp32 accumulation.
 //
 // Decode streams every weight once per step, so the kernel is shaped for HBM
-// bandwidth: a 256-thread workgroup owns 64 output columns (four
-// v_mfma_f32_16x16x32_bf16 column blocks) and one K slice; its four waves
-// take interleaved 32-wide k-steps of that slice, so together they read each
-// weight row as one contiguous stream, and they combine their partial tiles
-// through LDS at the end.  Each lane loads its weight fragment straight from
-// global memory as 16-byte loads; several k-steps are in flight per wave.
-// Each workgroup starts at a different point of its K range so that the
-// workgroups running at the same time spread their activation reads over L2.  The activations (<= 128 x K bf16) are read through L2, where
-// every workgroup of the GPU shares them; owning 64 columns amortises each
-// activation fragment over four weight fragments.
-//
-// The K split is kept small (1-4 slices): with one slice the epilogue is
-// applied in place (SwiGLU to bf16 h, or a plain fp32 store); with more, fp32
-// partial sums go to a buffer that one consumer kernel reduces in a fixed
-// order, so results are bitwise deterministic.
+// bandwidth and for balance over the CUs:
+//  - One persistent 256-thread workgroup per CU.  The work is cut into units
+//    of 64 output columns x 256 K.  Whole column tiles are dealt out one per
+//    workgroup per round; the tiles left over after the last full round are
+//    split into their units, and each workgroup takes an equal contiguous run
+//    of those (stream-K), so every workgroup streams the same weight bytes.
+//  - Every tile segment a workgroup finishes is written as an fp32 partial
+//    sum into a slot of a partial buffer; the consumer kernel adds a tile's
+//    slots in slot order, so results are bitwise deterministic.  The slot of
+//    a segment and a tile's slot count follow from the plan in closed form.
+//  - Within a unit the four waves take one 64-wide K step (a 128-byte line of
+//    every row) each, as two v_mfma_f32_16x16x32_bf16 k-steps; each load
+//    instruction reads one contiguous 64-byte half line of 16 rows.  Loads
+//    run a ring of units ahead of the MFMAs (about 96 KB of weights in flight
+//    per CU), pinned in issue order.
+//  - The activations (<= 128 x K bf16) are read through L2, where every
+//    workgroup of the GPU shares them; owning 64 columns amortises each
+//    activation fragment over four weight fragments.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -24,112 +29,98 @@ namespace vla {
 
 namespace {
 
-constexpr int COLS = 64;      // output columns per workgroup
-constexpr int NW = 4;         // waves per workgroup
+constexpr int COLS = 64;   // output columns per tile
+constexpr int NW = 4;      // waves per workgroup
+constexpr int UNIT_K = 256;
+#define PIN() __builtin_amdgcn_sched_barrier(0)
 
-template <int MB, int U, int EPI>
-__global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a, int kslice) {
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
+
+// Ring depth (units in flight) by the number of 16-row blocks of A.
+template <int MB>
+constexpr int ring_depth() { return MB <= 4 ? 3 : 2; }
+
+template <int MB>
+__global__ __launch_bounds__(64 * NW, 1) void skinny_kernel(SkinnyArgs a, SkinnyPlan p) {
   extern __shared__ float red[];  // [NW][MB*16][COLS]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * COLS;
-  const int s = blockIdx.y;
-  const int kb = s * kslice;
-  const int ke = min(a.K, kb + kslice);
-  const int r16 = lane & 15, g = lane >> 4;
-
-  const bf16_t* wp[4];
-#pragma unroll
-  for (int nb = 0; nb < 4; ++nb) wp[nb] = a.W + (size_t)(n0 + nb * 16 + r16) * a.K + 8 * g;
-  const bf16_t* ap[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) ap[mb] = a.A + (size_t)min(mb * 16 + r16, a.M - 1) * a.lda + 8 * g;
-
-  f32x4 acc[MB][4];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // Wave w takes the k-steps kb + 32 * (NW * j + w), j < Tw, starting at a
-  // workgroup-dependent rotation so that concurrently running workgroups read
-  // different parts of the shared activations.  Batches of U k-steps are
-  // double-buffered in registers: batch b+1 is in flight while the MFMAs of
-  // batch b run.
-  const int T = (ke - kb + 31) / 32;
-  const int Tw = T > wave ? (T - wave + NW - 1) / NW : 0;
-  const int rot = Tw > 0 ? (int)((blockIdx.x * 37u + blockIdx.y * 11u) % (unsigned)Tw) : 0;
-  const int nbatch = Tw / U;
-  uint4 wv[2][U][4], av[2][U][MB];
-  auto kstep = [&](int j) {
-    j += rot;
-    j = j >= Tw ? j - Tw : j;
-    return kb + 32 * (NW * j + wave);
-  };
-  auto load = [&](int b, uint4 (&w)[U][4], uint4 (&x)[U][MB]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = kstep(b * U + u);
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) w[u][nb] = *reinterpret_cast<const uint4*>(wp[nb] + k);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) x[u][mb] = *reinterpret_cast<const uint4*>(ap[mb] + k);
-    }
-  };
-  auto math = [&](const uint4 (&w)[U][4], const uint4 (&x)[U][MB]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x[u][mb]), as_bf16x8(w[u][nb]), acc[mb][nb]);
-  };
-  if (nbatch > 0) load(0, wv[0], av[0]);
-  int b = 0;
-  for (; b + 2 <= nbatch; b += 2) {
-    load(b + 1, wv[1], av[1]);
-    math(wv[0], av[0]);
-    if (b + 2 < nbatch) load(b + 2, wv[0], av[0]);
-    math(wv[1], av[1]);
-  }
-  if (b < nbatch) math(wv[0], av[0]);
-  for (int j = nbatch * U; j < Tw; ++j) {
-    const int k = kstep(j);
-    uint4 w1[4], x1[MB];
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) w1[nb] = *reinterpret_cast<const uint4*>(wp[nb] + k);
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) x1[mb] = *reinterpret_cast<const uint4*>(ap[mb] + k);
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x1[mb]), as_bf16x8(w1[nb]), acc[mb][nb]);
-  }
-
-  // acc[mb][nb][r] is row mb*16 + 4g + r, column nb*16 + r16 of the tile
+  constexpr int D = ring_depth<MB>();
   constexpr int ROWS = MB * 16;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: keeps load offsets scalar
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int G = p.G, g = blockIdx.x, C = p.chunks;
+
+  // this workgroup's units: whole tiles first, then its stream-K run
+  const int n_dp = (p.dp_tiles / G) * C;
+  const int U = (p.tiles - p.dp_tiles) * C;
+  const int su0 = (int)(((long long)g * U) / G), su1 = (int)(((long long)(g + 1) * U) / G);
+  const int total = n_dp + (su1 - su0);
+  auto unit_tile = [&](int i, int& chunk) {
+    if (i < n_dp) {
+      chunk = i % C;
+      return (i / C) * G + g;
+    }
+    const int su = su0 + i - n_dp;
+    chunk = su % C;
+    return p.dp_tiles + su / C;
+  };
+
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
+  // byte offsets: weight row nb*16 + r16 of a tile (tile base added per unit), A row mb*16 + r16;
+  // lane (r16, g4) reads 16 bytes at 16 g4 of each 64-byte half of the row's 128-byte K step
+  uint32_t woff[4], aoff[MB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+  for (int nb = 0; nb < 4; ++nb) woff[nb] = (uint32_t)(((nb * 16 + r16) * a.K + 8 * g4) * 2);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) aoff[mb] = (uint32_t)((min(mb * 16 + r16, a.M - 1) * a.lda + 8 * g4) * 2);
+
+  uint4 wr[D][4][2], ar[D][MB][2];
+  // issue the loads of unit i (clamped: past the end the last unit is re-read) into ring slot S
+  auto load = [&](int i, uint4 (&w)[4][2], uint4 (&x)[MB][2]) {
+    int chunk;
+    const int tile = unit_tile(min(i, total - 1), chunk);
+    const int k0 = chunk * UNIT_K + wave * 64;
+    const int wbase = (tile * COLS * a.K + k0) * 2;  // wave-uniform
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[(wave * ROWS + mb * 16 + 4 * g + r) * COLS + nb * 16 + r16] = acc[mb][nb][r];
-  __syncthreads();
-
-  if constexpr (EPI == kSkinnySwiGlu) {
-    // columns [0, 32) of the tile are gate rows, [32, 64) the matching up rows
-    for (int e = threadIdx.x; e < ROWS * 32; e += 64 * NW) {
-      const int row = e / 32, c = e % 32;
-      if (row >= a.M) break;
-      float gs = 0.f, us = 0.f;
+      for (int h = 0; h < 2; ++h)
+        w[nb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, woff[nb] + 64 * h, wbase, 0));
 #pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        gs += red[(w * ROWS + row) * COLS + c];
-        us += red[(w * ROWS + row) * COLS + c + 32];
-      }
-      a.h[(size_t)row * a.ldh + n0 / 2 + c] = f2bf(gs / (1.f + expf(-gs)) * us);
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        x[mb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, aoff[mb] + 64 * h, k0 * 2, 0));
+  };
+
+  f32x4 acc[MB][4];
+  auto zero = [&]() {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  zero();
+
+  // Reduce the four waves' partial tiles through LDS and store the segment's
+  // partial sum into its slot.  acc[mb][nb][r] is row mb*16 + 4*g4 + r,
+  // column nb*16 + r16 of the tile.
+  auto flush = [&](int tile) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[(wave * ROWS + mb * 16 + 4 * g4 + r) * COLS + nb * 16 + r16] = acc[mb][nb][r];
+    __syncthreads();
+    int slot = 0;
+    if (tile >= p.dp_tiles) {
+      const int t = tile - p.dp_tiles;
+      slot = g - skinny_owner(t * C, U, G);
     }
-  } else {
-    float* out = a.part + (size_t)s * a.M * a.N + n0;
+    float* out = a.part + (size_t)slot * a.M * a.N + tile * COLS;
     for (int e = threadIdx.x; e < ROWS * COLS; e += 64 * NW) {
       const int row = e / COLS, c = e % COLS;
       if (row >= a.M) break;
@@ -138,56 +129,80 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a, int kslic
       for (int w = 0; w < NW; ++w) v += red[(w * ROWS + row) * COLS + c];
       out[(size_t)row * a.N + c] = v;
     }
+    __syncthreads();
+    zero();
+  };
+
+  // unit i: MFMAs on ring slot i % D, after issuing the loads of unit i + D - 1
+  auto step = [&](int i, uint4 (&w)[4][2], uint4 (&x)[MB][2], uint4 (&wn)[4][2], uint4 (&xn)[MB][2]) {
+    load(i + D - 1, wn, xn);  // unconditional, so the wait counts are the same on every path
+    PIN();
+    if (i < total) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x[mb][h]), as_bf16x8(w[nb][h]), acc[mb][nb]);
+      int c0, c1;
+      const int t0 = unit_tile(i, c0);
+      if (i + 1 >= total || unit_tile(i + 1, c1) != t0) flush(t0);
+    }
+    PIN();
+  };
+
+  if (total <= 0) return;
+#pragma unroll
+  for (int j = 0; j < D - 1; ++j) load(j, wr[j], ar[j]);
+  for (int i = 0; i < total; i += D) {
+    // ring slots rotate statically: unit i + j uses slot j, its loads go to slot (j + D - 1) % D
+#pragma unroll
+    for (int j = 0; j < D; ++j) step(i + j, wr[j], ar[j], wr[(j + D - 1) % D], ar[(j + D - 1) % D]);
   }
 }
 
-template <int MB, int U, int EPI>
-hipError_t launch_one(const SkinnyArgs& a, int kslice, hipStream_t st) {
-  const dim3 grid(a.N / COLS, a.splits), block(64 * NW);
+template <int MB>
+hipError_t launch_mb(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t st) {
   const size_t lds = (size_t)NW * MB * 16 * COLS * sizeof(float);
   static bool attr_set = false;  // dynamic LDS above 64 KB must be allowed once per kernel
   if (!attr_set && lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<MB, U, EPI>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<MB>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((skinny_kernel<MB, U, EPI>), grid, block, lds, st, a, kslice);
+  hipLaunchKernelGGL((skinny_kernel<MB>), dim3(p.G), dim3(64 * NW), lds, st, a, p);
   return hipGetLastError();
-}
-
-template <int MB, int U>
-hipError_t launch_mb(const SkinnyArgs& a, int kslice, SkinnyEpilogue epi, hipStream_t st) {
-  if (epi == kSkinnySwiGlu) return launch_one<MB, U, kSkinnySwiGlu>(a, kslice, st);
-  return launch_one<MB, U, kSkinnyPartial>(a, kslice, st);
 }
 
 }  // namespace
 
-int skinny_splits(int M, int N, int K, int max_splits) {
-  (void)M;
-  // enough workgroups for ~2 per CU without splitting K more than 4 ways
-  const int blocks = N / COLS;
-  int s = (512 + blocks - 1) / blocks;
-  if (s > 4) s = 4;
-  if (s > max_splits) s = max_splits;
-  const int ksteps = K / 32;
-  if (s > ksteps) s = ksteps;
-  return s < 1 ? 1 : s;
+SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots) {
+  SkinnyPlan p{};
+  p.tiles = N / COLS;
+  p.chunks = K / UNIT_K;
+  for (int G = workgroups; G >= 1; --G) {
+    p.G = G;
+    p.dp_tiles = (p.tiles / G) * G;
+    const int U = (p.tiles - p.dp_tiles) * p.chunks;
+    if (U > 0 && U < G) continue;  // every workgroup of a stream-K run needs at least one unit
+    p.slots = 1;
+    for (int t = p.dp_tiles; t < p.tiles; ++t) p.slots = std::max(p.slots, skinny_slots(p, t));
+    if (p.slots <= max_slots) break;
+  }
+  return p;
 }
 
-hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t st, SkinnyEpilogue epi) {
+hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (a.M > 128 || a.N % COLS != 0 || a.K % 32 != 0 || a.splits < 1 || a.lda % 8 != 0) return hipErrorInvalidValue;
-  if (epi == kSkinnySwiGlu && a.splits != 1) return hipErrorInvalidValue;
-  // K slice: a multiple of 32, splits * kslice >= K
-  const int ksteps = a.K / 32;
-  const int kslice = ((ksteps + a.splits - 1) / a.splits) * 32;
+  if (a.M > 128 || a.N % COLS != 0 || a.K % UNIT_K != 0 || a.lda % 8 != 0 || p.tiles != a.N / COLS ||
+      p.chunks != a.K / UNIT_K || p.G < 1 || (long long)a.N * a.K >= (1ll << 30))
+    return hipErrorInvalidValue;
   const int mb = (a.M + 15) / 16;
-  if (mb <= 1) return launch_mb<1, 4>(a, kslice, epi, st);
-  if (mb <= 2) return launch_mb<2, 4>(a, kslice, epi, st);
-  if (mb <= 4) return launch_mb<4, 2>(a, kslice, epi, st);
-  return launch_mb<8, 1>(a, kslice, epi, st);
+  if (mb <= 1) return launch_mb<1>(a, p, st);
+  if (mb <= 2) return launch_mb<2>(a, p, st);
+  if (mb <= 4) return launch_mb<4>(a, p, st);
+  return launch_mb<8>(a, p, st);
 }
 
 }  // namespace vla

@@ -57,25 +57,39 @@ struct GemmArgs {
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s);
 
-// Skinny split-K GEMM for decode: C = A[M, K] * W[N, K]^T for M <= 128 rows.
-// Requires N % 64 == 0, K % 32 == 0.  kSkinnyPartial writes the fp32 partial
-// sum of K slice s to part[s, m, n]; kSkinnySwiGlu (one slice only) treats W
-// as interleaved [gate; up] blocks of 32 rows and writes
-// h[m, j] = bf16(silu(gate_j) * up_j).
-enum SkinnyEpilogue { kSkinnyPartial = 0, kSkinnySwiGlu = 1 };
+// Skinny GEMM for decode: C = A[M, K] * W[N, K]^T for M <= 128 rows, N % 64 == 0,
+// K % 256 == 0, N * K < 2^30.  The work is cut into units of 64 columns
+// (a tile) x 256 K; a persistent grid of `G` workgroups takes whole tiles one
+// per workgroup per round while at least G remain (tiles [0, dp_tiles)), then
+// splits the remaining tiles' units evenly, in tile order, over the G
+// workgroups.  Each tile segment a workgroup computes is stored as an fp32
+// partial sum at part[slot, m, n]; tile t has skinny_slots(plan, t) slots and
+// its result is their sum in slot order.
 struct SkinnyArgs {
   const bf16_t* A;
   int lda;
   int M;
   const bf16_t* W;
   int N, K;
-  float* part;  // [splits, M, N]
-  int splits;
-  bf16_t* h;    // kSkinnySwiGlu output [M, ldh]
-  int ldh;
+  float* part;  // [plan.slots, M, N]
 };
-int skinny_splits(int M, int N, int K, int max_splits);
-hipError_t launch_skinny(const SkinnyArgs& a, hipStream_t s, SkinnyEpilogue epi = kSkinnyPartial);
+struct SkinnyPlan {
+  int tiles;     // N / 64
+  int chunks;    // K / 256 units per tile
+  int G;         // workgroups
+  int dp_tiles;  // tiles computed whole (a multiple of G)
+  int slots;     // most partial slots of any tile
+};
+// workgroup whose stream-K run holds unit u of U (runs [g U / G, (g+1) U / G))
+__host__ __device__ inline int skinny_owner(int u, int U, int G) { return ((u + 1) * G + U - 1) / U - 1; }
+__host__ __device__ inline int skinny_slots(const SkinnyPlan& p, int tile) {
+  if (tile < p.dp_tiles) return 1;
+  const int U = (p.tiles - p.dp_tiles) * p.chunks, t = tile - p.dp_tiles;
+  return skinny_owner((t + 1) * p.chunks - 1, U, p.G) - skinny_owner(t * p.chunks, U, p.G) + 1;
+}
+// The plan for `workgroups` workgroups, with fewer if needed to keep every tile within `max_slots`.
+SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots);
+hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t s);
 
 // Elementwise / reduction kernels
 struct EmbedArgs {
@@ -102,18 +116,22 @@ hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float*
                                    const float* g, float eps, int B, int d, int vocab,
                                    uint32_t* flags, hipStream_t s);
 
-// x[m] += sum_s part[s, m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d)
-hipError_t launch_reduce_residual_norm(const float* part, int splits, float* x, bf16_t* u,
+// Consumers of a skinny GEMM's partial sums (plan `p`, partial rows of p.tiles * 64 floats):
+// x[m] += C[m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d)
+hipError_t launch_reduce_residual_norm(const float* part, const SkinnyPlan& p, float* x, bf16_t* u,
                                        const float* g, float eps, int M, int d, hipStream_t s);
-
-// z[m, n] = sum_s part[s, m, n] for n < N; partial rows have stride ldp >= N
-hipError_t launch_reduce_sum(const float* part, int splits, float* z, int M, int N, int ldp, hipStream_t s);
+// z[m, n] = C[m, n] for n < N (z rows of N floats)
+hipError_t launch_reduce_sum(const float* part, const SkinnyPlan& p, float* z, int M, int N, hipStream_t s);
+// h[m, j] = bf16(silu(C[m, gate_j]) * C[m, up_j]) for j < F, C's columns interleaved
+// as [32 gate; 32 up] blocks (column 64 (j / 32) + j % 32 and 32 further)
+hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* h, int ldh, int M, int F,
+                                hipStream_t s);
 
 // Decode: sum QKV partials, RoPE at position env_prefix[b] + step - 1, store q
 // and append K/V of the new token to the page pool.
 struct DecodeQkvArgs {
   const float* part;
-  int splits;
+  SkinnyPlan plan;
   bf16_t* q;
   KvCache kv;
   const int32_t* page_table;

@@ -74,7 +74,7 @@ int check_config(const vla_config* c, Dims* o) {
   D.H = c->n_heads;
   D.hd = c->head_dim;
   D.F = c->d_ffn;
-  D.Fp = round_up(c->d_ffn, 64);
+  D.Fp = round_up(c->d_ffn, 256);  // decode GEMM K units are 256 wide
   D.A = c->action_bins;
   D.Ap = round_up(c->action_bins, 64);
   D.V = c->vocab;
@@ -145,6 +145,8 @@ struct vla_model {
   std::vector<int> prefix_host;  // L_b of the last prefill
   int layer_limit;               // test hook: run only the first layer_limit layers (0 = all)
   float scale;
+  // decode GEMM work splits (one persistent workgroup per CU)
+  SkinnyPlan plan_qkv, plan_o, plan_gu, plan_d, plan_head;
   // live profiling
   struct ProfSlot {
     hipEvent_t a, b;
@@ -257,10 +259,9 @@ int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t
   const Dims& D = m->D;
   for (int r0 = 0; r0 < R; r0 += kSkinnyRows) {
     const int rows = std::min(kSkinnyRows, R - r0);
-    SkinnyArgs sa{u + (size_t)r0 * D.d, D.d, rows, m->lm_act, D.Ap, D.d, m->part, 0};
-    sa.splits = skinny_splits(rows, D.Ap, D.d, kMaxSplits);
-    VLA_CK(launch_skinny(sa, s));
-    VLA_CK(launch_reduce_sum(m->part, sa.splits, logits + (size_t)r0 * D.A, rows, D.A, D.Ap, s));
+    SkinnyArgs sa{u + (size_t)r0 * D.d, D.d, rows, m->lm_act, D.Ap, D.d, m->part};
+    VLA_CK(launch_skinny(sa, m->plan_head, s));
+    VLA_CK(launch_reduce_sum(m->part, m->plan_head, logits + (size_t)r0 * D.A, rows, D.A, s));
   }
   return VLA_OK;
 }
@@ -405,6 +406,17 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
     return fail(VLA_EWORKSPACE, "workspace smaller than vla_workspace_size()");
   }
   m->scale = 1.0f / std::sqrt((float)D.hd);
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+      cus = 256;
+    m->plan_qkv = skinny_plan(3 * D.d, D.d, cus, kMaxSplits);
+    m->plan_o = skinny_plan(D.d, D.d, cus, kMaxSplits);
+    m->plan_gu = skinny_plan(2 * D.Fp, D.d, cus, kMaxSplits);
+    m->plan_d = skinny_plan(D.d, D.Fp, cus, kMaxSplits);
+    m->plan_head = skinny_plan(D.Ap, D.d, cus, kMaxSplits);
+  }
   set_meta_views(m, m->meta_dev);
   m->meta_pending = false;
   m->state_batch = 0;
@@ -528,26 +540,24 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
       for (int b = 0; b < B; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + i);
       for (int l = 0; l < D.L; ++l) {
         const LayerW& w = m->lw[l];
-        SkinnyArgs sq{m->u, D.d, B, w.wqkv, 3 * D.d, D.d, m->part, 0};
-        sq.splits = skinny_splits(B, sq.N, sq.K, kMaxSplits);
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, s));
-        DecodeQkvArgs qa{m->part, sq.splits, m->q, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, m->rope,
-                         B, D.d, D.H, D.hd};
+        SkinnyArgs sq{m->u, D.d, B, w.wqkv, 3 * D.d, D.d, m->part};
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, m->plan_qkv, s));
+        DecodeQkvArgs qa{m->part, m->plan_qkv, m->q, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i,
+                         m->rope, B, D.d, D.H, D.hd};
         VLA_CK(launch_decode_qkv(qa, s));
         DecodeAttnArgs da{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, B, D.d, D.H, D.hd,
                           m->scale};
         PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
-        SkinnyArgs so{m->u, D.d, B, w.wo, D.d, D.d, m->part, 0};
-        so.splits = skinny_splits(B, so.N, so.K, kMaxSplits);
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, s));
-        VLA_CK(launch_reduce_residual_norm(m->part, so.splits, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
-        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part, 1, m->h, D.Fp};
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, s, kSkinnySwiGlu));
-        SkinnyArgs sd{m->h, D.Fp, B, w.wd, D.d, D.Fp, m->part, 0};
-        sd.splits = skinny_splits(B, sd.N, sd.K, kMaxSplits);
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, s));
+        SkinnyArgs so{m->u, D.d, B, w.wo, D.d, D.d, m->part};
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, m->plan_o, s));
+        VLA_CK(launch_reduce_residual_norm(m->part, m->plan_o, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
+        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part};
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, m->plan_gu, s));
+        VLA_CK(launch_reduce_swiglu(m->part, m->plan_gu, m->h, D.Fp, B, D.Fp, s));
+        SkinnyArgs sd{m->h, D.Fp, B, w.wd, D.d, D.Fp, m->part};
+        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, m->plan_d, s));
         const float* gnext = (l + 1 < D.L) ? m->lw[l + 1].attn_norm : m->final_norm;
-        VLA_CK(launch_reduce_residual_norm(m->part, sd.splits, m->x, m->u, gnext, eps, B, D.d, s));
+        VLA_CK(launch_reduce_residual_norm(m->part, m->plan_d, m->x, m->u, gnext, eps, B, D.d, s));
       }
       int rc = head_logits(m, m->u, B, m->logits_dec, s);
       if (rc) return rc;

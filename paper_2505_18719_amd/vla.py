@@ -239,13 +239,14 @@ def debug_gemm(A: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
     return C
 
 
-def debug_skinny(A: torch.Tensor, W: torch.Tensor, splits: int) -> torch.Tensor:
+def debug_skinny(A: torch.Tensor, W: torch.Tensor, workgroups: int = 256) -> torch.Tensor:
     lib = load_library()
     M, K = A.shape
     N = W.shape[0]
-    scratch = torch.empty(splits * M * N, dtype=torch.float32, device=A.device)
+    scratch = torch.empty(16 * M * N, dtype=torch.float32, device=A.device)
     C = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    _check(lib.vla_debug_skinny(_ptr(A), K, _ptr(W), M, N, K, splits, _ptr(scratch), _ptr(C), _stream(A.device)))
+    _check(lib.vla_debug_skinny(_ptr(A), K, _ptr(W), M, N, K, workgroups, _ptr(scratch), _ptr(C),
+                                _stream(A.device)))
     return C
 
 

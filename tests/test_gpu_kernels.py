@@ -25,8 +25,10 @@ def _check_matmul(C, A, W, label):
     assert bool((err <= bound).all())
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 384, 320), (513, 1408, 704), (256, 256, 4096),
-                                   (1000, 3072, 1024)])
+# (M, N, K): tiny, ragged M and N with more tiles than CUs per workgroup round
+# or fewer, several rounds per workgroup, long K
+@pytest.mark.parametrize("M,N,K", [(1, 64, 128), (300, 384, 384), (513, 1408, 768), (256, 256, 4096),
+                                   (1000, 3072, 1024), (4100, 16448, 256)])
 def test_prefill_gemm_matches_float64(M, N, K):
     from paper_2505_18719_amd import vla
     A, W = _rand_bf16((M, K), 1), _rand_bf16((N, K), 2, 0.02)
@@ -46,14 +48,27 @@ def test_prefill_gemm_7b_shape_sampled_rows():
     _check_matmul(C[rows], A[rows], W, "gemm-7b-sampled")
 
 
+# (N, K, workgroups): whole tiles only, stream-K only, whole tiles plus a
+# stream-K remainder, a single unit, and the 7B shapes on 256 workgroups
 @pytest.mark.parametrize("M", [1, 7, 16, 33, 64, 128])
-@pytest.mark.parametrize("N,K,splits", [(256, 4096, 16), (1024, 704, 3), (768, 256, 1), (4096, 11008, 4)])
-def test_decode_skinny_gemm_matches_float64(M, N, K, splits):
+@pytest.mark.parametrize("N,K,wg", [(256, 4096, 256), (1024, 768, 3), (768, 256, 5), (64, 256, 1),
+                                    (4096, 11008, 256), (12288, 4096, 256), (22016, 4096, 256), (4096, 4096, 256)])
+def test_decode_skinny_gemm_matches_float64(M, N, K, wg):
     from paper_2505_18719_amd import vla
     A, W = _rand_bf16((M, K), 5 + M), _rand_bf16((N, K), 6, 0.02)
-    C = vla.debug_skinny(A, W, splits)
+    C = vla.debug_skinny(A, W, wg)
     torch.cuda.synchronize()
-    _check_matmul(C, A, W, f"skinny s={splits}")
+    _check_matmul(C, A, W, f"skinny wg={wg}")
+
+
+@pytest.mark.parametrize("N,K", [(22016, 4096), (4096, 11008), (12288, 4096)])
+def test_decode_skinny_gemm_is_deterministic(N, K):
+    from paper_2505_18719_amd import vla
+    A, W = _rand_bf16((64, K), 11), _rand_bf16((N, K), 12, 0.02)
+    C1 = vla.debug_skinny(A, W, 256)
+    C2 = vla.debug_skinny(A, W, 256)
+    torch.cuda.synchronize()
+    assert torch.equal(C1, C2)
 
 
 @pytest.mark.parametrize("T", [1.0, 1.5])
