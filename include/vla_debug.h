@@ -12,17 +12,26 @@
 extern "C" {
 #endif
 
-/* Prefill MFMA GEMM: C[M, N] fp32 = A[M, K] bf16 (row stride lda) * W[N, K]^T bf16.
+/* Prefill MFMA GEMM: C[M, N] fp32 = A[M, K] bf16 (row-major, row stride lda)
+ * * W[N, K]^T bf16, W in frag layout (vla_debug_pack_frag).
  * Requires K % 64 == 0, N % 64 == 0, lda % 8 == 0. */
 int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, float* C,
                    void* stream);
 
-/* Decode skinny GEMM: C[M, N] fp32 = A * W^T for M <= 128 on a persistent
- * grid of at most `workgroups` workgroups; tile segments' partial sums go to
- * `scratch` (16 * M * N floats).  Requires N % 64 == 0, K % 256 == 0,
- * N * K < 2^30. */
-int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
+/* Decode skinny GEMM: C[M, N] fp32 = A * W^T for M <= 128, A [M, K] and W
+ * [N, K] in frag layout, on a persistent grid of at most `workgroups`
+ * workgroups; tile segments' partial sums go to `scratch` (16 * M * N floats).
+ * Requires N % 64 == 0, K % 256 == 0, N * K < 2^30. */
+int vla_debug_skinny(const void* A, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
                      float* scratch, float* C, void* stream);
+
+/* Repack a row-major bf16 matrix src [rows, K] (row stride ld) into the frag
+ * layout the GEMMs read: 16 x 32 blocks of 1 KB, block (r / 16, k / 32) at
+ * element ((r / 16) * (K / 32) + k / 32) * 512, and in it the 8 elements
+ * (r, 8 (k % 32 / 8) .. + 8) at element 8 (r % 16 + 16 (k % 32 / 8)).  dst holds
+ * ceil(rows / 16) * 16 * K elements; rows past `rows` are left unwritten.
+ * Requires K % 32 == 0. */
+int vla_debug_pack_frag(const void* src, int32_t rows, int32_t K, int32_t ld, void* dst, void* stream);
 
 /* Sampler on given logits z[B, A] at step `step` of gumbel[B, n_actions, A]:
  * writes tokens / logp / entropy / logits at [b, step] exactly as

@@ -282,7 +282,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
     float t = 0.f;
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) t += op[gg][i];
-    a.o[(size_t)b * a.d + head * HD + i] = f2bf(t / s);
+    a.o[frag_index(b, head * HD + i, a.d)] = f2bf(t / s);  // frag layout: A operand of the O projection
   }
 }
 

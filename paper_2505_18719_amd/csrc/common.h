@@ -70,6 +70,16 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_b
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Fragment-major ("frag") layout of a bf16 matrix X[R][K], K % 32 == 0: 16 x 32
+// blocks of 1 KB, block (r / 16, k / 32) at element ((r/16) * (K/32) + k/32) * 512,
+// and inside a block the 16 bytes that lane l of an MFMA 16x16x32 operand holds
+// (row l % 16, K elements 8 (l / 16) .. + 8) at 16 l bytes.  One 64-lane 16-byte
+// load of a block reads 1 KB of contiguous memory and leaves every lane holding
+// its fragment.  Storage covers ceil(R / 16) * 16 rows.
+__host__ __device__ __forceinline__ size_t frag_index(int r, int k, int K) {
+  return ((((size_t)(r >> 4) * (K >> 5) + (k >> 5)) << 6) + (r & 15) + (((k & 31) >> 3) << 4)) * 8 + (k & 7);
+}
+
 // 16-byte streaming load (data used once: weights during decode).
 __device__ __forceinline__ uint4 load_stream16(const void* p) {
   const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));

@@ -24,14 +24,20 @@ int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t
   return launch_gemm(g, kEpiStoreF32, static_cast<hipStream_t>(stream)) == hipSuccess ? VLA_OK : VLA_EHIP;
 }
 
-int vla_debug_skinny(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
+int vla_debug_skinny(const void* A, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
                      float* scratch, float* C, void* stream) {
   if (!A || !W || !C || !scratch || M < 0 || N <= 0 || K <= 0 || workgroups < 1) return VLA_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const SkinnyPlan p = skinny_plan(N, K, workgroups, 16);
-  SkinnyArgs a{static_cast<const bf16_t*>(A), lda, M, static_cast<const bf16_t*>(W), N, K, scratch};
+  SkinnyArgs a{static_cast<const bf16_t*>(A), M, static_cast<const bf16_t*>(W), N, K, scratch};
   if (launch_skinny(a, p, s) != hipSuccess) return VLA_EHIP;
   return launch_reduce_sum(scratch, p, C, M, N, s) == hipSuccess ? VLA_OK : VLA_EHIP;
+}
+
+int vla_debug_pack_frag(const void* src, int32_t rows, int32_t K, int32_t ld, void* dst, void* stream) {
+  if (!src || !dst || rows < 0 || K <= 0 || K % 32 != 0 || ld < K) return VLA_EINVAL;
+  PackArgs pa{static_cast<bf16_t*>(dst), rows, K, static_cast<const bf16_t*>(src), nullptr, ld, rows, K, kPackRows, 0};
+  return launch_pack_frag(pa, static_cast<hipStream_t>(stream)) == hipSuccess ? VLA_OK : VLA_EHIP;
 }
 
 int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, int32_t step, int32_t action_begin,

@@ -43,11 +43,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One wave per row: u = bf16(x * rsqrt(mean(x^2) + eps) * g).
+// One wave per row: u = bf16(x * rsqrt(mean(x^2) + eps) * g), row-major (row
+// stride ldu) or, with frag set, in frag layout of K = d.
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
                                                       const int32_t* __restrict__ rows,
                                                       const float* __restrict__ g, float eps,
-                                                      bf16_t* __restrict__ u, int ldu, int M, int d) {
+                                                      bf16_t* __restrict__ u, int ldu, int M, int d, int frag) {
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= M) return;
@@ -67,7 +68,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
     uint2 o;
     o.x = pack2bf(v.x * r * w.x, v.y * r * w.y);
     o.y = pack2bf(v.z * r * w.z, v.w * r * w.w);
-    *reinterpret_cast<uint2*>(ur + c) = o;
+    *reinterpret_cast<uint2*>(frag ? u + frag_index(i, c, d) : ur + c) = o;
   }
 }
 
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(256) void embed_token_norm_kernel(const int32_t* to
   n = 0;
   for (int c = threadIdx.x; c < d; c += 256, ++n) {
     x[(size_t)b * d + c] = v[n];
-    u[(size_t)b * d + c] = f2bf(v[n] * r * g[c]);
+    u[frag_index(b, c, d)] = f2bf(v[n] * r * g[c]);
   }
 }
 
@@ -141,7 +142,7 @@ __global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* 
     if (i < n) {
       const int c = threadIdx.x + 256 * i;
       x[(size_t)m * d + c] = v[i];
-      u[(size_t)m * d + c] = f2bf(v[i] * r * g[c]);
+      u[frag_index(m, c, d)] = f2bf(v[i] * r * g[c]);
     }
 }
 
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restr
   const int N = p.tiles * 64;
   const int cg = 64 * (j >> 5) + (j & 31);
   const float gs = skinny_sum(part, p, M, N, m, cg), us = skinny_sum(part, p, M, N, m, cg + 32);
-  h[(size_t)m * ldh + j] = f2bf(gs / (1.f + expf(-gs)) * us);
+  h[frag_index(m, j, ldh)] = f2bf(gs / (1.f + expf(-gs)) * us);
 }
 
 // One thread per rotary pair of q and k, and per pair of v features.
@@ -209,32 +210,38 @@ __global__ __launch_bounds__(256) void decode_qkv_kernel(DecodeQkvArgs a) {
 }
 
 // ------------------------------------------------------------------ repacking
-// q/k rows of each head reordered so that each 64-row block holds rotary
-// pairs 32 rows apart: block b = rows [32b, 32b+32) then [half+32b, half+32b+32).
-__global__ __launch_bounds__(256) void repack_qk_kernel(bf16_t* dst, const bf16_t* src, int d, int hd) {
-  const int r = blockIdx.x;  // destination row
-  const int head = r / hd, p = r % hd, half = hd / 2;
-  const int blk = p / 64, c = p % 64;
-  const int orig = head * hd + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32);
-  for (int k = threadIdx.x * 8; k < d; k += 256 * 8)
-    *reinterpret_cast<uint4*>(dst + (size_t)r * d + k) = *reinterpret_cast<const uint4*>(src + (size_t)orig * d + k);
-}
-
-// [gate; up] interleaved in blocks of 32 rows, zero rows past F.
-__global__ __launch_bounds__(256) void repack_gate_up_kernel(bf16_t* dst, const bf16_t* gate, const bf16_t* up,
-                                                             int F, int d) {
-  const int r = blockIdx.x;
-  const int j = 32 * (r / 64) + (r % 32);
-  const bf16_t* src = (j < F) ? ((r % 64) < 32 ? gate : up) + (size_t)j * d : nullptr;
-  for (int k = threadIdx.x * 8; k < d; k += 256 * 8)
-    *reinterpret_cast<uint4*>(dst + (size_t)r * d + k) =
-        src ? *reinterpret_cast<const uint4*>(src + k) : make_uint4(0, 0, 0, 0);
-}
-
-__global__ __launch_bounds__(256) void pad_cols_kernel(bf16_t* dst, const bf16_t* src, int cols, int cols_p) {
-  const int r = blockIdx.x;
-  for (int c = threadIdx.x; c < cols_p; c += 256)
-    dst[(size_t)r * cols_p + c] = c < cols ? src[(size_t)r * cols + c] : (bf16_t)0;
+// One 16-byte chunk (8 K elements) of destination row r per thread, written in
+// frag layout.  The source row (or a zero row) follows the packing mode:
+//  kPackRows:   source row r, rows >= src_rows zero, K elements >= src_cols zero
+//  kPackQk:     q/k rows of each head reordered so that each 64-row block holds
+//               rotary pairs 32 rows apart: block b = rows [32b, 32b+32) then
+//               [half+32b, half+32b+32)
+//  kPackGateUp: [gate; up] interleaved in blocks of 32 rows, zero rows past src_rows
+__global__ __launch_bounds__(256) void pack_frag_kernel(PackArgs a) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int kc = a.K / 8;
+  if (i >= (size_t)a.rows * kc) return;
+  const int r = (int)(i / kc), k = (int)(i % kc) * 8;
+  const bf16_t* src = nullptr;
+  if (a.mode == kPackRows) {
+    if (r < a.src_rows) src = a.src + (size_t)r * a.src_ld;
+  } else if (a.mode == kPackQk) {
+    const int hd = a.head_dim, head = r / hd, p = r % hd, half = hd / 2;
+    const int blk = p / 64, c = p % 64;
+    src = a.src + (size_t)(head * hd + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32)) * a.src_ld;
+  } else {
+    const int j = 32 * (r / 64) + (r % 32);
+    if (j < a.src_rows) src = ((r % 64) < 32 ? a.src : a.src2) + (size_t)j * a.src_ld;
+  }
+  bf16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (src && k + e < a.src_cols) ? src[k + e] : (bf16_t)0;
+  uint4 o;
+  o.x = v[0] | (uint32_t(v[1]) << 16);
+  o.y = v[2] | (uint32_t(v[3]) << 16);
+  o.z = v[4] | (uint32_t(v[5]) << 16);
+  o.w = v[6] | (uint32_t(v[7]) << 16);
+  *reinterpret_cast<uint4*>(a.dst + frag_index(r, k, a.K)) = o;
 }
 
 __global__ void bf16_to_f32_kernel(float* dst, const bf16_t* src, int n) {
@@ -257,10 +264,11 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps, bf16_t* u,
-                          int ldu, int M, int d, hipStream_t s) {
+                          int ldu, int M, int d, hipStream_t s, bool frag) {
   if (M <= 0) return hipSuccess;
-  if (d % 4 != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d);
+  if (d % 4 != 0 || (frag && d % 32 != 0)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d,
+                     frag ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -304,19 +312,12 @@ hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_repack_qk(bf16_t* dst, const bf16_t* src, int d, int hd, hipStream_t s) {
-  hipLaunchKernelGGL(repack_qk_kernel, dim3(d), dim3(256), 0, s, dst, src, d, hd);
-  return hipGetLastError();
-}
-
-hipError_t launch_repack_gate_up(bf16_t* dst, const bf16_t* gate, const bf16_t* up, int F, int Fp, int d,
-                                 hipStream_t s) {
-  hipLaunchKernelGGL(repack_gate_up_kernel, dim3(2 * Fp), dim3(256), 0, s, dst, gate, up, F, d);
-  return hipGetLastError();
-}
-
-hipError_t launch_pad_cols(bf16_t* dst, const bf16_t* src, int rows, int cols, int cols_p, hipStream_t s) {
-  hipLaunchKernelGGL(pad_cols_kernel, dim3(rows), dim3(256), 0, s, dst, src, cols, cols_p);
+hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  if (a.K % 32 != 0 || a.src_cols > a.K || !a.dst || !a.src || (a.mode == kPackGateUp && !a.src2))
+    return hipErrorInvalidValue;
+  const size_t n = (size_t)a.rows * (a.K / 8);
+  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

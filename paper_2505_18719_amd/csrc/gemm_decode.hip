@@ -12,11 +12,13 @@
 //    sum into a slot of a partial buffer; the consumer kernel adds a tile's
 //    slots in slot order, so results are bitwise deterministic.  The slot of
 //    a segment and a tile's slot count follow from the plan in closed form.
-//  - Within a unit the four waves take one 64-wide K step (a 128-byte line of
-//    every row) each, as two v_mfma_f32_16x16x32_bf16 k-steps; each load
-//    instruction reads one contiguous 64-byte half line of 16 rows.  Loads
-//    run a ring of units ahead of the MFMAs (about 96 KB of weights in flight
-//    per CU), pinned in issue order.
+//  - Within a unit the four waves take one 64-wide K step each, as two
+//    v_mfma_f32_16x16x32_bf16 k-steps.  Weights and activations are both in
+//    frag layout, so every load instruction reads one contiguous 1 KB block
+//    that leaves each lane holding its MFMA fragment (the number of memory
+//    requests per byte is what bounds this kernel).  Loads run a ring of units
+//    ahead of the MFMAs (about 96 KB of weights in flight per CU), pinned in
+//    issue order.
 //  - The activations (<= 128 x K bf16) are read through L2, where every
 //    workgroup of the GPU shares them; owning 64 columns amortises each
 //    activation fragment over four weight fragments.
@@ -68,31 +70,28 @@ __global__ __launch_bounds__(64 * NW, 1) void skinny_kernel(SkinnyArgs a, Skinny
 
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
-  // byte offsets: weight row nb*16 + r16 of a tile (tile base added per unit), A row mb*16 + r16;
-  // lane (r16, g4) reads 16 bytes at 16 g4 of each 64-byte half of the row's 128-byte K step
-  uint32_t woff[4], aoff[MB];
-#pragma unroll
-  for (int nb = 0; nb < 4; ++nb) woff[nb] = (uint32_t)(((nb * 16 + r16) * a.K + 8 * g4) * 2);
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) aoff[mb] = (uint32_t)((min(mb * 16 + r16, a.M - 1) * a.lda + 8 * g4) * 2);
+  // W and A are in frag layout: the fragment of block (row block, K block) is
+  // 1 KB at ((row block) * K/32 + K block) * 1024, lane l's 16 bytes at 16 l
+  const uint32_t loff = lane * 16;
+  const int KB = a.K / 32;
 
   uint4 wr[D][4][2], ar[D][MB][2];
-  // issue the loads of unit i (clamped: past the end the last unit is re-read) into ring slot S
+  // issue the loads of unit i (clamped: past the end the last unit is re-read) into a ring slot;
+  // the wave takes K blocks 8 chunk + 2 wave + h, h = 0, 1
   auto load = [&](int i, uint4 (&w)[4][2], uint4 (&x)[MB][2]) {
     int chunk;
     const int tile = unit_tile(min(i, total - 1), chunk);
-    const int k0 = chunk * UNIT_K + wave * 64;
-    const int wbase = (tile * COLS * a.K + k0) * 2;  // wave-uniform
+    const int kb = 8 * chunk + 2 * wave;
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-        w[nb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, woff[nb] + 64 * h, wbase, 0));
+        w[nb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, loff, ((tile * 4 + nb) * KB + kb + h) * 1024, 0));
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-        x[mb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, aoff[mb] + 64 * h, k0 * 2, 0));
+        x[mb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, loff, (mb * KB + kb + h) * 1024, 0));
   };
 
   f32x4 acc[MB][4];
@@ -195,7 +194,7 @@ SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots) {
 
 hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (a.M > 128 || a.N % COLS != 0 || a.K % UNIT_K != 0 || a.lda % 8 != 0 || p.tiles != a.N / COLS ||
+  if (a.M > 128 || a.N % COLS != 0 || a.K % UNIT_K != 0 || p.tiles != a.N / COLS ||
       p.chunks != a.K / UNIT_K || p.G < 1 || (long long)a.N * a.K >= (1ll << 30))
     return hipErrorInvalidValue;
   const int mb = (a.M + 15) / 16;

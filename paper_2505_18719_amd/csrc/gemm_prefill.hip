@@ -84,20 +84,30 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int wm = wave >> 1, wn = wave & 1;
 
   // Loads: per K step each thread brings 8 16-byte chunks of the A tile and 8
-  // of the W tile into VGPRs (row 32 j + tid / 8, chunk tid % 8: each wave
-  // instruction reads 8 whole 128-byte rows) and later writes them to LDS at
-  // physical chunk (tid % 8) ^ swz(row).
+  // of the W tile into VGPRs and later writes them to LDS at physical chunk
+  // c ^ swz(row).  A (row-major): chunk j is row 32 j + tid / 8, K chunk
+  // tid % 8, so each wave instruction reads 8 whole 128-byte rows.  W (frag
+  // layout, see frag_index): wave w's chunk j is lane l's 16 bytes of 1 KB
+  // block (16-row block 2 j + w / 2, K block w % 2) of the step, i.e. row
+  // 16 (2 j + w / 2) + l % 16, K chunk 4 (w % 2) + l / 16: each wave
+  // instruction reads one contiguous 1 KB block.
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
-  uint32_t voff[2][8];
+  uint32_t voffA[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int row = j * 32 + (tid >> 3);
-    voff[0][j] = (uint32_t)((min(m0 + row, M - 1) * a.lda + (tid & 7) * 8) * 2);
-    voff[1][j] = (uint32_t)((min(n0 + row, N - 1) * K + (tid & 7) * 8) * 2);
-  }
-  // uint4 index of this thread's chunk in an operand tile (rows 32 j + tid / 8: + 256 j)
+  for (int j = 0; j < 8; ++j)
+    voffA[j] = (uint32_t)((min(m0 + j * 32 + (tid >> 3), M - 1) * a.lda + (tid & 7) * 8) * 2);
+  // W rows past N (whole 16-row blocks, N % 64 == 0) are clamped to the last block
+  const int wv = tid >> 6, wl = tid & 63;
+  const int KB = K / 32;
+  uint32_t voffW[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    voffW[j] = (uint32_t)((min((n0 >> 4) + 2 * j + (wv >> 1), N / 16 - 1) * KB + (wv & 1)) * 1024 + wl * 16);
+  // uint4 index of this thread's chunk in the A tile (chunk j: + 256 j) and in the W tile (chunk j: + 256 j)
   const int widx = (tid >> 3) * CH + ((tid & 7) ^ ((tid >> 4) & 7));
+  const int wrow = (wv >> 1) * 16 + (wl & 15);
+  const int widx_w = wrow * CH + (((wv & 1) * 4 + (wl >> 4)) ^ swz(wrow));
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -107,23 +117,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // fragment rows wm*128 + 32 i + l31 (A) and wn*128 + 32 i + l31 (W): all share swz = swz(l31)
   const int l31 = lane & 31;
-  int roff[2][4], rswz[2][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ra = wm * 128 + i * 32 + l31, rw = wn * 128 + i * 32 + l31;
-    roff[0][i] = ra * CH;
-    roff[1][i] = BM * CH + rw * CH;
-    rswz[0][i] = swz(ra);
-    rswz[1][i] = swz(rw);
-  }
+  const int roff[2] = {(wm * 128 + l31) * CH, BM * CH + (wn * 128 + l31) * CH};
+  const int rswz = swz(l31);
   uint4* ring = &lds[0][0][0];
   bf16x8 fr[2][2][4];
   uint4 rg[2][16];  // register stages: [parity][A chunks 0-7, W chunks 0-7]
   auto read = [&](int ord, int r, int st, int q) {
     const int o = kReadO[ord][r], i = kReadB[ord][r];
-    const int c = (2 * q + (lane >> 5)) ^ rswz[o][i];
-    fr[q & 1][o][i] = as_bf16x8(ring[st * (2 * BM * CH) + roff[o][i] + c]);
+    const int c = (2 * q + (lane >> 5)) ^ rswz;
+    fr[q & 1][o][i] = as_bf16x8(ring[st * (2 * BM * CH) + roff[o] + i * 32 * CH + c]);
   };
   auto mfma = [&](int ord, int t, int q) {
     const int i = kMfmaI[ord][t], j = kMfmaJ[ord][t];
@@ -132,12 +136,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int nk = K / BK;
   // load chunk c (0..15: A 0-7, W 8-15) of K step ks into register stage p
   auto gload = [&](int p, int c, int ks) {
-    const int o = c >> 3, j = c & 7;
-    rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(o ? rsW : rsA, voff[o][j], ks * BK * 2, 0));
+    const int j = c & 7;
+    if (c < 8)
+      rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, voffA[j], ks * BK * 2, 0));
+    else
+      rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, voffW[j], ks * BK * 32, 0));
   };
   auto lwrite = [&](int p, int c, int st) {
-    const int o = c >> 3, j = c & 7;
-    ring[st * (2 * BM * CH) + o * (BM * CH) + j * 256 + widx] = rg[p][c];
+    const int j = c & 7;
+    if (c < 8)
+      ring[st * (2 * BM * CH) + j * 256 + widx] = rg[p][c];
+    else
+      ring[st * (2 * BM * CH) + BM * CH + j * 256 + widx_w] = rg[p][c];
   };
 
   // Pipeline: step s's tiles are loaded into register stage s % 2 during step
@@ -326,7 +336,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (a.K % BK != 0 || a.N % 64 != 0 || a.lda % 8 != 0) return hipErrorInvalidValue;
+  if (a.K % BK != 0 || a.N % 64 != 0 || a.lda % 8 != 0 || (long long)a.N * a.K * 2 >= (1ll << 31))
+    return hipErrorInvalidValue;
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   const dim3 grid(tm * tn), block(NT);
   switch (epi) {

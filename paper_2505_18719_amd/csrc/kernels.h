@@ -38,9 +38,9 @@ enum GemmEpilogue {
 };
 
 struct GemmArgs {
-  const bf16_t* A;
+  const bf16_t* A;  // row-major, row stride lda
   int lda;
-  const bf16_t* W;
+  const bf16_t* W;  // [N, K] in frag layout
   int M, N, K;
   float* C;
   int ldc;
@@ -66,12 +66,11 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s);
 // partial sum at part[slot, m, n]; tile t has skinny_slots(plan, t) slots and
 // its result is their sum in slot order.
 struct SkinnyArgs {
-  const bf16_t* A;
-  int lda;
+  const bf16_t* A;  // [M, K] in frag layout
   int M;
-  const bf16_t* W;
+  const bf16_t* W;  // [N, K] in frag layout
   int N, K;
-  float* part;  // [plan.slots, M, N]
+  float* part;      // [plan.slots, M, N]
 };
 struct SkinnyPlan {
   int tiles;     // N / 64
@@ -107,22 +106,24 @@ struct EmbedArgs {
 };
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 
-// u[i] = bf16(rmsnorm(x[rows ? rows[i] : i]) * g), i < M
+// u[i] = bf16(rmsnorm(x[rows ? rows[i] : i]) * g), i < M; u row-major with row
+// stride ldu, or in frag layout (K = d) when `frag` is set
 hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps,
-                          bf16_t* u, int ldu, int M, int d, hipStream_t s);
+                          bf16_t* u, int ldu, int M, int d, hipStream_t s, bool frag = false);
 
-// Decode step input: x[b] = emb[tok[b]], u[b] = bf16(rmsnorm(x[b]) * g)
+// Decode step input: x[b] = emb[tok[b]], u[b] = bf16(rmsnorm(x[b]) * g), u in frag layout
 hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float* x, bf16_t* u,
                                    const float* g, float eps, int B, int d, int vocab,
                                    uint32_t* flags, hipStream_t s);
 
 // Consumers of a skinny GEMM's partial sums (plan `p`, partial rows of p.tiles * 64 floats):
-// x[m] += C[m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d)
+// x[m] += C[m, :];  u[m] = bf16(rmsnorm(x[m]) * g)   (M rows of d; u in frag layout)
 hipError_t launch_reduce_residual_norm(const float* part, const SkinnyPlan& p, float* x, bf16_t* u,
                                        const float* g, float eps, int M, int d, hipStream_t s);
 // z[m, n] = C[m, n] for n < N (z rows of N floats)
 hipError_t launch_reduce_sum(const float* part, const SkinnyPlan& p, float* z, int M, int N, hipStream_t s);
-// h[m, j] = bf16(silu(C[m, gate_j]) * C[m, up_j]) for j < F, C's columns interleaved
+// h[m, j] = bf16(silu(C[m, gate_j]) * C[m, up_j]) for j < F (h in frag layout, K = ldh),
+// C's columns interleaved
 // as [32 gate; 32 up] blocks (column 64 (j / 32) + j % 32 and 32 further)
 hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* h, int ldh, int M, int F,
                                 hipStream_t s);
@@ -160,7 +161,7 @@ hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
 
 struct DecodeAttnArgs {
   const bf16_t* q;  // [B, d]
-  bf16_t* o;        // [B, d]
+  bf16_t* o;        // [B, d] in frag layout
   KvCache kv;
   const int32_t* page_table;
   int max_pages;
@@ -192,12 +193,17 @@ struct SamplerArgs {
 };
 hipError_t launch_sampler(const SamplerArgs& a, hipStream_t s);
 
-// Weight repacking (one-time, at create)
-hipError_t launch_repack_qk(bf16_t* dst, const bf16_t* src, int d, int head_dim, hipStream_t s);
-hipError_t launch_repack_gate_up(bf16_t* dst, const bf16_t* gate, const bf16_t* up, int F, int Fp,
-                                 int d, hipStream_t s);
-hipError_t launch_pad_cols(bf16_t* dst, const bf16_t* src, int rows, int cols, int cols_p,
-                           hipStream_t s);
+// Weight packing (one-time, at create): dst [rows, K] in frag layout (see frag_index)
+enum PackMode { kPackRows = 0, kPackQk = 1, kPackGateUp = 2 };
+struct PackArgs {
+  bf16_t* dst;
+  int rows, K;
+  const bf16_t* src;   // row-major source, row stride src_ld
+  const bf16_t* src2;  // up projection (kPackGateUp)
+  int src_ld, src_rows, src_cols;
+  int mode, head_dim;
+};
+hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

@@ -12,6 +12,7 @@
 #include <string>
 #include <vector>
 
+#include "common.h"
 #include "kernels.h"
 #include "vla.h"
 
@@ -38,6 +39,7 @@ constexpr int kQBlock = 64;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up(int v, int a) { return (v + a - 1) / a * a; }
+size_t round_up_z(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Sizes derived from a configuration.
 struct Dims {
@@ -184,14 +186,14 @@ void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
   }
   M.rope = L.take<float2>((size_t)D.Smax * (D.hd / 2));
   M.x = L.take<float>(D.Mmax * D.d);
-  M.u = L.take<bf16_t>(D.Mmax * D.d);
+  M.u = L.take<bf16_t>(round_up_z(D.Mmax, 16) * D.d);  // frag layout in decode covers whole 16-row blocks
   M.q = L.take<bf16_t>(D.Mmax * D.d);
-  M.h = L.take<bf16_t>(D.Mmax * D.Fp);
+  M.h = L.take<bf16_t>(round_up_z(D.Mmax, 16) * D.Fp);
   M.part = L.take<float>((size_t)kMaxSplits * kSkinnyRows * D.Nmax);
   M.logits_pre = L.take<float>((size_t)D.Bmax * D.A);
   M.logits_dec = L.take<float>((size_t)D.Bmax * D.A);
   M.logits_tf = L.take<float>((size_t)D.Bmax * D.nact * D.A);
-  M.u_head = L.take<bf16_t>((size_t)D.Bmax * D.nact * D.d);
+  M.u_head = L.take<bf16_t>(round_up_z((size_t)D.Bmax * D.nact, 16) * D.d);
   M.next_tok = L.take<int32_t>(D.Bmax);
   M.flags = L.take<uint32_t>(4);
   M.meta_dev = L.take<int32_t>(D.meta_ints);
@@ -259,7 +261,7 @@ int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t
   const Dims& D = m->D;
   for (int r0 = 0; r0 < R; r0 += kSkinnyRows) {
     const int rows = std::min(kSkinnyRows, R - r0);
-    SkinnyArgs sa{u + (size_t)r0 * D.d, D.d, rows, m->lm_act, D.Ap, D.d, m->part};
+    SkinnyArgs sa{u + frag_index(r0, 0, D.d), rows, m->lm_act, D.Ap, D.d, m->part};
     VLA_CK(launch_skinny(sa, m->plan_head, s));
     VLA_CK(launch_reduce_sum(m->part, m->plan_head, logits + (size_t)r0 * D.A, rows, D.A, s));
   }
@@ -361,7 +363,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     if (l + 1 < D.L) VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s));
   }
   const int R = tf ? B * D.nact : B;
-  VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s));
+  VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
   *out_rows = R;
   return VLA_OK;
 }
@@ -451,20 +453,24 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
   const bf16_t* emb = static_cast<const bf16_t*>(w->embed);
   const bf16_t* lm = static_cast<const bf16_t*>(w->lm_head);
   CREATE_CK(hipMemcpyAsync(m->emb, emb, (size_t)D.V * D.d * 2, hipMemcpyDeviceToDevice, s));
-  CREATE_CK(launch_fill_zero(m->lm_act, align_up((size_t)D.Ap * D.d * 2, 16), s));
-  CREATE_CK(hipMemcpyAsync(m->lm_act, lm + (size_t)cfg->action_begin * D.d, (size_t)D.A * D.d * 2,
-                           hipMemcpyDeviceToDevice, s));
+  // projection weights are stored in frag layout (see frag_index); the LM head keeps only the action rows
+  auto pack = [&](bf16_t* dst, int rows, int K, const void* src, int src_ld, int src_rows, int src_cols, int mode,
+                  const void* src2 = nullptr) {
+    PackArgs pa{dst, rows, K, static_cast<const bf16_t*>(src), static_cast<const bf16_t*>(src2), src_ld, src_rows,
+                src_cols, mode, D.hd};
+    return launch_pack_frag(pa, s);
+  };
+  CREATE_CK(pack(m->lm_act, D.Ap, D.d, lm + (size_t)cfg->action_begin * D.d, D.d, D.A, D.d, kPackRows));
   CREATE_CK(launch_bf16_to_f32(m->final_norm, static_cast<const bf16_t*>(w->final_norm), D.d, s));
   for (int l = 0; l < D.L; ++l) {
     LayerW& lw = m->lw[l];
-    CREATE_CK(launch_repack_qk(lw.wqkv, static_cast<const bf16_t*>(w->wq[l]), D.d, D.hd, s));
-    CREATE_CK(launch_repack_qk(lw.wqkv + (size_t)D.d * D.d, static_cast<const bf16_t*>(w->wk[l]), D.d, D.hd, s));
-    CREATE_CK(hipMemcpyAsync(lw.wqkv + (size_t)2 * D.d * D.d, w->wv[l], (size_t)D.d * D.d * 2,
-                             hipMemcpyDeviceToDevice, s));
-    CREATE_CK(hipMemcpyAsync(lw.wo, w->wo[l], (size_t)D.d * D.d * 2, hipMemcpyDeviceToDevice, s));
-    CREATE_CK(launch_repack_gate_up(lw.wgu, static_cast<const bf16_t*>(w->wgate[l]),
-                                    static_cast<const bf16_t*>(w->wup[l]), D.F, D.Fp, D.d, s));
-    CREATE_CK(launch_pad_cols(lw.wd, static_cast<const bf16_t*>(w->wdown[l]), D.d, D.F, D.Fp, s));
+    // [Wq; Wk; Wv] is 3d rows of one frag matrix: d is a multiple of 256, so each part starts on a block row
+    CREATE_CK(pack(lw.wqkv, D.d, D.d, w->wq[l], D.d, D.d, D.d, kPackQk));
+    CREATE_CK(pack(lw.wqkv + (size_t)D.d * D.d, D.d, D.d, w->wk[l], D.d, D.d, D.d, kPackQk));
+    CREATE_CK(pack(lw.wqkv + (size_t)2 * D.d * D.d, D.d, D.d, w->wv[l], D.d, D.d, D.d, kPackRows));
+    CREATE_CK(pack(lw.wo, D.d, D.d, w->wo[l], D.d, D.d, D.d, kPackRows));
+    CREATE_CK(pack(lw.wgu, 2 * D.Fp, D.d, w->wgate[l], D.d, D.F, D.d, kPackGateUp, w->wup[l]));
+    CREATE_CK(pack(lw.wd, D.d, D.Fp, w->wdown[l], D.F, D.d, D.F, kPackRows));
     CREATE_CK(launch_bf16_to_f32(lw.attn_norm, static_cast<const bf16_t*>(w->attn_norm[l]), D.d, s));
     CREATE_CK(launch_bf16_to_f32(lw.mlp_norm, static_cast<const bf16_t*>(w->mlp_norm[l]), D.d, s));
   }
@@ -540,7 +546,7 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
       for (int b = 0; b < B; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + i);
       for (int l = 0; l < D.L; ++l) {
         const LayerW& w = m->lw[l];
-        SkinnyArgs sq{m->u, D.d, B, w.wqkv, 3 * D.d, D.d, m->part};
+        SkinnyArgs sq{m->u, B, w.wqkv, 3 * D.d, D.d, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, m->plan_qkv, s));
         DecodeQkvArgs qa{m->part, m->plan_qkv, m->q, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i,
                          m->rope, B, D.d, D.H, D.hd};
@@ -548,13 +554,13 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
         DecodeAttnArgs da{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, B, D.d, D.H, D.hd,
                           m->scale};
         PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
-        SkinnyArgs so{m->u, D.d, B, w.wo, D.d, D.d, m->part};
+        SkinnyArgs so{m->u, B, w.wo, D.d, D.d, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, m->plan_o, s));
         VLA_CK(launch_reduce_residual_norm(m->part, m->plan_o, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
-        SkinnyArgs sg{m->u, D.d, B, w.wgu, 2 * D.Fp, D.d, m->part};
+        SkinnyArgs sg{m->u, B, w.wgu, 2 * D.Fp, D.d, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, m->plan_gu, s));
         VLA_CK(launch_reduce_swiglu(m->part, m->plan_gu, m->h, D.Fp, B, D.Fp, s));
-        SkinnyArgs sd{m->h, D.Fp, B, w.wd, D.d, D.Fp, m->part};
+        SkinnyArgs sd{m->h, B, w.wd, D.d, D.Fp, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, m->plan_d, s));
         const float* gnext = (l + 1 < D.L) ? m->lw[l + 1].attn_norm : m->final_norm;
         VLA_CK(launch_reduce_residual_norm(m->part, m->plan_d, m->x, m->u, gnext, eps, B, D.d, s));

@@ -25,7 +25,7 @@ FLAG_BAD_ACTION = 2
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
            "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy", "vla_last_error")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
-DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_sample", "vla_debug_read",
+DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
                  "vla_debug_set_layer_limit")
 
 
@@ -75,7 +75,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_destroy.restype = None
     lib.vla_last_error.restype = ctypes.c_char_p
     lib.vla_debug_gemm.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp]
-    lib.vla_debug_skinny.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
+    lib.vla_debug_skinny.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp]
+    lib.vla_debug_pack_frag.argtypes = [vp, i32, i32, i32, vp, vp]
     lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
     lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
     lib.vla_debug_set_layer_limit.argtypes = [vp, i32]
@@ -230,12 +231,22 @@ class VlaModel:
 
 
 # ------------------------------------------------------------------ test hooks
+def debug_pack_frag(X: torch.Tensor) -> torch.Tensor:
+    """Row-major bf16 [R, K] -> frag layout (flat, ceil(R/16)*16*K elements; pad rows zero)."""
+    lib = load_library()
+    R, K = X.shape
+    out = torch.zeros(((R + 15) // 16) * 16 * K, dtype=torch.bfloat16, device=X.device)
+    _check(lib.vla_debug_pack_frag(_ptr(X), R, K, X.stride(0), _ptr(out), _stream(X.device)))
+    return out
+
+
 def debug_gemm(A: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
     lib = load_library()
     M, K = A.shape
     N = W.shape[0]
+    Wf = debug_pack_frag(W)
     C = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    _check(lib.vla_debug_gemm(_ptr(A), K, _ptr(W), M, N, K, _ptr(C), _stream(A.device)))
+    _check(lib.vla_debug_gemm(_ptr(A), K, _ptr(Wf), M, N, K, _ptr(C), _stream(A.device)))
     return C
 
 
@@ -243,10 +254,10 @@ def debug_skinny(A: torch.Tensor, W: torch.Tensor, workgroups: int = 256) -> tor
     lib = load_library()
     M, K = A.shape
     N = W.shape[0]
+    Af, Wf = debug_pack_frag(A), debug_pack_frag(W)
     scratch = torch.empty(16 * M * N, dtype=torch.float32, device=A.device)
     C = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    _check(lib.vla_debug_skinny(_ptr(A), K, _ptr(W), M, N, K, workgroups, _ptr(scratch), _ptr(C),
-                                _stream(A.device)))
+    _check(lib.vla_debug_skinny(_ptr(Af), _ptr(Wf), M, N, K, workgroups, _ptr(scratch), _ptr(C), _stream(A.device)))
     return C
 
 
