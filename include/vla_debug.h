@@ -12,11 +12,9 @@
 extern "C" {
 #endif
 
-/* Prefill MFMA GEMM: C[M, N] fp32 = A[M, K] bf16 (row-major, row stride lda)
- * * W[N, K]^T bf16, W in frag layout (vla_debug_pack_frag).
- * Requires K % 64 == 0, N % 64 == 0, lda % 8 == 0. */
-int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, float* C,
-                   void* stream);
+/* Prefill MFMA GEMM: C[M, N] fp32 = A[M, K] bf16 * W[N, K]^T bf16, A and W in
+ * frag layout (vla_debug_pack_frag).  Requires K % 32 == 0, N % 64 == 0. */
+int vla_debug_gemm(const void* A, const void* W, int32_t M, int32_t N, int32_t K, float* C, void* stream);
 
 /* Decode skinny GEMM: C[M, N] fp32 = A * W^T for M <= 128, A [M, K] and W
  * [N, K] in frag layout, on a persistent grid of at most `workgroups`
@@ -43,7 +41,7 @@ int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, in
 /* Copy `bytes` of an internal buffer of the handle to `dst` (device):
  * which = 0 residual x fp32 [rows, d], 1 rotated q bf16 [rows, d], 2 / 3 the K / V
  * page pool of `layer` (bf16, page layouts of the KV cache), 4 the bf16
- * activation buffer [rows, d]. */
+ * activation buffer [rows, d] in frag layout (see vla_debug_pack_frag). */
 struct vla_model;
 int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream);
 

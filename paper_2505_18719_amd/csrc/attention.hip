@@ -200,10 +200,10 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
   // o[nb][r] = O(query qw + r16, feature nb*16 + 4g + r)
   if (qpos < L) {
     const float inv = 1.f / sum;
-    bf16_t* op = a.o + (size_t)(row0 + qpos) * a.d + head * HD + 4 * g;
+    // frag layout (the O projection's A operand): 4 consecutive features stay contiguous
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
-      *reinterpret_cast<uint2*>(op + nb * 16) =
+      *reinterpret_cast<uint2*>(a.o + frag_index(row0 + qpos, head * HD + nb * 16 + 4 * g, a.d)) =
           make_uint2(pack2bf(o[nb][0] * inv, o[nb][1] * inv), pack2bf(o[nb][2] * inv, o[nb][3] * inv));
   }
 }

@@ -9,12 +9,10 @@ using namespace vla;
 
 extern "C" {
 
-int vla_debug_gemm(const void* A, int32_t lda, const void* W, int32_t M, int32_t N, int32_t K, float* C,
-                   void* stream) {
+int vla_debug_gemm(const void* A, const void* W, int32_t M, int32_t N, int32_t K, float* C, void* stream) {
   if (!A || !W || !C || M < 0 || N < 0 || K <= 0) return VLA_EINVAL;
   GemmArgs g{};
   g.A = static_cast<const bf16_t*>(A);
-  g.lda = lda;
   g.W = static_cast<const bf16_t*>(W);
   g.M = M;
   g.N = N;

@@ -6,19 +6,21 @@
 // output tile; each wave owns 128 x 128 of it as 4 x 4 blocks of
 // v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane, held in AGPRs),
 // which halves the LDS operand traffic per MFMA compared with 128 x 64 wave
-// tiles.  K advances in steps of 64 through two 64 KB LDS stages.
+// tiles.
 //
-// The kernel is bound by how fast L2 delivers the A and W tiles to the CU
-// (128 flops per delivered byte at this tile size): the operand tiles are
-// brought in with plain 16-byte buffer loads into VGPRs, two K steps ahead,
-// and written to LDS one step ahead, so about 1.5 steps of loads are in flight
-// per CU; each wave load instruction reads 8 whole 128-byte rows.  Loads, LDS
-// writes, operand reads and MFMAs are interleaved one memory instruction per
-// MFMA in a pinned order.  16-byte chunks are XOR-swizzled by row so that the
-// MFMA operand reads (ds_read_b128, 32 rows x one chunk column) and the LDS
-// writes spread over the banks.  Workgroup ids are remapped so that the tiles
-// one XCD runs are contiguous in a grouped (8 tile-rows) order, which keeps A
-// panels and W panels resident in that XCD's L2.
+// The kernel is bound by how fast the A and W tiles reach LDS (128 flops per
+// delivered byte at this tile size), and a copy's round trip is long when its
+// lines miss L2, so the copies run four K steps of 32 ahead through a ring of
+// five 32 KB LDS stages (all 160 KB of LDS).  Both operands are in frag layout
+// (see frag_index), so a K step of either tile is sixteen 1 KB blocks and
+// every copy is one block moved whole by buffer_load ... lds (no VGPR round
+// trip, one contiguous 1 KB read per wave instruction).  An MFMA operand read
+// then takes 32 rows of a block pair as contiguous 256-byte runs, which is
+// free of LDS bank conflicts without any swizzle.  Copies, operand reads and
+// MFMAs are interleaved one memory instruction per MFMA in a pinned order.
+// Workgroup ids are remapped so that the tiles one XCD runs are contiguous in
+// a grouped (8 tile-rows) order, which keeps A panels and W panels resident
+// in that XCD's L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -26,9 +28,11 @@ namespace vla {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int NT = 256;        // 4 waves, 2 x 2, each owning 128 x 128 of the tile
-constexpr int CH = BK / 8;     // 16-byte chunks per tile row (128-byte rows)
+constexpr int NSTAGE = 5;      // LDS ring of K steps: A 16 KB + W 16 KB each
+constexpr int AHEAD = 4;       // K steps whose copies are in flight ahead of the one consumed
+constexpr int STAGE_U4 = 2 * 16 * 64;  // uint4 per stage: 2 operands x 16 blocks x 64 lanes
 constexpr int GROUP_M = 8;
 
 
@@ -46,13 +50,6 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
   tn = r / gm;
 }
 
-// Physical position of logical 16-byte chunk c of tile row r is c ^ swz(r).
-// An operand read takes one chunk column of 16 consecutive rows per 16 lanes;
-// two 128-byte rows share a 256-byte bank row, so the chunk index must take 8
-// distinct values over the 8 rows of each parity: then the 16 reads hit 16
-// distinct 16-byte bank groups.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
-
 // nothing may be scheduled across this point
 #define PIN() __builtin_amdgcn_sched_barrier(0)
 
@@ -69,45 +66,54 @@ __device__ constexpr int kMfmaJ[2][16] = {{0, 1, 0, 1, 2, 2, 0, 1, 2, 3, 3, 3, 0
 __device__ constexpr int kReadO[2][8] = {{0, 1, 0, 1, 0, 1, 0, 1}, {0, 0, 1, 1, 1, 1, 0, 0}};
 __device__ constexpr int kReadB[2][8] = {{0, 0, 1, 1, 2, 2, 3, 3}, {0, 1, 0, 1, 2, 3, 2, 3}};
 
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+// s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) >> 4) << 14) | (0xF << 8) | (0x7 << 4) | ((n) & 15))
+
+// 16 bytes per lane from a buffer straight into LDS (buffer_load_dwordx4 ... lds):
+// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS byte address
+// m0.  Issued through inline assembly so that the compiler does not treat it
+// as an LDS store (it would wait for every copy in flight before any later LDS
+// read); the kernel waits for the copies it consumes itself.
+__device__ __forceinline__ void dma16(uint32_t m0, uint32_t voff, __amdgpu_buffer_rsrc_t rsrc, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory");
+}
 
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds[2][2][BM * CH];  // [stage][A / W][256 rows x 8 chunks]
+  // [stage][A 16 blocks | W 16 blocks][64 lanes]: block b of an operand is its
+  // 16-row block b of the tile over the stage's 32 K
+  __shared__ uint4 lds[NSTAGE][STAGE_U4];
 
   int tm, tn;
   map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int M = a.M, N = a.N, K = a.K;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
+  const int KB = K / 32;
+  const int last_rb_a = (M + 15) / 16 - 1, last_rb_w = N / 16 - 1;
 
-  // Loads: per K step each thread brings 8 16-byte chunks of the A tile and 8
-  // of the W tile into VGPRs and later writes them to LDS at physical chunk
-  // c ^ swz(row).  A (row-major): chunk j is row 32 j + tid / 8, K chunk
-  // tid % 8, so each wave instruction reads 8 whole 128-byte rows.  W (frag
-  // layout, see frag_index): wave w's chunk j is lane l's 16 bytes of 1 KB
-  // block (16-row block 2 j + w / 2, K block w % 2) of the step, i.e. row
-  // 16 (2 j + w / 2) + l % 16, K chunk 4 (w % 2) + l / 16: each wave
-  // instruction reads one contiguous 1 KB block.
+  // Copies: wave w moves blocks 8 w .. 8 w + 7 of the step's 32 (A blocks
+  // 0-15, W blocks 16-31).  Row blocks past the matrix are clamped to its last
+  // one (their rows only feed outputs that are not stored).
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
-  uint32_t voffA[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-    voffA[j] = (uint32_t)((min(m0 + j * 32 + (tid >> 3), M - 1) * a.lda + (tid & 7) * 8) * 2);
-  // W rows past N (whole 16-row blocks, N % 64 == 0) are clamped to the last block
-  const int wv = tid >> 6, wl = tid & 63;
-  const int KB = K / 32;
-  uint32_t voffW[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-    voffW[j] = (uint32_t)((min((n0 >> 4) + 2 * j + (wv >> 1), N / 16 - 1) * KB + (wv & 1)) * 1024 + wl * 16);
-  // uint4 index of this thread's chunk in the A tile (chunk j: + 256 j) and in the W tile (chunk j: + 256 j)
-  const int widx = (tid >> 3) * CH + ((tid & 7) ^ ((tid >> 4) & 7));
-  const int wrow = (wv >> 1) * 16 + (wl & 15);
-  const int widx_w = wrow * CH + (((wv & 1) * 4 + (wl >> 4)) ^ swz(wrow));
+  // waves 0, 1 copy A blocks 0-15, waves 2, 3 W blocks 0-15 (wave-uniform choice, no branch)
+  const bool copies_a = wave < 2;
+  const __amdgpu_buffer_rsrc_t rsC = copies_a ? rsA : rsW;
+  const int rb0 = copies_a ? (m0 >> 4) : (n0 >> 4), rb_last = copies_a ? last_rb_a : last_rb_w;
+  const uint32_t voff = lane * 16;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)((lds_ptr_t*)&lds[0][0]);
+  auto copy = [&](int j, int st, int ks) {
+    const int b = wave * 8 + j;  // A block b, or W block b - 16
+    dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb0 + (b & 15), rb_last) * KB + ks) * 1024);
+  };
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -117,116 +123,84 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // fragment rows wm*128 + 32 i + l31 (A) and wn*128 + 32 i + l31 (W): all share swz = swz(l31)
-  const int l31 = lane & 31;
-  const int roff[2] = {(wm * 128 + l31) * CH, BM * CH + (wn * 128 + l31) * CH};
-  const int rswz = swz(l31);
-  uint4* ring = &lds[0][0][0];
-  bf16x8 fr[2][2][4];
-  uint4 rg[2][16];  // register stages: [parity][A chunks 0-7, W chunks 0-7]
+  // Operand fragments of MFMA k-step q (0, 1) for lane (l31, lhi): row
+  // 128 wm + 32 i + l31 of A (128 wn + ... of W) is row l31 % 16 of the
+  // operand's block 8 wm + 2 i + l31 / 16, and K 16 q + 8 lhi is its column
+  // group 2 q + lhi: the lane's 16 bytes sit at block lane (l31 % 16) + 16 (2 q + lhi).
+  const int l31 = lane & 31, lhi = lane >> 5;
+  const int fa = (wm * 8 + (l31 >> 4)) * 64 + (l31 & 15) + 16 * lhi;
+  const int fw = 16 * 64 + (wn * 8 + (l31 >> 4)) * 64 + (l31 & 15) + 16 * lhi;
+  const uint4* ring = &lds[0][0];
+  bf16x8 fr[2][2][4];  // [k-step][A / W][block]
   auto read = [&](int ord, int r, int st, int q) {
     const int o = kReadO[ord][r], i = kReadB[ord][r];
-    const int c = (2 * q + (lane >> 5)) ^ rswz;
-    fr[q & 1][o][i] = as_bf16x8(ring[st * (2 * BM * CH) + roff[o] + i * 32 * CH + c]);
+    fr[q][o][i] = as_bf16x8(ring[st * STAGE_U4 + (o ? fw : fa) + i * 128 + 32 * q]);
   };
   auto mfma = [&](int ord, int t, int q) {
     const int i = kMfmaI[ord][t], j = kMfmaJ[ord][t];
-    acc[i][j] = mfma32(fr[q & 1][0][i], fr[q & 1][1][j], acc[i][j]);
+    acc[i][j] = mfma32(fr[q][0][i], fr[q][1][j], acc[i][j]);
   };
+
+  // Pipeline over K steps of 32 (two MFMA k-steps of 16).  One step of a wave
+  // is 32 MFMAs with one memory instruction after 24 of them:
+  //   k-step 0: MFMAs 0-7 + the 8 operand reads of k-step 1 (row-major order),
+  //             MFMAs 8-15 + the 8 copies of step kt+AHEAD
+  //   k-step 1: MFMAs 0-7 (row blocks 0, 1), wait for this wave's copies of
+  //             step kt+1, barrier, MFMAs 8-15 + the 8 operand reads of
+  //             k-step 0 of step kt+1
+  // The order is pinned (the scheduler would otherwise hoist the barrier and
+  // its LDS wait above the MFMAs that are meant to hide them).  The stage
+  // filled in step kt was last read in step kt-1, before that step's barrier.
+  // Loads complete in order: with the copies of AHEAD-1 later steps allowed
+  // to stay in flight, the wait covers exactly the copies of step kt+1.
   const int nk = K / BK;
-  // load chunk c (0..15: A 0-7, W 8-15) of K step ks into register stage p
-  auto gload = [&](int p, int c, int ks) {
-    const int j = c & 7;
-    if (c < 8)
-      rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, voffA[j], ks * BK * 2, 0));
-    else
-      rg[p][c] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, voffW[j], ks * BK * 32, 0));
-  };
-  auto lwrite = [&](int p, int c, int st) {
-    const int j = c & 7;
-    if (c < 8)
-      ring[st * (2 * BM * CH) + j * 256 + widx] = rg[p][c];
-    else
-      ring[st * (2 * BM * CH) + BM * CH + j * 256 + widx_w] = rg[p][c];
-  };
-
-  // Pipeline: step s's tiles are loaded into register stage s % 2 during step
-  // s - 2, written to LDS stage s % 2 during the second half of step s - 1,
-  // and consumed in step s.  One step of a wave is 64 MFMAs with one memory
-  // instruction after each:
-  //   k-step 0: + the 8 operand reads of k-step 1, + loads 0-7 of step kt+2
-  //   k-step 1: + the 8 operand reads of k-step 2, + loads 8-15 of step kt+2
-  //   k-step 2: + the 8 operand reads of k-step 3 (row-major order), + LDS writes 0-7 of step kt+1
-  //   k-step 3: MFMAs 0-7 + LDS writes 8-15 of step kt+1, barrier,
-  //             MFMAs 8-15 + the 8 operand reads of k-step 0 of step kt+1
-  // The order is pinned.  LDS stage (kt+1) % 2 was last read in step kt-1,
-  // before that step's barrier.
-  auto step = [&](int kt, int P) {
-    const int cur = P, nxt = P ^ 1;
-    const int k2 = min(kt + 2, nk - 1);
-    PIN();
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+  for (int st = 0; st < AHEAD; ++st)
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        mfma(0, t, q);
-        read(0, t, cur, q + 1);
-        PIN();
-      }
-#pragma unroll
-      for (int t = 8; t < 16; ++t) {
-        mfma(0, t, q);
-        gload(P, 8 * q + t - 8, k2);
-        PIN();
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      mfma(0, t, 2);
-      read(1, t, cur, 3);
-      PIN();
-    }
-#pragma unroll
-    for (int t = 8; t < 16; ++t) {
-      mfma(0, t, 2);
-      lwrite(nxt, t - 8, nxt);
-      PIN();
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      mfma(1, t, 3);
-      lwrite(nxt, t + 8, nxt);
-      PIN();
-    }
-    __syncthreads();
-    PIN();
-#pragma unroll
-    for (int t = 8; t < 16; ++t) {
-      mfma(1, t, 3);
-      read(0, t - 8, nxt, 0);
-      PIN();
-    }
-  };
-
-#pragma unroll
-  for (int c = 0; c < 16; ++c) gload(0, c, 0);
-#pragma unroll
-  for (int c = 0; c < 16; ++c) gload(1, c, min(1, nk - 1));
-#pragma unroll
-  for (int c = 0; c < 16; ++c) lwrite(0, c, 0);
+    for (int j = 0; j < 8; ++j) copy(j, st, min(st, nk - 1));
+  WAIT_VMCNT(8 * (AHEAD - 1));
   __syncthreads();
   PIN();
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
+  for (int r = 0; r < 8; ++r) {  // same order as in the loop, so the loop's waits hold on entry
     read(0, r, 0, 0);
     PIN();
   }
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    step(kt, 0);
-    step(kt + 1, 1);
+  int cur = 0, fill = AHEAD;  // ring stages of steps kt and kt + AHEAD
+  for (int kt = 0; kt < nk; ++kt) {
+    const int nxt = cur + 1 == NSTAGE ? 0 : cur + 1;
+    const int kfill = min(kt + AHEAD, nk - 1);  // past the end the last step is re-copied
+    PIN();
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      mfma(0, t, 0);
+      read(1, t, cur, 1);
+      PIN();
+    }
+#pragma unroll
+    for (int t = 8; t < 16; ++t) {
+      mfma(0, t, 0);
+      copy(t - 8, fill, kfill);
+      PIN();
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      mfma(1, t, 1);
+      PIN();
+    }
+    WAIT_VMCNT(8 * (AHEAD - 1));   // this wave's copies of step kt+1 have landed
+    __syncthreads();               // ... and everyone's
+    PIN();
+#pragma unroll
+    for (int t = 8; t < 16; ++t) {
+      mfma(1, t, 1);
+      read(0, t - 8, nxt, 0);
+      PIN();
+    }
+    cur = nxt;
+    fill = fill + 1 == NSTAGE ? 0 : fill + 1;
   }
-  if (kt < nk) step(kt, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   // ---------------------------------------------------------------- epilogue
@@ -235,8 +209,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   // time, and then writes the epilogue's outputs with contiguous stores.
   // acc[i][j][r] holds row i*32 + 8*(r/4) + 4*lhi + r%4 and column j*32 + l31
   // of the wave tile; in LDS the float4 chunk q of row rl sits at q ^ (rl%16).
-  float* st = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (128 * 64);
-  const int lhi = lane >> 5;
+  float* st = reinterpret_cast<float*>(&lds[0][0]) + wave * (128 * 64);
+  // (l31, lhi as in the main loop)
   const int wrow0 = m0 + wm * 128;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -284,7 +258,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
           float o[4];
 #pragma unroll
           for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
-          *reinterpret_cast<uint2*>(a.H + (size_t)row * a.ldh + c0 / 2 + 4 * q) =
+          *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
               make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
         } else {  // kEpiQkvRope
           const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
@@ -336,7 +310,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (a.K % BK != 0 || a.N % 64 != 0 || a.lda % 8 != 0 || (long long)a.N * a.K * 2 >= (1ll << 31))
+  // frag-layout operands, 32-bit byte offsets into them
+  if (a.K % BK != 0 || a.N % 64 != 0 || (long long)((a.M + 15) / 16) * 16 * a.K * 2 >= (1ll << 31) ||
+      (long long)a.N * a.K * 2 >= (1ll << 31))
     return hipErrorInvalidValue;
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   const dim3 grid(tm * tn), block(NT);

@@ -33,13 +33,13 @@ struct RowMeta {
 enum GemmEpilogue {
   kEpiStoreF32 = 0,  // C[m, n] = acc                         (fp32, ldc)
   kEpiResidual = 1,  // C[m, n] += acc                        (fp32 residual stream, ldc)
-  kEpiSwiGlu = 2,    // H[m, j] = bf16(silu(gate) * up)  for W = interleaved [gate; up] blocks of 32 rows
+  kEpiSwiGlu = 2,    // H[m, j] = bf16(silu(gate) * up)  for W = interleaved [gate; up] blocks of 32 rows;
+                     //   H in frag layout with K = ldh
   kEpiQkvRope = 3,   // rotate q, k by RoPE, store q bf16 [M, d] and K/V into the page pool
 };
 
 struct GemmArgs {
-  const bf16_t* A;  // row-major, row stride lda
-  int lda;
+  const bf16_t* A;  // [M, K] in frag layout
   const bf16_t* W;  // [N, K] in frag layout
   int M, N, K;
   float* C;
@@ -147,7 +147,7 @@ hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s);
 // Attention
 struct PrefillAttnArgs {
   const bf16_t* q;  // [M, d]
-  bf16_t* o;        // [M, d]
+  bf16_t* o;        // [M, d] in frag layout
   KvCache kv;
   const int32_t* page_table;
   int max_pages;

@@ -338,12 +338,13 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
                m->env_prefix, m->env_prompt_off, Mi, D.d, D.nvis, D.nact, D.V, m->flags};
   VLA_CK(launch_embed(ea, s));
   const float eps = m->cfg.rms_eps;
-  VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s));
+  // the prefill GEMMs read their activations (u, attention output, h) in frag layout
+  VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
   const int n_layers = m->layer_limit > 0 ? std::min(m->layer_limit, D.L) : D.L;
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     GemmArgs g{};
-    g.A = m->u; g.lda = D.d; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
+    g.A = m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
     g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
     g.d_model = D.d; g.n_heads = D.H; g.head_dim = D.hd;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 3.0 * D.d, D.d), launch_gemm(g, kEpiQkvRope, s));
@@ -351,16 +352,17 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
                        nq, D.d, D.H, D.hd, m->scale};
     PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, attn_flops, launch_attn_prefill(pa, s));
     GemmArgs go{};
-    go.A = m->u; go.lda = D.d; go.W = w.wo; go.M = Mi; go.N = D.d; go.K = D.d; go.C = m->x; go.ldc = D.d;
+    go.A = m->u; go.W = w.wo; go.M = Mi; go.N = D.d; go.K = D.d; go.C = m->x; go.ldc = D.d;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.d), launch_gemm(go, kEpiResidual, s));
-    VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, w.mlp_norm, eps, m->u, D.d, Mi, D.d, s));
+    VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, w.mlp_norm, eps, m->u, D.d, Mi, D.d, s, true));
     GemmArgs gg{};
-    gg.A = m->u; gg.lda = D.d; gg.W = w.wgu; gg.M = Mi; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = m->h; gg.ldh = D.Fp;
+    gg.A = m->u; gg.W = w.wgu; gg.M = Mi; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = m->h; gg.ldh = D.Fp;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
     GemmArgs gd{};
-    gd.A = m->h; gd.lda = D.Fp; gd.W = w.wd; gd.M = Mi; gd.N = D.d; gd.K = D.Fp; gd.C = m->x; gd.ldc = D.d;
+    gd.A = m->h; gd.W = w.wd; gd.M = Mi; gd.N = D.d; gd.K = D.Fp; gd.C = m->x; gd.ldc = D.d;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
-    if (l + 1 < D.L) VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s));
+    if (l + 1 < D.L)
+      VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
   }
   const int R = tf ? B * D.nact : B;
   VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));

@@ -74,7 +74,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_destroy.argtypes = [vp]
     lib.vla_destroy.restype = None
     lib.vla_last_error.restype = ctypes.c_char_p
-    lib.vla_debug_gemm.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp]
+    lib.vla_debug_gemm.argtypes = [vp, vp, i32, i32, i32, vp, vp]
     lib.vla_debug_skinny.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp]
     lib.vla_debug_pack_frag.argtypes = [vp, i32, i32, i32, vp, vp]
     lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
@@ -244,9 +244,9 @@ def debug_gemm(A: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
     lib = load_library()
     M, K = A.shape
     N = W.shape[0]
-    Wf = debug_pack_frag(W)
+    Af, Wf = debug_pack_frag(A), debug_pack_frag(W)
     C = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    _check(lib.vla_debug_gemm(_ptr(A), K, _ptr(Wf), M, N, K, _ptr(C), _stream(A.device)))
+    _check(lib.vla_debug_gemm(_ptr(Af), _ptr(Wf), M, N, K, _ptr(C), _stream(A.device)))
     return C
 
 
