@@ -24,11 +24,12 @@ int vla_debug_skinny(const void* A, const void* W, int32_t M, int32_t N, int32_t
                      float* scratch, float* C, void* stream);
 
 /* Repack a row-major bf16 matrix src [rows, K] (row stride ld) into the frag
- * layout the GEMMs read: 16 x 32 blocks of 1 KB, block (r / 16, k / 32) at
- * element ((r / 16) * (K / 32) + k / 32) * 512, and in it the 8 elements
- * (r, 8 (k % 32 / 8) .. + 8) at element 8 (r % 16 + 16 (k % 32 / 8)).  dst holds
- * ceil(rows / 16) * 16 * K elements; rows past `rows` are left unwritten.
- * Requires K % 32 == 0. */
+ * layout the GEMMs read: 16 x 32 blocks of 1 KB; 16-row block r / 16 holds
+ * K / 32 + 1 consecutive blocks (the last one spare), K block k / 32 at
+ * element ((r / 16) * (K / 32 + 1) + k / 32) * 512, and in it the 8 elements
+ * (r, 8 (k % 32 / 8) .. + 8) at element 8 (r % 16 + 16 (k % 32 / 8)).  dst
+ * holds ceil(rows / 16) * (K / 32 + 1) * 512 elements; rows past `rows` and
+ * the spare blocks are left unwritten.  Requires K % 32 == 0. */
 int vla_debug_pack_frag(const void* src, int32_t rows, int32_t K, int32_t ld, void* dst, void* stream);
 
 /* Sampler on given logits z[B, A] at step `step` of gumbel[B, n_actions, A]:

@@ -71,19 +71,20 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_b
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Fragment-major ("frag") layout of a bf16 matrix X[R][K], K % 32 == 0: 16 x 32
-// blocks of 1 KB, block (r / 16, k / 32) at element ((r/16) * (K/32) + k/32) * 512,
-// and inside a block the 16 bytes that lane l of an MFMA 16x16x32 operand holds
-// (row l % 16, K elements 8 (l / 16) .. + 8) at 16 l bytes.  One 64-lane 16-byte
-// load of a block reads 1 KB of contiguous memory and leaves every lane holding
-// its fragment.  Storage covers ceil(R / 16) * 16 rows.
-__host__ __device__ __forceinline__ size_t frag_index(int r, int k, int K) {
-  return ((((size_t)(r >> 4) * (K >> 5) + (k >> 5)) << 6) + (r & 15) + (((k & 31) >> 3) << 4)) * 8 + (k & 7);
+// blocks of 1 KB.  The blocks of 16-row block r / 16 are consecutive, K block
+// k / 32 at element ((r/16) * frag_kb(K) + k/32) * 512, and one spare block
+// ends each 16-row block so that equal K blocks of consecutive 16-row blocks
+// are not a power-of-two distance apart (they would share memory channels).
+// Inside a block, the 16 bytes that lane l of an MFMA 16x16x32 operand holds
+// (row l % 16, K elements 8 (l / 16) .. + 8) are at 16 l bytes.  One 64-lane
+// 16-byte load of a block reads 1 KB of contiguous memory and leaves every
+// lane holding its fragment.  Storage: frag_elems(R, K) elements.
+__host__ __device__ __forceinline__ int frag_kb(int K) { return (K >> 5) + 1; }
+__host__ __device__ __forceinline__ size_t frag_elems(size_t R, int K) {
+  return ((R + 15) >> 4) * (size_t)frag_kb(K) * 512;
 }
-
-// 16-byte streaming load (data used once: weights during decode).
-__device__ __forceinline__ uint4 load_stream16(const void* p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  return make_uint4(v[0], v[1], v[2], v[3]);
+__host__ __device__ __forceinline__ size_t frag_index(int r, int k, int K) {
+  return ((((size_t)(r >> 4) * frag_kb(K) + (k >> 5)) << 6) + (r & 15) + (((k & 31) >> 3) << 4)) * 8 + (k & 7);
 }
 
 }  // namespace vla

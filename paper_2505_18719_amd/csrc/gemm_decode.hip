@@ -71,9 +71,9 @@ __global__ __launch_bounds__(64 * NW, 1) void skinny_kernel(SkinnyArgs a, Skinny
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
   // W and A are in frag layout: the fragment of block (row block, K block) is
-  // 1 KB at ((row block) * K/32 + K block) * 1024, lane l's 16 bytes at 16 l
+  // 1 KB at ((row block) * frag_kb(K) + K block) * 1024, lane l's 16 bytes at 16 l
   const uint32_t loff = lane * 16;
-  const int KB = a.K / 32;
+  const int KB = frag_kb(a.K);  // blocks per 16-row block (frag layout)
 
   uint4 wr[D][4][2], ar[D][MB][2];
   // issue the loads of unit i (clamped: past the end the last unit is re-read) into a ring slot;
@@ -195,7 +195,7 @@ SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots) {
 hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.M > 128 || a.N % COLS != 0 || a.K % UNIT_K != 0 || p.tiles != a.N / COLS ||
-      p.chunks != a.K / UNIT_K || p.G < 1 || (long long)a.N * a.K >= (1ll << 30))
+      p.chunks != a.K / UNIT_K || p.G < 1 || (long long)frag_elems(a.N, a.K) * 2 >= (1ll << 31))
     return hipErrorInvalidValue;
   const int mb = (a.M + 15) / 16;
   if (mb <= 1) return launch_mb<1>(a, p, st);

@@ -96,7 +96,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int KB = K / 32;
+  const int KB = frag_kb(K);  // blocks per 16-row block (frag layout)
   const int last_rb_a = (M + 15) / 16 - 1, last_rb_w = N / 16 - 1;
 
   // Copies: wave w moves blocks 8 w .. 8 w + 7 of the step's 32 (A blocks
@@ -311,8 +311,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   // frag-layout operands, 32-bit byte offsets into them
-  if (a.K % BK != 0 || a.N % 64 != 0 || (long long)((a.M + 15) / 16) * 16 * a.K * 2 >= (1ll << 31) ||
-      (long long)a.N * a.K * 2 >= (1ll << 31))
+  if (a.K % BK != 0 || a.N % 64 != 0 || (long long)frag_elems(a.M, a.K) * 2 >= (1ll << 31) ||
+      (long long)frag_elems(a.N, a.K) * 2 >= (1ll << 31))
     return hipErrorInvalidValue;
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   const dim3 grid(tm * tn), block(NT);

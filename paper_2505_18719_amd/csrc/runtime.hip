@@ -39,7 +39,6 @@ constexpr int kQBlock = 64;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up(int v, int a) { return (v + a - 1) / a * a; }
-size_t round_up_z(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 // Sizes derived from a configuration.
 struct Dims {
@@ -166,16 +165,16 @@ void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
   vla_model tmp;
   vla_model& M = m ? *m : tmp;
   M.emb = L.take<bf16_t>((size_t)D.V * D.d);
-  M.lm_act = L.take<bf16_t>((size_t)D.Ap * D.d);
+  M.lm_act = L.take<bf16_t>(frag_elems(D.Ap, D.d));
   M.final_norm = L.take<float>(D.d);
   M.lw.resize(n_layers);
   M.kv.resize(n_layers);
   for (int l = 0; l < n_layers; ++l) {
     LayerW& w = M.lw[l];
-    w.wqkv = L.take<bf16_t>((size_t)3 * D.d * D.d);
-    w.wo = L.take<bf16_t>((size_t)D.d * D.d);
-    w.wgu = L.take<bf16_t>((size_t)2 * D.Fp * D.d);
-    w.wd = L.take<bf16_t>((size_t)D.d * D.Fp);
+    w.wqkv = L.take<bf16_t>(frag_elems(3 * D.d, D.d));
+    w.wo = L.take<bf16_t>(frag_elems(D.d, D.d));
+    w.wgu = L.take<bf16_t>(frag_elems(2 * D.Fp, D.d));
+    w.wd = L.take<bf16_t>(frag_elems(D.d, D.Fp));
     w.attn_norm = L.take<float>(D.d);
     w.mlp_norm = L.take<float>(D.d);
   }
@@ -186,14 +185,14 @@ void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
   }
   M.rope = L.take<float2>((size_t)D.Smax * (D.hd / 2));
   M.x = L.take<float>(D.Mmax * D.d);
-  M.u = L.take<bf16_t>(round_up_z(D.Mmax, 16) * D.d);  // frag layout in decode covers whole 16-row blocks
+  M.u = L.take<bf16_t>(frag_elems(D.Mmax, D.d));  // activations in frag layout
   M.q = L.take<bf16_t>(D.Mmax * D.d);
-  M.h = L.take<bf16_t>(round_up_z(D.Mmax, 16) * D.Fp);
+  M.h = L.take<bf16_t>(frag_elems(D.Mmax, D.Fp));
   M.part = L.take<float>((size_t)kMaxSplits * kSkinnyRows * D.Nmax);
   M.logits_pre = L.take<float>((size_t)D.Bmax * D.A);
   M.logits_dec = L.take<float>((size_t)D.Bmax * D.A);
   M.logits_tf = L.take<float>((size_t)D.Bmax * D.nact * D.A);
-  M.u_head = L.take<bf16_t>(round_up_z((size_t)D.Bmax * D.nact, 16) * D.d);
+  M.u_head = L.take<bf16_t>(frag_elems((size_t)D.Bmax * D.nact, D.d));
   M.next_tok = L.take<int32_t>(D.Bmax);
   M.flags = L.take<uint32_t>(4);
   M.meta_dev = L.take<int32_t>(D.meta_ints);
@@ -466,10 +465,11 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
   CREATE_CK(launch_bf16_to_f32(m->final_norm, static_cast<const bf16_t*>(w->final_norm), D.d, s));
   for (int l = 0; l < D.L; ++l) {
     LayerW& lw = m->lw[l];
-    // [Wq; Wk; Wv] is 3d rows of one frag matrix: d is a multiple of 256, so each part starts on a block row
+    // [Wq; Wk; Wv] is 3d rows of one frag matrix: d is a multiple of 256, so each part starts on a 16-row block
+    const size_t part = frag_elems(D.d, D.d);
     CREATE_CK(pack(lw.wqkv, D.d, D.d, w->wq[l], D.d, D.d, D.d, kPackQk));
-    CREATE_CK(pack(lw.wqkv + (size_t)D.d * D.d, D.d, D.d, w->wk[l], D.d, D.d, D.d, kPackQk));
-    CREATE_CK(pack(lw.wqkv + (size_t)2 * D.d * D.d, D.d, D.d, w->wv[l], D.d, D.d, D.d, kPackRows));
+    CREATE_CK(pack(lw.wqkv + part, D.d, D.d, w->wk[l], D.d, D.d, D.d, kPackQk));
+    CREATE_CK(pack(lw.wqkv + 2 * part, D.d, D.d, w->wv[l], D.d, D.d, D.d, kPackRows));
     CREATE_CK(pack(lw.wo, D.d, D.d, w->wo[l], D.d, D.d, D.d, kPackRows));
     CREATE_CK(pack(lw.wgu, 2 * D.Fp, D.d, w->wgate[l], D.d, D.F, D.d, kPackGateUp, w->wup[l]));
     CREATE_CK(pack(lw.wd, D.d, D.Fp, w->wdown[l], D.F, D.d, D.F, kPackRows));
@@ -686,7 +686,7 @@ int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t
     case 1: src = m->q; avail = D.Mmax * D.d * sizeof(bf16_t); break;
     case 2: src = m->kv[layer].k; avail = kv; break;
     case 3: src = m->kv[layer].v; avail = kv; break;
-    case 4: src = m->u; avail = D.Mmax * D.d * sizeof(bf16_t); break;
+    case 4: src = m->u; avail = frag_elems(D.Mmax, D.d) * sizeof(bf16_t); break;
     default: return fail(VLA_EINVAL, "unknown buffer");
   }
   if (bytes > avail) return fail(VLA_EINVAL, "read larger than the buffer");

@@ -232,10 +232,11 @@ class VlaModel:
 
 # ------------------------------------------------------------------ test hooks
 def debug_pack_frag(X: torch.Tensor) -> torch.Tensor:
-    """Row-major bf16 [R, K] -> frag layout (flat, ceil(R/16)*16*K elements; pad rows zero)."""
+    """Row-major bf16 [R, K] -> frag layout (flat, ceil(R/16) * (K/32 + 1) * 512 elements; pad rows and
+    the spare block of each 16-row block zero)."""
     lib = load_library()
     R, K = X.shape
-    out = torch.zeros(((R + 15) // 16) * 16 * K, dtype=torch.bfloat16, device=X.device)
+    out = torch.zeros(((R + 15) // 16) * (K // 32 + 1) * 512, dtype=torch.bfloat16, device=X.device)
     _check(lib.vla_debug_pack_frag(_ptr(X), R, K, X.stride(0), _ptr(out), _stream(X.device)))
     return out
 
