@@ -43,12 +43,11 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One wave per row: u = bf16(x * rsqrt(mean(x^2) + eps) * g), row-major (row
-// stride ldu) or, with frag set, in frag layout of K = d.
+// One wave per row: u = bf16(x * rsqrt(mean(x^2) + eps) * g), row-major (row stride ldu).
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
                                                       const int32_t* __restrict__ rows,
                                                       const float* __restrict__ g, float eps,
-                                                      bf16_t* __restrict__ u, int ldu, int M, int d, int frag) {
+                                                      bf16_t* __restrict__ u, int ldu, int M, int d) {
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= M) return;
@@ -68,7 +67,56 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
     uint2 o;
     o.x = pack2bf(v.x * r * w.x, v.y * r * w.y);
     o.y = pack2bf(v.z * r * w.z, v.w * r * w.w);
-    *reinterpret_cast<uint2*>(frag ? u + frag_index(i, c, d) : ur + c) = o;
+    *reinterpret_cast<uint2*>(ur + c) = o;
+  }
+}
+
+// Frag-layout RMSNorm: one workgroup per 16-row block of u.  Each wave first
+// takes the mean square of 4 of the rows; then the waves write the block's
+// 1 KB frag blocks, one per instruction (lane l: row l % 16, K 8 (l / 16) ..
+// + 8), reading x again (from cache: the rows were just read).
+__global__ __launch_bounds__(256) void rmsnorm_frag_kernel(const float* __restrict__ x, int ldx,
+                                                           const int32_t* __restrict__ rows,
+                                                           const float* __restrict__ g, float eps,
+                                                           bf16_t* __restrict__ u, int M, int d) {
+  __shared__ float rs[16];
+  __shared__ int src[16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = blockIdx.x * 16;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = r0 + wave * 4 + k;
+    if (i >= M) break;  // wave-uniform
+    const int sr = rows ? rows[i] : i;
+    const float* xr = x + (size_t)sr * ldx;
+    float ss = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) {
+      rs[wave * 4 + k] = rsqrtf(ss / (float)d + eps);
+      src[wave * 4 + k] = sr;
+    }
+  }
+  __syncthreads();
+  const int row = lane & 15, kc = lane >> 4;
+  if (r0 + row >= M) return;  // lanes of rows past M write nothing (no barrier follows)
+  const float r = rs[row];
+  const float* xr = x + (size_t)src[row] * ldx + 8 * kc;
+  bf16_t* ub = u + frag_index(r0, 0, d) + 8 * lane;
+  for (int kb = wave; kb < d / 32; kb += 4) {
+    const float4 a0 = *reinterpret_cast<const float4*>(xr + 32 * kb);
+    const float4 a1 = *reinterpret_cast<const float4*>(xr + 32 * kb + 4);
+    const float4 g0 = *reinterpret_cast<const float4*>(g + 32 * kb + 8 * kc);
+    const float4 g1 = *reinterpret_cast<const float4*>(g + 32 * kb + 8 * kc + 4);
+    uint4 o;
+    o.x = pack2bf(a0.x * r * g0.x, a0.y * r * g0.y);
+    o.y = pack2bf(a0.z * r * g0.z, a0.w * r * g0.w);
+    o.z = pack2bf(a1.x * r * g1.x, a1.y * r * g1.y);
+    o.w = pack2bf(a1.z * r * g1.z, a1.w * r * g1.w);
+    *reinterpret_cast<uint4*>(ub + (size_t)kb * 512) = o;
   }
 }
 
@@ -94,17 +142,35 @@ __global__ __launch_bounds__(256) void embed_token_norm_kernel(const int32_t* to
   if (!ok && threadIdx.x == 0) atomicOr(flags, 1u);
   float v[kMaxPerThread];
   float ss = 0.f;
-  int n = 0;
-  for (int c = threadIdx.x; c < d; c += 256, ++n) {
-    v[n] = ok ? bf2f(emb[(size_t)id * d + c]) : 0.f;
-    ss += v[n] * v[n];
+  const int n = (d / 4 + 255) / 256;  // groups of 4 columns per thread
+#pragma unroll
+  for (int t = 0; t < kMaxPerThread / 4; ++t) {
+    if (t >= n) break;
+    const int c = 4 * (threadIdx.x + 256 * t);
+    if (c >= d) {
+      v[4 * t] = v[4 * t + 1] = v[4 * t + 2] = v[4 * t + 3] = 0.f;
+      continue;
+    }
+    const uint2 e = ok ? *reinterpret_cast<const uint2*>(emb + (size_t)id * d + c) : make_uint2(0, 0);
+    v[4 * t] = __uint_as_float(e.x << 16);
+    v[4 * t + 1] = __uint_as_float(e.x & 0xffff0000u);
+    v[4 * t + 2] = __uint_as_float(e.y << 16);
+    v[4 * t + 3] = __uint_as_float(e.y & 0xffff0000u);
+    ss += v[4 * t] * v[4 * t] + v[4 * t + 1] * v[4 * t + 1] + v[4 * t + 2] * v[4 * t + 2] +
+          v[4 * t + 3] * v[4 * t + 3];
   }
   ss = block_sum256(ss, sh);
   const float r = rsqrtf(ss / (float)d + eps);
-  n = 0;
-  for (int c = threadIdx.x; c < d; c += 256, ++n) {
-    x[(size_t)b * d + c] = v[n];
-    u[frag_index(b, c, d)] = f2bf(v[n] * r * g[c]);
+#pragma unroll
+  for (int t = 0; t < kMaxPerThread / 4; ++t) {
+    if (t >= n) break;
+    const int c = 4 * (threadIdx.x + 256 * t);
+    if (c >= d) break;
+    const float4 gv = *reinterpret_cast<const float4*>(g + c);
+    *reinterpret_cast<float4*>(x + (size_t)b * d + c) = make_float4(v[4 * t], v[4 * t + 1], v[4 * t + 2], v[4 * t + 3]);
+    *reinterpret_cast<uint2*>(u + frag_index(b, c, d)) =
+        make_uint2(pack2bf(v[4 * t] * r * gv.x, v[4 * t + 1] * r * gv.y),
+                   pack2bf(v[4 * t + 2] * r * gv.z, v[4 * t + 3] * r * gv.w));
   }
 }
 
@@ -117,33 +183,45 @@ __device__ __forceinline__ float skinny_sum(const float* __restrict__ part, cons
   return v;
 }
 
-__global__ __launch_bounds__(256) void reduce_residual_norm_kernel(const float* __restrict__ part, SkinnyPlan p,
-                                                                   float* __restrict__ x, bf16_t* __restrict__ u,
-                                                                   const float* __restrict__ g, float eps, int M,
-                                                                   int d) {
-  __shared__ float sh[4];
+// One 1024-thread workgroup per row: 4 consecutive columns per thread and
+// pass (two passes cover d <= 8192), every partial slot's float4 in flight together.
+__global__ __launch_bounds__(1024) void reduce_residual_norm_kernel(const float* __restrict__ part, SkinnyPlan p,
+                                                                    float* __restrict__ x, bf16_t* __restrict__ u,
+                                                                    const float* __restrict__ g, float eps, int M,
+                                                                    int d) {
+  __shared__ float sh[16];
   const int m = blockIdx.x;
-  const int n = d / 256;  // elements per thread (d % 256 == 0)
-  float v[kMaxPerThread];
-#pragma unroll
-  for (int i = 0; i < kMaxPerThread; ++i)
-    if (i < n) v[i] = x[(size_t)m * d + threadIdx.x + 256 * i];
-#pragma unroll
-  for (int i = 0; i < kMaxPerThread; ++i)
-    if (i < n) v[i] += skinny_sum(part, p, M, d, m, threadIdx.x + 256 * i);
+  float4 v[2];
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxPerThread; ++i)
-    if (i < n) ss += v[i] * v[i];
-  ss = block_sum256(ss, sh);
+  for (int t = 0; t < 2; ++t) {  // d <= 8192
+    const int c = 4 * (threadIdx.x + 1024 * t);
+    if (c >= d) break;
+    float4 a = *reinterpret_cast<const float4*>(x + (size_t)m * d + c);
+    const int ns = skinny_slots(p, c >> 6);
+    for (int sl = 0; sl < ns; ++sl) {
+      const float4 q = *reinterpret_cast<const float4*>(part + ((size_t)sl * M + m) * d + c);
+      a.x += q.x; a.y += q.y; a.z += q.z; a.w += q.w;
+    }
+    v[t] = a;
+    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  ss = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) ss += sh[w];
   const float r = rsqrtf(ss / (float)d + eps);
 #pragma unroll
-  for (int i = 0; i < kMaxPerThread; ++i)
-    if (i < n) {
-      const int c = threadIdx.x + 256 * i;
-      x[(size_t)m * d + c] = v[i];
-      u[frag_index(m, c, d)] = f2bf(v[i] * r * g[c]);
-    }
+  for (int t = 0; t < 2; ++t) {
+    const int c = 4 * (threadIdx.x + 1024 * t);
+    if (c >= d) break;
+    const float4 gv = *reinterpret_cast<const float4*>(g + c);
+    *reinterpret_cast<float4*>(x + (size_t)m * d + c) = v[t];
+    *reinterpret_cast<uint2*>(u + frag_index(m, c, d)) =
+        make_uint2(pack2bf(v[t].x * r * gv.x, v[t].y * r * gv.y), pack2bf(v[t].z * r * gv.z, v[t].w * r * gv.w));
+  }
 }
 
 __global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict__ part, SkinnyPlan p,
@@ -156,13 +234,22 @@ __global__ __launch_bounds__(256) void reduce_sum_kernel(const float* __restrict
 
 __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restrict__ part, SkinnyPlan p,
                                                             bf16_t* __restrict__ h, int ldh, int M, int F) {
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (size_t)M * F) return;
-  const int m = (int)(i / F), j = (int)(i % F);
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;  // group of 4 consecutive j
+  if (i >= (size_t)M * (F / 4)) return;
+  const int m = (int)(i / (F / 4)), j = 4 * (int)(i % (F / 4));
   const int N = p.tiles * 64;
-  const int cg = 64 * (j >> 5) + (j & 31);
-  const float gs = skinny_sum(part, p, M, N, m, cg), us = skinny_sum(part, p, M, N, m, cg + 32);
-  h[frag_index(m, j, ldh)] = f2bf(gs / (1.f + expf(-gs)) * us);
+  const int cg = 64 * (j >> 5) + (j & 31);  // gate columns cg .. cg+3, up columns 32 further (one 64-column tile)
+  const int ns = skinny_slots(p, cg >> 6);
+  float4 gs = make_float4(0.f, 0.f, 0.f, 0.f), us = gs;
+  for (int sl = 0; sl < ns; ++sl) {
+    const float* pr = part + ((size_t)sl * M + m) * N + cg;
+    const float4 a = *reinterpret_cast<const float4*>(pr), b = *reinterpret_cast<const float4*>(pr + 32);
+    gs.x += a.x; gs.y += a.y; gs.z += a.z; gs.w += a.w;
+    us.x += b.x; us.y += b.y; us.z += b.z; us.w += b.w;
+  }
+  auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
+  *reinterpret_cast<uint2*>(h + frag_index(m, j, ldh)) =
+      make_uint2(pack2bf(sw(gs.x, us.x), sw(gs.y, us.y)), pack2bf(sw(gs.z, us.z), sw(gs.w, us.w)));
 }
 
 // One thread per rotary pair of q and k, and per pair of v features.
@@ -267,15 +354,17 @@ hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const fl
                           int ldu, int M, int d, hipStream_t s, bool frag) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0 || (frag && d % 32 != 0)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d,
-                     frag ? 1 : 0);
+  if (frag)
+    hipLaunchKernelGGL(rmsnorm_frag_kernel, dim3((M + 15) / 16), dim3(256), 0, s, x, ldx, rows, g, eps, u, M, d);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d);
   return hipGetLastError();
 }
 
 hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float* x, bf16_t* u, const float* g,
                                    float eps, int B, int d, int vocab, uint32_t* flags, hipStream_t s) {
   if (B <= 0) return hipSuccess;
-  if (d > 256 * kMaxPerThread) return hipErrorInvalidValue;
+  if (d > 256 * kMaxPerThread || d % 32 != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(embed_token_norm_kernel, dim3(B), dim3(256), 0, s, tok, emb, x, u, g, eps, d, vocab, flags);
   return hipGetLastError();
 }
@@ -283,8 +372,8 @@ hipError_t launch_embed_token_norm(const int32_t* tok, const bf16_t* emb, float*
 hipError_t launch_reduce_residual_norm(const float* part, const SkinnyPlan& p, float* x, bf16_t* u, const float* g,
                                        float eps, int M, int d, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (d > 256 * kMaxPerThread || d % 256 != 0 || p.tiles * 64 != d) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(256), 0, s, part, p, x, u, g, eps, M, d);
+  if (d > 8192 || d % 64 != 0 || p.tiles * 64 != d) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_residual_norm_kernel, dim3(M), dim3(1024), 0, s, part, p, x, u, g, eps, M, d);
   return hipGetLastError();
 }
 
@@ -298,7 +387,7 @@ hipError_t launch_reduce_sum(const float* part, const SkinnyPlan& p, float* z, i
 
 hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* h, int ldh, int M, int F,
                                 hipStream_t s) {
-  const size_t n = (size_t)M * F;
+  const size_t n = (size_t)M * (F / 4);
   if (n == 0) return hipSuccess;
   if (2 * F > p.tiles * 64 || F % 32 != 0 || ldh < F) return hipErrorInvalidValue;
   hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, p, h, ldh, M, F);
