@@ -71,53 +71,57 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-// Frag-layout RMSNorm: one workgroup per 16-row block of u.  Each wave first
-// takes the mean square of 4 of the rows; then the waves write the block's
-// 1 KB frag blocks, one per instruction (lane l: row l % 16, K 8 (l / 16) ..
-// + 8), reading x again (from cache: the rows were just read).
-__global__ __launch_bounds__(256) void rmsnorm_frag_kernel(const float* __restrict__ x, int ldx,
-                                                           const int32_t* __restrict__ rows,
-                                                           const float* __restrict__ g, float eps,
-                                                           bf16_t* __restrict__ u, int M, int d) {
-  __shared__ float rs[16];
-  __shared__ int src[16];
+// RMSNorm into frag layout.  A workgroup of RPW waves normalises RPW rows of
+// one 16-row frag block (RPW = 16: the whole block; 8: one half), one wave per
+// row: the wave reads its row once into registers (NJ float4 per lane, 1 KB
+// per load instruction), reduces the mean square, and writes the scaled bf16
+// row into LDS, row-major with a 16-byte pad per row; the workgroup then reads
+// LDS in frag order (the pad puts the 8 rows of one 16-lane read phase on
+// distinct banks) and writes each 1 KB block as one contiguous store per 64
+// (or 32) lanes.  Rows past M are written as zeros.
+template <int NJ, int RPW>
+__global__ __launch_bounds__(64 * RPW) void rmsnorm_frag_kernel(const float* __restrict__ x, int ldx,
+                                                                const int32_t* __restrict__ rows,
+                                                                const float* __restrict__ g, float eps,
+                                                                bf16_t* __restrict__ u, int M, int d) {
+  extern __shared__ uint4 norm_lds[];
+  char* ls = reinterpret_cast<char*>(norm_lds);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r0 = blockIdx.x * 16;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = r0 + wave * 4 + k;
-    if (i >= M) break;  // wave-uniform
-    const int sr = rows ? rows[i] : i;
-    const float* xr = x + (size_t)sr * ldx;
+  const int r0 = blockIdx.x * RPW, nj = d / 256;
+  const int lrow = 2 * d + 16;  // LDS bytes per row
+  char* lr = ls + wave * lrow + 8 * lane;
+  if (r0 + wave < M) {  // wave-uniform
+    const int i = r0 + wave;
+    const float* xr = x + (size_t)(rows ? rows[i] : i) * ldx + 4 * lane;
+    float4 v[NJ];
     float ss = 0.f;
-    for (int c = lane * 4; c < d; c += 256) {
-      const float4 v = *reinterpret_cast<const float4*>(xr + c);
-      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < nj) v[j] = *reinterpret_cast<const float4*>(xr + 256 * j);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < nj) ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
     ss = wave_sum(ss);
-    if (lane == 0) {
-      rs[wave * 4 + k] = rsqrtf(ss / (float)d + eps);
-      src[wave * 4 + k] = sr;
-    }
+    const float r = rsqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < nj) {
+        const float4 gv = *reinterpret_cast<const float4*>(g + 4 * lane + 256 * j);
+        *reinterpret_cast<uint2*>(lr + 512 * j) =
+            make_uint2(pack2bf(v[j].x * r * gv.x, v[j].y * r * gv.y), pack2bf(v[j].z * r * gv.z, v[j].w * r * gv.w));
+      }
+  } else {
+    for (int j = 0; j < nj; ++j) *reinterpret_cast<uint2*>(lr + 512 * j) = make_uint2(0, 0);
   }
   __syncthreads();
-  const int row = lane & 15, kc = lane >> 4;
-  if (r0 + row >= M) return;  // lanes of rows past M write nothing (no barrier follows)
-  const float r = rs[row];
-  const float* xr = x + (size_t)src[row] * ldx + 8 * kc;
-  bf16_t* ub = u + frag_index(r0, 0, d) + 8 * lane;
-  for (int kb = wave; kb < d / 32; kb += 4) {
-    const float4 a0 = *reinterpret_cast<const float4*>(xr + 32 * kb);
-    const float4 a1 = *reinterpret_cast<const float4*>(xr + 32 * kb + 4);
-    const float4 g0 = *reinterpret_cast<const float4*>(g + 32 * kb + 8 * kc);
-    const float4 g1 = *reinterpret_cast<const float4*>(g + 32 * kb + 8 * kc + 4);
-    uint4 o;
-    o.x = pack2bf(a0.x * r * g0.x, a0.y * r * g0.y);
-    o.y = pack2bf(a0.z * r * g0.z, a0.w * r * g0.w);
-    o.z = pack2bf(a1.x * r * g1.x, a1.y * r * g1.y);
-    o.w = pack2bf(a1.z * r * g1.z, a1.w * r * g1.w);
-    *reinterpret_cast<uint4*>(ub + (size_t)kb * 512) = o;
-  }
+  // block kb of the 16-row block: lane l = row % 16 + 16 (k % 32 / 8) holds 16 bytes
+  constexpr int LPB = 4 * RPW;  // lanes of a block this workgroup writes
+  const int idx = threadIdx.x % LPB, rr = idx % RPW, q = idx / RPW;
+  const int ro = r0 & 15, l = ro + rr + 16 * q;
+  bf16_t* ub = u + frag_index(r0 & ~15, 0, d) + 8 * l;
+  const char* src = ls + rr * lrow + 16 * q;
+  for (int kb = threadIdx.x / LPB; kb < d / 32; kb += 16)
+    *reinterpret_cast<uint4*>(ub + (size_t)kb * 512) = *reinterpret_cast<const uint4*>(src + 64 * kb);
 }
 
 // Block-wide sum over 256 threads.
@@ -350,13 +354,33 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+namespace {
+template <int NJ, int RPW>
+hipError_t launch_norm_frag(const float* x, int ldx, const int32_t* rows, const float* g, float eps, bf16_t* u,
+                            int M, int d, hipStream_t s) {
+  const size_t lds = (size_t)RPW * (2 * d + 16);
+  static bool attr_set = false;  // dynamic LDS above 64 KB must be allowed once per kernel
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&rmsnorm_frag_kernel<NJ, RPW>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)(RPW * (2 * 256 * NJ + 16)));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((rmsnorm_frag_kernel<NJ, RPW>), dim3((M + RPW - 1) / RPW), dim3(64 * RPW), lds, s, x, ldx, rows,
+                     g, eps, u, M, d);
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps, bf16_t* u,
                           int ldu, int M, int d, hipStream_t s, bool frag) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0 || (frag && d % 32 != 0)) return hipErrorInvalidValue;
-  if (frag)
-    hipLaunchKernelGGL(rmsnorm_frag_kernel, dim3((M + 15) / 16), dim3(256), 0, s, x, ldx, rows, g, eps, u, M, d);
-  else
+  if (frag) {
+    if (d % 256 != 0 || d > 8192) return hipErrorInvalidValue;
+    if (d <= 4096) return launch_norm_frag<16, 8>(x, ldx, rows, g, eps, u, M, d, s);
+    return launch_norm_frag<32, 8>(x, ldx, rows, g, eps, u, M, d, s);
+  }
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, ldx, rows, g, eps, u, ldu, M, d);
   return hipGetLastError();
 }

@@ -107,7 +107,8 @@ struct EmbedArgs {
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 
 // u[i] = bf16(rmsnorm(x[rows ? rows[i] : i]) * g), i < M; u row-major with row
-// stride ldu, or in frag layout (K = d) when `frag` is set
+// stride ldu, or in frag layout (K = d, d % 256 == 0, d <= 8192) when `frag` is
+// set, where the rows of the last 16-row block past M are written as zeros
 hipError_t launch_rmsnorm(const float* x, int ldx, const int32_t* rows, const float* g, float eps,
                           bf16_t* u, int ldu, int M, int d, hipStream_t s, bool frag = false);
 
