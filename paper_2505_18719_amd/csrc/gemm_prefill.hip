@@ -2,25 +2,34 @@
 // fp32 accumulation, with fused epilogues (residual add, SwiGLU, RoPE + paged
 // KV append).
 //
-// Tiling: a 256-thread workgroup (4 wave64s, one per SIMD) owns a 256 x 256
-// output tile; each wave owns 128 x 128 of it as 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane, held in AGPRs),
-// which halves the LDS operand traffic per MFMA compared with 128 x 64 wave
-// tiles.
+// Tiling: a 512-thread workgroup (8 wave64s, two per SIMD) owns a 256 x 256
+// output tile; each wave owns 128 x 64 of it as 8 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16 (128 fp32 accumulators per lane).
 //
-// The kernel is bound by how fast the A and W tiles reach LDS (128 flops per
-// delivered byte at this tile size), and a copy's round trip is long when its
-// lines miss L2, so the copies run four K steps of 32 ahead through a ring of
-// five 32 KB LDS stages (all 160 KB of LDS).  Both operands are in frag layout
-// (see frag_index), so a K step of either tile is sixteen 1 KB blocks and
-// every copy is one block moved whole by buffer_load ... lds (no VGPR round
-// trip, one contiguous 1 KB read per wave instruction).  An MFMA operand read
-// then takes 32 rows of a block pair as contiguous 256-byte runs, which is
-// free of LDS bank conflicts without any swizzle.  Copies, operand reads and
-// MFMAs are interleaved one memory instruction per MFMA in a pinned order.
+// Ping-pong: waves 0-3 and 4-7 form two groups that run half a phase apart,
+// separated by workgroup barriers.  While one group issues its 32 MFMAs of a
+// K step of 32, the wave of the other group on the same SIMD reads its
+// operand fragments of that step from LDS and issues its share of the copies
+// of a later step, so the MFMA pipe of every SIMD is fed alternately by its
+// two waves and a memory instruction that stalls never holds up an MFMA.
+//
+// Operands: A and W are in frag layout (see frag_index), so a K step of either
+// 256-row panel is sixteen 1 KB blocks, each one v_mfma_f32_16x16x32 operand,
+// and every copy moves one block whole with buffer_load ... lds (global to
+// LDS, no VGPR round trip, one contiguous 1 KB read per wave instruction).
+// The copies run four K steps ahead through a ring of five 32 KB stages (all
+// 160 KB of LDS).  An operand read is one 16-byte LDS read per lane of a
+// contiguous block: free of bank conflicts without a swizzle.
+//
+// Why these choices: the kernel runs at the chip's power limit (the shader
+// clock measured inside it is 1.2-1.6 GHz with all CUs busy), so what counts
+// is issue efficiency per clock and energy per flop.  The two-waves-per-SIMD
+// ping-pong keeps the MFMA pipe fed (measured ~93 % of MFMA cycles in the main
+// loop); the 16x16x32 instruction moves half the accumulator register traffic
+// per flop of the 32x32x16 one and ran ~5 % faster at the same tiling.
 // Workgroup ids are remapped so that the tiles one XCD runs are contiguous in
-// a grouped (8 tile-rows) order, which keeps A panels and W panels resident
-// in that XCD's L2.
+// a grouped order (4 tile-rows high), which keeps A and W panels shared in
+// that XCD's L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -29,12 +38,11 @@ namespace vla {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 32;
-constexpr int NT = 256;        // 4 waves, 2 x 2, each owning 128 x 128 of the tile
-constexpr int NSTAGE = 5;      // LDS ring of K steps: A 16 KB + W 16 KB each
-constexpr int AHEAD = 4;       // K steps whose copies are in flight ahead of the one consumed
+constexpr int NT = 512;                // 8 waves: 2 x 4, each owning 128 x 64 of the tile
+constexpr int NSTAGE = 5;              // LDS ring of K steps: A 16 KB + W 16 KB each
+constexpr int AHEAD = 4;               // K steps whose copies are in flight ahead of the one read
 constexpr int STAGE_U4 = 2 * 16 * 64;  // uint4 per stage: 2 operands x 16 blocks x 64 lanes
-constexpr int GROUP_M = 8;
-
+constexpr int GROUP_M = 4;
 
 __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_n, int& tm, int& tn) {
   // XCD-aware remap: the hardware deals workgroups round-robin to 8 XCDs.
@@ -53,19 +61,6 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
 // nothing may be scheduled across this point
 #define PIN() __builtin_amdgcn_sched_barrier(0)
 
-// Orders of the 16 MFMAs of one k-step over the 4 x 4 blocks of the wave
-// tile (row block i, column block j) and of the 8 operand reads that feed them
-// (o = 0 for A, 1 for W; block index).  Order 0 ("triangular") lets each MFMA
-// wait only for fragments read well before it; order 1 is row-major, so that
-// its first 8 MFMAs need only the first 6 reads (the k-step that straddles the
-// barrier).
-__device__ constexpr int kMfmaI[2][16] = {{0, 0, 1, 1, 0, 1, 2, 2, 2, 0, 1, 2, 3, 3, 3, 3},
-                                          {0, 0, 0, 0, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3}};
-__device__ constexpr int kMfmaJ[2][16] = {{0, 1, 0, 1, 2, 2, 0, 1, 2, 3, 3, 3, 0, 1, 2, 3},
-                                          {0, 1, 2, 3, 0, 1, 2, 3, 0, 1, 2, 3, 0, 1, 2, 3}};
-__device__ constexpr int kReadO[2][8] = {{0, 1, 0, 1, 0, 1, 0, 1}, {0, 0, 1, 1, 1, 1, 0, 0}};
-__device__ constexpr int kReadB[2][8] = {{0, 0, 1, 1, 2, 2, 3, 3}, {0, 1, 0, 1, 2, 3, 2, 3}};
-
 typedef __attribute__((address_space(3))) void lds_ptr_t;
 
 // s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
@@ -83,10 +78,65 @@ __device__ __forceinline__ void dma16(uint32_t m0, uint32_t voff, __amdgpu_buffe
                : "memory");
 }
 
+// Epilogues that pair column c of a 64-column group with column c + 32:
+// SwiGLU (gate rows, then the matching up rows) and the QKV projection
+// (rotary pairs).  v1, v2: float4 chunks q and q + 8 of output row `row`,
+// group starting at column c0.
+template <int EPI>
+__device__ __forceinline__ void pair_epilogue(const GemmArgs& a, int row, int c0, int q, const float4& v1,
+                                              const float4& v2) {
+  const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
+  if constexpr (EPI == kEpiSwiGlu) {
+    // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
+    float o[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
+    *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
+        make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
+  } else {  // kEpiQkvRope
+    const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
+    const int region = c0 / d;
+    const int cc0 = c0 - region * d;
+    const int head = cc0 / hd;
+    const int blk = (cc0 % hd) / 64;
+    const int pos = a.meta.row_pos[row];
+    if (region < 2) {
+      // q and k rows were permuted per head so that columns c and c+32 of
+      // this 64-column group are the rotary pair (32*blk + c, half + 32*blk + c)
+      const int ai = 32 * blk + 4 * q;
+      float o1[4], o2[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float2 cs = a.rope[pos * half + ai + t];
+        o1[t] = x1[t] * cs.x - x2[t] * cs.y;
+        o2[t] = x1[t] * cs.y + x2[t] * cs.x;
+      }
+      bf16_t* dst;
+      if (region == 0) {
+        dst = a.q + (size_t)row * a.ldq + head * hd;
+      } else {
+        const int env = a.meta.row_env[row];
+        const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
+        dst = a.kv.k + (((size_t)page * H + head) * kPage + pos % kPage) * hd;
+      }
+      *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
+      *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
+    } else {
+      const int env = a.meta.row_env[row];
+      const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
+      bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + pos % kPage;
+      const int i1 = cc0 % hd + 4 * q;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        vb[(size_t)(i1 + t) * kPage] = f2bf(x1[t]);
+        vb[(size_t)(i1 + t + 32) * kPage] = f2bf(x2[t]);
+      }
+    }
+  }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  // [stage][A 16 blocks | W 16 blocks][64 lanes]: block b of an operand is its
-  // 16-row block b of the tile over the stage's 32 K
   __shared__ uint4 lds[NSTAGE][STAGE_U4];
 
   int tm, tn;
@@ -95,141 +145,99 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int KB = frag_kb(K);  // blocks per 16-row block (frag layout)
+  const int grp = wave >> 2;
+  const int wm = wave & 1, wn = wave >> 1;  // 128-row half, 64-column quarter of the tile
+  const int KB = frag_kb(K);
   const int last_rb_a = (M + 15) / 16 - 1, last_rb_w = N / 16 - 1;
 
-  // Copies: wave w moves blocks 8 w .. 8 w + 7 of the step's 32 (A blocks
-  // 0-15, W blocks 16-31).  Row blocks past the matrix are clamped to its last
-  // one (their rows only feed outputs that are not stored).
+  // copies: wave w moves blocks 4 w .. 4 w + 3 of a step's 32 (waves 0-3: A, 4-7: W)
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
-  // waves 0, 1 copy A blocks 0-15, waves 2, 3 W blocks 0-15 (wave-uniform choice, no branch)
-  const bool copies_a = wave < 2;
+  const bool copies_a = wave < 4;
   const __amdgpu_buffer_rsrc_t rsC = copies_a ? rsA : rsW;
   const int rb0 = copies_a ? (m0 >> 4) : (n0 >> 4), rb_last = copies_a ? last_rb_a : last_rb_w;
   const uint32_t voff = lane * 16;
   const uint32_t lds_base = (uint32_t)(uintptr_t)((lds_ptr_t*)&lds[0][0]);
   auto copy = [&](int j, int st, int ks) {
-    const int b = wave * 8 + j;  // A block b, or W block b - 16
+    const int b = wave * 4 + j;
     dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb0 + (b & 15), rb_last) * KB + ks) * 1024);
   };
 
-  f32x16 acc[4][4];
+  f32x4 acc[8][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Operand fragments of MFMA k-step q (0, 1) for lane (l31, lhi): row
-  // 128 wm + 32 i + l31 of A (128 wn + ... of W) is row l31 % 16 of the
-  // operand's block 8 wm + 2 i + l31 / 16, and K 16 q + 8 lhi is its column
-  // group 2 q + lhi: the lane's 16 bytes sit at block lane (l31 % 16) + 16 (2 q + lhi).
-  const int l31 = lane & 31, lhi = lane >> 5;
-  const int fa = (wm * 8 + (l31 >> 4)) * 64 + (l31 & 15) + 16 * lhi;
-  const int fw = 16 * 64 + (wn * 8 + (l31 >> 4)) * 64 + (l31 & 15) + 16 * lhi;
+  // 16x16x32 fragments: A rows 128 wm + 16 i are frag block 8 wm + i, W rows
+  // 64 wn + 16 j block 4 wn + j; a lane's 16 bytes sit at 16 * lane of a block
+  const int fa = (wm * 8) * 64 + lane;
+  const int fw = (16 + wn * 4) * 64 + lane;
   const uint4* ring = &lds[0][0];
-  bf16x8 fr[2][2][4];  // [k-step][A / W][block]
-  auto read = [&](int ord, int r, int st, int q) {
-    const int o = kReadO[ord][r], i = kReadB[ord][r];
-    fr[q][o][i] = as_bf16x8(ring[st * STAGE_U4 + (o ? fw : fa) + i * 128 + 32 * q]);
-  };
-  auto mfma = [&](int ord, int t, int q) {
-    const int i = kMfmaI[ord][t], j = kMfmaJ[ord][t];
-    acc[i][j] = mfma32(fr[q][0][i], fr[q][1][j], acc[i][j]);
-  };
+  bf16x8 fa_r[8], fw_r[4];
 
-  // Pipeline over K steps of 32 (two MFMA k-steps of 16).  One step of a wave
-  // is 32 MFMAs with one memory instruction after 24 of them:
-  //   k-step 0: MFMAs 0-7 + the 8 operand reads of k-step 1 (row-major order),
-  //             MFMAs 8-15 + the 8 copies of step kt+AHEAD
-  //   k-step 1: MFMAs 0-7 (row blocks 0, 1), wait for this wave's copies of
-  //             step kt+1, barrier, MFMAs 8-15 + the 8 operand reads of
-  //             k-step 0 of step kt+1
-  // The order is pinned (the scheduler would otherwise hoist the barrier and
-  // its LDS wait above the MFMAs that are meant to hide them).  The stage
-  // filled in step kt was last read in step kt-1, before that step's barrier.
-  // Loads complete in order: with the copies of AHEAD-1 later steps allowed
-  // to stay in flight, the wait covers exactly the copies of step kt+1.
   const int nk = K / BK;
 #pragma unroll
   for (int st = 0; st < AHEAD; ++st)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) copy(j, st, min(st, nk - 1));
-  WAIT_VMCNT(8 * (AHEAD - 1));
-  __syncthreads();
+    for (int j = 0; j < 4; ++j) copy(j, st, min(st, nk - 1));
+  WAIT_VMCNT(4 * (AHEAD - 1));
+  __builtin_amdgcn_s_barrier();
+  if (grp) __builtin_amdgcn_s_barrier();
   PIN();
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {  // same order as in the loop, so the loop's waits hold on entry
-    read(0, r, 0, 0);
-    PIN();
-  }
-  int cur = 0, fill = AHEAD;  // ring stages of steps kt and kt + AHEAD
+  int cur = 0, fill = AHEAD;
   for (int kt = 0; kt < nk; ++kt) {
-    const int nxt = cur + 1 == NSTAGE ? 0 : cur + 1;
+    // ---- memory phase: operand fragments of step kt, copies of step kt + AHEAD
+    const uint4* sp = ring + cur * STAGE_U4;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) fa_r[i] = as_bf16x8(sp[fa + i * 64]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fw_r[j] = as_bf16x8(sp[fw + j * 64]);
     const int kfill = min(kt + AHEAD, nk - 1);  // past the end the last step is re-copied
+#pragma unroll
+    for (int j = 0; j < 4; ++j) copy(j, fill, kfill);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments in registers, this stage's reads done
+    WAIT_VMCNT(4 * (AHEAD - 1));      // this wave's copies of step kt + 1 have landed
     PIN();
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      mfma(0, t, 0);
-      read(1, t, cur, 1);
-      PIN();
-    }
-#pragma unroll
-    for (int t = 8; t < 16; ++t) {
-      mfma(0, t, 0);
-      copy(t - 8, fill, kfill);
-      PIN();
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      mfma(1, t, 1);
-      PIN();
-    }
-    WAIT_VMCNT(8 * (AHEAD - 1));   // this wave's copies of step kt+1 have landed
-    __syncthreads();               // ... and everyone's
+    __builtin_amdgcn_s_barrier();
     PIN();
+    // ---- compute phase
 #pragma unroll
-    for (int t = 8; t < 16; ++t) {
-      mfma(1, t, 1);
-      read(0, t - 8, nxt, 0);
-      PIN();
-    }
-    cur = nxt;
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16(fa_r[i], fw_r[j], acc[i][j]);
+    PIN();
+    __builtin_amdgcn_s_barrier();
+    PIN();
+    cur = cur + 1 == NSTAGE ? 0 : cur + 1;
     fill = fill + 1 == NSTAGE ? 0 : fill + 1;
   }
+  if (!grp) __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   // ---------------------------------------------------------------- epilogue
-  // The LDS stages are free after the last barrier; each wave stages its
-  // 128 x 128 accumulator tile through its own 32 KB of them, 64 columns at a
-  // time, and then writes the epilogue's outputs with contiguous stores.
-  // acc[i][j][r] holds row i*32 + 8*(r/4) + 4*lhi + r%4 and column j*32 + l31
-  // of the wave tile; in LDS the float4 chunk q of row rl sits at q ^ (rl%16).
-  float* st = reinterpret_cast<float*>(&lds[0][0]) + wave * (128 * 64);
-  // (l31, lhi as in the main loop)
-  const int wrow0 = m0 + wm * 128;
+  // acc[i][j][r] holds row 16 i + 4 (lane / 16) + r, column 16 j + lane % 16 of the wave tile
+  float* st = reinterpret_cast<float*>(&lds[0][0]) + wave * (64 * 64);
+  const int c0 = n0 + wn * 64;
+  if (c0 >= N) return;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int c0 = n0 + wn * 128 + h * 64;   // first column of this 64-column group
-    if (c0 >= N) break;
+    const int wrow0 = m0 + wm * 128 + h * 64;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
+      for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = i * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
-          const int cl = jj * 32 + l31;
-          st[rl * 64 + (((cl >> 2) ^ (rl & 15)) << 2) + (cl & 3)] = acc[i][2 * h + jj][r];
+        for (int r = 0; r < 4; ++r) {
+          const int rl = ii * 16 + 4 * (lane >> 4) + r;
+          const int cl = jj * 16 + (lane & 15);
+          st[rl * 64 + (((cl >> 2) ^ (rl & 15)) << 2) + (cl & 3)] = acc[4 * h + ii][jj][r];
         }
     __builtin_amdgcn_s_waitcnt(0);
     if constexpr (EPI == kEpiStoreF32 || EPI == kEpiResidual) {
       const int q = lane & 15;
-      for (int it = 0; it < 32; ++it) {
+      for (int it = 0; it < 16; ++it) {
         const int rl = it * 4 + (lane >> 4);
         const int row = wrow0 + rl;
         const float4 v = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
@@ -244,62 +252,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
         }
       }
     } else {
-      // pair epilogues: chunk q (< 8) of the group pairs with chunk q + 8
       const int q = lane & 7;
-      for (int it = 0; it < 16; ++it) {
+      for (int it = 0; it < 8; ++it) {
         const int rl = it * 8 + (lane >> 3);
         const int row = wrow0 + rl;
         const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
         const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
         if (row >= M) continue;
-        const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
-        if constexpr (EPI == kEpiSwiGlu) {
-          // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
-          float o[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
-          *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
-              make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
-        } else {  // kEpiQkvRope
-          const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
-          const int region = c0 / d;
-          const int cc0 = c0 - region * d;
-          const int head = cc0 / hd;
-          const int blk = (cc0 % hd) / 64;
-          const int pos = a.meta.row_pos[row];
-          if (region < 2) {
-            // q and k rows were permuted per head so that columns c and c+32 of
-            // this 64-column group are the rotary pair (32*blk + c, half + 32*blk + c)
-            const int ai = 32 * blk + 4 * q;
-            float o1[4], o2[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const float2 cs = a.rope[pos * half + ai + t];
-              o1[t] = x1[t] * cs.x - x2[t] * cs.y;
-              o2[t] = x1[t] * cs.y + x2[t] * cs.x;
-            }
-            bf16_t* dst;
-            if (region == 0) {
-              dst = a.q + (size_t)row * a.ldq + head * hd;
-            } else {
-              const int env = a.meta.row_env[row];
-              const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
-              dst = a.kv.k + (((size_t)page * H + head) * kPage + pos % kPage) * hd;
-            }
-            *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
-            *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
-          } else {
-            const int env = a.meta.row_env[row];
-            const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
-            bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + pos % kPage;
-            const int i1 = cc0 % hd + 4 * q;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              vb[(size_t)(i1 + t) * kPage] = f2bf(x1[t]);
-              vb[(size_t)(i1 + t + 32) * kPage] = f2bf(x2[t]);
-            }
-          }
-        }
+        pair_epilogue<EPI>(a, row, c0, q, v1, v2);
       }
     }
     __builtin_amdgcn_s_waitcnt(0);
