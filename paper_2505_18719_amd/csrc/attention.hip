@@ -1,11 +1,11 @@
 // Causal attention over the paged KV cache on gfx950.
 //
-// Prefill: one 256-thread workgroup per (64-query block of one environment,
-// head); each wave owns 16 queries.  K and V^T are staged through LDS one
-// 32-key chunk at a time (double-buffered, one copy per workgroup), scores
-// are computed transposed so that P stays in registers in the layout the
-// P*V MFMA consumes, and a whole score row (<= 320 keys, the longest sequence
-// of one environment) stays in registers, so the softmax is exact.
+// Prefill: one 512-thread workgroup per (environment, head); the head's whole
+// K and V^T are copied into LDS once, then 16-query tiles are dealt to the 8
+// waves.  Scores are computed transposed so that P stays in registers in the
+// layout the P*V MFMA consumes, and a whole score row (<= 320 keys, the
+// longest sequence of one environment) stays in registers, so the softmax is
+// exact.
 //
 // Decode: one workgroup per (environment, head) and one query; scores and
 // P*V in fp32 on the vector ALUs, streaming K rows and transposed V pages with
@@ -17,187 +17,124 @@ namespace vla {
 
 namespace {
 
-constexpr int kMaxKeyTiles = 20;  // 320 keys
-constexpr int kMaxChunks = kMaxKeyTiles / 2;  // 32-key chunks
+// Prefill attention: one 512-thread workgroup (8 waves) per (environment,
+// head).  The environment's whole K (key rows) and V^T (feature rows) for
+// this head, <= 320 keys, are copied once into LDS with buffer_load ... lds
+// (80 KB each at head_dim 128), then every wave takes 16-query tiles of the
+// causal triangle in a balanced order.  Per tile, scores are computed
+// transposed, S^T = K Q^T, with the keys of each 32-key chunk assigned to MFMA
+// rows so that lane group g ends up holding keys 8g .. 8g+7 of the chunk for
+// its query: exactly the B-operand fragment of P^T in O^T = V^T P^T.  P never
+// leaves registers and enters the MFMA as P_hi + P_lo (two bf16 products,
+// ~16 significant bits).  The whole score row (<= 320 keys) is kept, so the
+// softmax is exact (true maximum, no online rescaling).
+//
+// LDS layouts (both conflict-free for the 16-byte operand reads, no padding):
+//  K: row R holds key kperm(R), with the 32 keys of a chunk ordered as the
+//     MFMA rows of its two 16-key tiles; 16-byte feature chunk j of row R is
+//     stored at slot j ^ kswz(R).
+//  V^T: the cache's own page layout, one 16-key page after the other (feature
+//     f of a page: 16 keys, two 16-byte halves); half h of feature f is stored
+//     at 16-byte unit 2f + (h ^ ((f >> 3) & 1)) of its page.
+constexpr int kMaxKeys = 320;
+constexpr int kMaxChunks = kMaxKeys / 32;
+constexpr int kMaxPages = kMaxKeys / kPage;
 
-// One 32-key chunk of one head staged in LDS.  K rows keep the page layout
-// (key-major, HD contiguous) with a 16-byte pad per row; V^T rows (one per
-// feature, 16 keys of one page) get a 16-byte pad too.  The pads put the 16
-// rows read by one MFMA operand load on distinct bank groups.
+// key held by LDS row R of K: MFMA row i of 16-key tile t of chunk c is key 32c + 8(i/4) + 4t + i%4
+__device__ __forceinline__ int kperm(int R) {
+  const int i = R & 15, t = (R >> 4) & 1, c = R >> 5;
+  return 32 * c + 8 * (i >> 2) + 4 * t + (i & 3);
+}
 template <int HD>
-struct AttnChunk {
-  static constexpr int KROW = HD * 2 + 16;       // bytes per key row
-  static constexpr int VROW = 48;                // bytes per feature row (16 keys + pad)
-  static constexpr int KBYTES = 32 * KROW;
-  static constexpr int VBYTES = 2 * HD * VROW;
-};
-
-// Copy chunk c (pages 2c, 2c+1 of this environment) of head `head` from the
-// page pool into registers: each thread moves 16-byte pieces of both pages of
-// K and of V^T (coalesced: a page of one head is contiguous).
-template <int HD>
-struct ChunkRegs {
-  static constexpr int PER = (2 * 16 * HD * 2) / (256 * 16);  // 16-byte pieces per thread per tensor
-  uint4 k[PER], v[PER];
-};
-
-template <int HD>
-__device__ __forceinline__ void chunk_load(ChunkRegs<HD>& r, const bf16_t* kpool, const bf16_t* vpool,
-                                           const int32_t* pt, int c, int H, int head, bool kv_k, bool kv_v) {
-  constexpr int PIECES_PER_PAGE = 16 * HD * 2 / 16;
-#pragma unroll
-  for (int i = 0; i < ChunkRegs<HD>::PER; ++i) {
-    const int piece = threadIdx.x + 256 * i;
-    const int pl = piece / PIECES_PER_PAGE, off = piece % PIECES_PER_PAGE;
-    const size_t base = ((size_t)pt[2 * c + pl] * H + head) * (16 * HD);
-    if (kv_k) r.k[i] = *reinterpret_cast<const uint4*>(kpool + base + off * 8);
-    if (kv_v) r.v[i] = *reinterpret_cast<const uint4*>(vpool + base + off * 8);
-  }
+__device__ __forceinline__ int kswz(int R) {
+  return HD == 128 ? (R & 15) : ((R >> 1) & 7);
 }
 
-template <int HD>
-__device__ __forceinline__ void chunk_store(const ChunkRegs<HD>& r, char* kl, char* vl, bool kv_k, bool kv_v) {
-  constexpr int PIECES_PER_PAGE = 16 * HD * 2 / 16;
-#pragma unroll
-  for (int i = 0; i < ChunkRegs<HD>::PER; ++i) {
-    const int piece = threadIdx.x + 256 * i;
-    const int pl = piece / PIECES_PER_PAGE, off = piece % PIECES_PER_PAGE;
-    if (kv_k) {  // K page: [slot][HD]
-      const int slot = off / (HD / 8), j = off % (HD / 8);
-      *reinterpret_cast<uint4*>(kl + (pl * 16 + slot) * AttnChunk<HD>::KROW + j * 16) = r.k[i];
-    }
-    if (kv_v) {  // V^T page: [HD][16 slots]
-      const int f = off / 2, half = off % 2;
-      *reinterpret_cast<uint4*>(vl + (pl * HD + f) * AttnChunk<HD>::VROW + half * 16) = r.v[i];
-    }
-  }
-}
-
-// Prefill attention, one workgroup per (64-query block of one environment,
-// head), 16 queries per wave.  Scores are computed transposed, S^T = K Q^T,
-// with the keys of each 32-key chunk assigned to MFMA rows so that the lane
-// group g ends up holding keys 8g .. 8g+7 of the chunk for its query: exactly
-// the B-operand fragment of P^T in O^T = V^T P^T.  P therefore never leaves
-// registers; it enters the MFMA as P_hi + P_lo (two bf16 products, ~16
-// significant bits).  The whole score row of a query (<= 320 keys) is kept,
-// so the softmax is exact (true maximum, no online rescaling).
-template <int HD>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
-  using C = AttnChunk<HD>;
-  __shared__ __attribute__((aligned(16))) char klds[2][C::KBYTES];
-  __shared__ __attribute__((aligned(16))) char vlds[2][C::VBYTES];
-  const int item = blockIdx.x, head = blockIdx.y;
-  const int env = a.qblocks[2 * item], q0 = a.qblocks[2 * item + 1];
-  const int L = a.env_len[env], row0 = a.env_row0[env];
-  const int H = a.n_heads;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+// One 16-query tile (queries 16 qt .. 16 qt + 15 of the environment) whose
+// keys span NC 32-key chunks; only the last chunk holds keys that some query
+// of the tile must not see (ncq = qt / 2 + 1 for every tile of a sequence).
+// Straight-line code for a compile-time chunk count, so the scheduler can
+// overlap the LDS reads of one chunk with the MFMAs of another.
+template <int HD, int NC>
+__device__ __forceinline__ void attn_tile(const PrefillAttnArgs& a, const char* klds, const char* vlds, int qt, int L,
+                                          int row0, int head, int lane) {
+  constexpr int KROW = HD * 2, VPAGE = HD * kPage * 2;
+  constexpr int KS = HD / 32, NB = HD / 16;
   const int r16 = lane & 15, g = lane >> 4;
-  const int qw = q0 + wave * 16;                 // first query of this wave
-  const int kend = min(L, q0 + 64);
-  const int nch = (kend + 31) / 32;
-  const int32_t* pt = a.page_table + env * a.max_pages;
-
-  constexpr int KS = HD / 32;
-  uint4 qf[KS];  // B operand: query r16, features 32 ks + 8g .. +8
+  const int qpos = qt * 16 + r16;
+  uint4 qf[KS];  // B operand: query qpos, features 32 ks + 8g .. +8
   {
-    const bf16_t* qp = a.q + (size_t)(row0 + min(qw + r16, L - 1)) * a.d + head * HD + 8 * g;
+    const bf16_t* qp = a.q + (size_t)(row0 + min(qpos, L - 1)) * a.d + head * HD + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const uint4*>(qp + ks * 32);
   }
-  // MFMA row i of tile t (0: A, 1: B) of a chunk is key 8*(i/4) + 4t + i%4
-  const int krowA = 8 * (r16 >> 2) + (r16 & 3);
-
-  // ---- pass 1: scores
-  f32x4 sc[kMaxKeyTiles];
+  // scores: lane holds S(query qpos, key 32c + 8g + 4t + r) in sc[2c + t][r]
+  f32x4 sc[2 * NC];
 #pragma unroll
-  for (int t = 0; t < kMaxKeyTiles; ++t) sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  ChunkRegs<HD> cr;
-  chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, 0, H, head, true, false);
-  chunk_store<HD>(cr, klds[0], nullptr, true, false);
-  __syncthreads();
+  for (int t = 0; t < 2 * NC; ++t) sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int c = 0; c < kMaxChunks; ++c) {
-    if (c < nch) {
-      if (c + 1 < nch) chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, c + 1, H, head, true, false);
-      const char* kl = klds[c & 1];
+  for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const char* kr = kl + (krowA + 4 * t) * C::KROW + 16 * g;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          sc[2 * c + t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(kr + ks * 64)), as_bf16x8(qf[ks]),
-                                 sc[2 * c + t]);
-      }
-      if (c + 1 < nch) chunk_store<HD>(cr, klds[(c + 1) & 1], nullptr, true, false);
-      __syncthreads();
+    for (int ct = 0; ct < 2 * NC; ++ct) {
+      // LDS row 16 ct + r16 (chunk ct / 2, tile ct % 2); its swizzle is kswz<HD>(r16)
+      const char* kr = klds + (16 * ct + r16) * KROW + 16 * ((4 * ks + g) ^ kswz<HD>(r16));
+      sc[ct] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(kr)), as_bf16x8(qf[ks]), sc[ct]);
     }
   }
-
-  // lane holds S(query qw + r16, key 32c + 8g + 4t + r) in sc[2c + t][r]
-  const int qpos = qw + r16;
+  const int klim = min(qpos, L - 1);  // last key this lane's query sees
   float mx = -INFINITY;
 #pragma unroll
-  for (int c = 0; c < kMaxChunks; ++c)
+  for (int ct = 0; ct < 2 * NC; ++ct)
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = 32 * c + 8 * g + 4 * t + r;
-        const bool ok = c < nch && key <= qpos && key < L;
-        const float v = ok ? sc[2 * c + t][r] * a.scale : -INFINITY;
-        sc[2 * c + t][r] = v;
-        mx = fmaxf(mx, v);
+    for (int r = 0; r < 4; ++r) {
+      float v = sc[ct][r] * a.scale;
+      if (ct >= 2 * NC - 2) {
+        const int key = 32 * (ct >> 1) + 8 * g + 4 * (ct & 1) + r;
+        v = key <= klim ? v : -INFINITY;
       }
+      sc[ct][r] = v;
+      mx = fmaxf(mx, v);
+    }
   mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
   mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
   float sum = 0.f;
 #pragma unroll
-  for (int t = 0; t < kMaxKeyTiles; ++t)
+  for (int ct = 0; ct < 2 * NC; ++ct)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float p = sc[t][r] == -INFINITY ? 0.f : expf(sc[t][r] - mx);
-      sc[t][r] = p;
-      sum += p;
+      const float pv = expf(sc[ct][r] - mx);  // masked: expf(-inf) = 0
+      sc[ct][r] = pv;
+      sum += pv;
     }
   sum += __shfl_xor(sum, 16, kWave);
   sum += __shfl_xor(sum, 32, kWave);
 
-  // ---- pass 2: O^T = V^T P^T
-  constexpr int NB = HD / 16;
+  // O^T = V^T P^T: A operand = V^T rows (feature nb*16 + r16), keys 32c + 8g .. +8,
+  // i.e. page 2c + g/2, half g%2; (f >> 3) & 1 of feature 16nb + r16 is r16 >> 3
   f32x4 o[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, 0, H, head, false, true);
-  chunk_store<HD>(cr, nullptr, vlds[0], false, true);
-  __syncthreads();
+  const char* vp0 = vlds + (g >> 1) * VPAGE + 16 * (2 * r16 + ((g & 1) ^ (r16 >> 3)));
 #pragma unroll
-  for (int c = 0; c < kMaxChunks; ++c) {
-    if (c < nch) {
-      if (c + 1 < nch) chunk_load<HD>(cr, a.kv.k, a.kv.v, pt, c + 1, H, head, false, true);
-      bf16x8 phi, plo;
+  for (int c = 0; c < NC; ++c) {
+    bf16x8 phi, plo;
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = sc[2 * c + t][r];
-          const __bf16 h = (__bf16)p;
-          phi[4 * t + r] = h;
-          plo[4 * t + r] = (__bf16)(p - (float)h);
-        }
-      // A operand: V^T row (feature nb*16 + r16), keys 8g .. 8g+7 of the chunk
-      const char* vl = vlds[c & 1] + (g >> 1) * HD * C::VROW + (g & 1) * 16;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const uint4 vv = *reinterpret_cast<const uint4*>(vl + (nb * 16 + r16) * C::VROW);
-        o[nb] = mfma16(as_bf16x8(vv), phi, o[nb]);
-        o[nb] = mfma16(as_bf16x8(vv), plo, o[nb]);
+      for (int r = 0; r < 4; ++r) {
+        const float pv = sc[2 * c + t][r];
+        const __bf16 h = (__bf16)pv;
+        phi[4 * t + r] = h;
+        plo[4 * t + r] = (__bf16)(pv - (float)h);
       }
-      if (c + 1 < nch) chunk_store<HD>(cr, nullptr, vlds[(c + 1) & 1], false, true);
-      __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const uint4 vv = *reinterpret_cast<const uint4*>(vp0 + 2 * c * VPAGE + nb * 16 * 32);
+      o[nb] = mfma16(as_bf16x8(vv), phi, o[nb]);
+      o[nb] = mfma16(as_bf16x8(vv), plo, o[nb]);
     }
   }
-
-  // o[nb][r] = O(query qw + r16, feature nb*16 + 4g + r)
+  // o[nb][r] = O(query qpos, feature nb*16 + 4g + r)
   if (qpos < L) {
     const float inv = 1.f / sum;
     // frag layout (the O projection's A operand): 4 consecutive features stay contiguous
@@ -208,12 +145,116 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
   }
 }
 
+// Tiles qt_lo .. qt_hi - 1, most expensive first, dealt to the 8 waves in snake order.
+template <int HD>
+__device__ __forceinline__ void attn_tiles(const PrefillAttnArgs& a, const char* klds, const char* vlds, int qt_lo,
+                                           int qt_hi, int L, int row0, int head, int wave, int lane) {
+  const int n = qt_hi - qt_lo;
+  for (int p0 = 0; p0 < n; p0 += 8) {
+    const int p = p0 + (((p0 >> 3) & 1) ? 7 - wave : wave);
+    if (p >= n) continue;
+    const int qt = qt_hi - 1 - p;
+    switch (qt / 2 + 1) {  // live 32-key chunks
+      case 1: attn_tile<HD, 1>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 2: attn_tile<HD, 2>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 3: attn_tile<HD, 3>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 4: attn_tile<HD, 4>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 5: attn_tile<HD, 5>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 6: attn_tile<HD, 6>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 7: attn_tile<HD, 7>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 8: attn_tile<HD, 8>(a, klds, vlds, qt, L, row0, head, lane); break;
+      case 9: attn_tile<HD, 9>(a, klds, vlds, qt, L, row0, head, lane); break;
+      default: attn_tile<HD, 10>(a, klds, vlds, qt, L, row0, head, lane); break;
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(512, 1) void attn_prefill_kernel(PrefillAttnArgs a) {
+  constexpr int KROW = HD * 2;           // bytes per K row
+  constexpr int KCH = HD / 8;            // 16-byte chunks per K row
+  constexpr int VPAGE = HD * kPage * 2;  // bytes per V^T page
+  __shared__ __attribute__((aligned(1024))) char lds[kMaxKeys * KROW + kMaxPages * VPAGE];
+  char* const klds = lds;
+  char* const vlds = lds + kMaxKeys * KROW;
+  const int env = blockIdx.x, head = blockIdx.y;
+  const int L = a.env_len[env], row0 = a.env_row0[env];
+  const int H = a.n_heads;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nch = (L + 31) / 32;
+  const int32_t* pt = a.page_table + env * a.max_pages;
+  const int last_page = a.max_pages - 1;
+
+  // ---- copy the K rows and V^T pages of the nch chunks into LDS, chunk by
+  // chunk: copy i moves 1 KB of chunk i / CP (K rows first, then V^T pages);
+  // wave w issues copies w, w + 8, ..., i.e. CP / 8 per chunk
+  constexpr int KC = 32 * KROW / 1024, VC = 2 * VPAGE / 1024, CP = KC + VC;
+  constexpr int KROWS_PER_KB = 1024 / KROW;
+  static_assert(CP % 8 == 0, "copies per chunk must divide among the 8 waves");
+  {
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)a.kv.k, (short)0, 0x7fffffff, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)a.kv.v, (short)0, 0x7fffffff, 0x00020000);
+    const uint32_t kbase = (uint32_t)(uintptr_t)((lds_ptr_t*)klds), vbase = (uint32_t)(uintptr_t)((lds_ptr_t*)vlds);
+    // the environment's page table, one entry per lane, read once: a copy must
+    // not wait on a load of its own (the wait would also drain every copy
+    // issued before it)
+    int ptv = pt[min(lane, last_page)];
+    // the copies below use ptv; passing it through an empty asm ends the load's
+    // lifetime here, so the compiler waits for it once and not before each copy
+    asm volatile("" : "+v"(ptv));
+    for (int i = wave; i < CP * nch; i += 8) {
+      const int c = i / CP, sub = i % CP;
+      if (sub < KC) {
+        const int kcopy = c * KC + sub;  // 1 KB of K rows, all in one 16-key page
+        const int R = kcopy * KROWS_PER_KB + lane / KCH, slot = lane % KCH;
+        const int key = kperm(R);
+        const int page = __builtin_amdgcn_readlane(ptv, min(kperm(kcopy * KROWS_PER_KB) / kPage, last_page));
+        const uint32_t off = (uint32_t)((((page * H + head) * kPage + key % kPage) * HD + 8 * (slot ^ kswz<HD>(R))) * 2);
+        lds_dma16(kbase + kcopy * 1024, off, rk, 0);
+      } else {
+        const int vcopy = c * VC + (sub - KC);  // 1 KB of V^T pages
+        const int pg = vcopy / (VPAGE / 1024);
+        const int unit = (vcopy % (VPAGE / 1024)) * 64 + lane;  // 16-byte unit of the page
+        const int f = unit >> 1, h = (unit & 1) ^ ((f >> 3) & 1);
+        const int page = __builtin_amdgcn_readlane(ptv, min(pg, last_page));
+        const uint32_t off = (uint32_t)((((page * H + head) * HD + f) * kPage + 8 * h) * 2);
+        lds_dma16(vbase + vcopy * 1024, off, rv, 0);
+      }
+    }
+  }
+  // phase 1: the tiles whose keys lie in the first h1 chunks start as soon as
+  // those chunks have landed, while the rest are still being copied
+  const int h1 = min(nch, kMaxChunks / 2);
+  const int nq = (L + 15) / 16;
+  const int q1 = min(nq, 2 * h1);  // tiles 0 .. q1-1 need chunks < h1
+  switch ((nch - h1) * (CP / 8)) {  // this wave's copies of the later chunks may stay in flight
+    case 0: WAIT_VMCNT(0); break;
+    case 1: WAIT_VMCNT(1); break;
+    case 2: WAIT_VMCNT(2); break;
+    case 3: WAIT_VMCNT(3); break;
+    case 4: WAIT_VMCNT(4); break;
+    case 5: WAIT_VMCNT(5); break;
+    case 6: WAIT_VMCNT(6); break;
+    case 7: WAIT_VMCNT(7); break;
+    case 8: WAIT_VMCNT(8); break;
+    case 9: WAIT_VMCNT(9); break;
+    default: WAIT_VMCNT(10); break;
+  }
+  __syncthreads();
+  attn_tiles<HD>(a, klds, vlds, 0, q1, L, row0, head, wave, lane);
+  if (q1 < nq) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    attn_tiles<HD>(a, klds, vlds, q1, nq, L, row0, head, wave, lane);
+  }
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
   constexpr int LPK = HD / 8;          // lanes per key row
   constexpr int KPP = 256 / LPK;       // keys per pass
   constexpr int G = 256 / HD;          // feature groups in P*V
-  __shared__ float sc[kMaxKeyTiles * 16];
+  __shared__ float sc[kMaxKeys];
   __shared__ float qs[HD];
   __shared__ float red[4];
   __shared__ float op[G][HD];
@@ -380,8 +421,8 @@ __global__ __launch_bounds__(256) void sampler_kernel(SamplerArgs a) {
 }  // namespace
 
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s) {
-  if (a.n_qblocks <= 0) return hipSuccess;
-  const dim3 grid(a.n_qblocks, a.n_heads), block(256);
+  if (a.n_env <= 0) return hipSuccess;
+  const dim3 grid(a.n_env, a.n_heads), block(512);
   if (a.head_dim == 128) hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, block, 0, s, a);
   else if (a.head_dim == 64) hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, block, 0, s, a);
   else return hipErrorInvalidValue;

@@ -87,4 +87,21 @@ __host__ __device__ __forceinline__ size_t frag_index(int r, int k, int K) {
   return ((((size_t)(r >> 4) * frag_kb(K) + (k >> 5)) << 6) + (r & 15) + (((k & 31) >> 3) << 4)) * 8 + (k & 7);
 }
 
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+// s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) >> 4) << 14) | (0xF << 8) | (0x7 << 4) | ((n) & 15))
+
+// 16 bytes per lane from a buffer straight into LDS (buffer_load_dwordx4 ... lds):
+// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS byte address
+// m0.  Issued through inline assembly so that the compiler does not treat it
+// as an LDS store (it would wait for every copy in flight before any later LDS
+// read); the kernel waits for the copies it consumes itself.
+__device__ __forceinline__ void lds_dma16(uint32_t m0, uint32_t voff, __amdgpu_buffer_rsrc_t rsrc, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory");
+}
+
 }  // namespace vla

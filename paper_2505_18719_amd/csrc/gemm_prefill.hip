@@ -61,23 +61,6 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
 // nothing may be scheduled across this point
 #define PIN() __builtin_amdgcn_sched_barrier(0)
 
-typedef __attribute__((address_space(3))) void lds_ptr_t;
-
-// s_waitcnt with vmcnt <= n (n < 64) and the other counters unconstrained.
-#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) >> 4) << 14) | (0xF << 8) | (0x7 << 4) | ((n) & 15))
-
-// 16 bytes per lane from a buffer straight into LDS (buffer_load_dwordx4 ... lds):
-// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS byte address
-// m0.  Issued through inline assembly so that the compiler does not treat it
-// as an LDS store (it would wait for every copy in flight before any later LDS
-// read); the kernel waits for the copies it consumes itself.
-__device__ __forceinline__ void dma16(uint32_t m0, uint32_t voff, __amdgpu_buffer_rsrc_t rsrc, int soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :
-               : "s"(m0), "v"(voff), "s"(rsrc), "s"(soff)
-               : "memory");
-}
-
 // Epilogues that pair column c of a 64-column group with column c + 32:
 // SwiGLU (gate rows, then the matching up rows) and the QKV projection
 // (rotary pairs).  v1, v2: float4 chunks q and q + 8 of output row `row`,
@@ -160,7 +143,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const uint32_t lds_base = (uint32_t)(uintptr_t)((lds_ptr_t*)&lds[0][0]);
   auto copy = [&](int j, int st, int ks) {
     const int b = wave * 4 + j;
-    dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb0 + (b & 15), rb_last) * KB + ks) * 1024);
+    lds_dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb0 + (b & 15), rb_last) * KB + ks) * 1024);
   };
 
   f32x4 acc[8][4];

@@ -153,9 +153,8 @@ struct PrefillAttnArgs {
   const int32_t* page_table;
   int max_pages;
   const int32_t* env_row0;    // [B] first packed row of env b
-  const int32_t* env_len;     // [B] rows of env b in this pass
-  const int32_t* qblocks;     // [n_qblocks, 2] (env, first query row)
-  int n_qblocks, d, n_heads, head_dim;
+  const int32_t* env_len;     // [B] rows of env b in this pass (<= 320)
+  int n_env, d, n_heads, head_dim;
   float scale;
 };
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);

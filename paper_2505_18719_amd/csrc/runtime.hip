@@ -35,7 +35,6 @@ int fail(int code, const std::string& msg) {
 
 constexpr int kMaxSplits = 16;
 constexpr int kSkinnyRows = 128;
-constexpr int kQBlock = 64;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up(int v, int a) { return (v + a - 1) / a * a; }
@@ -46,7 +45,6 @@ struct Dims {
   int Bmax, Smax, max_pages, n_pages;
   size_t Mmax;      // packed rows of the largest pass
   int Nmax;         // widest skinny GEMM
-  int qblk_max;
   size_t meta_ints;
 };
 
@@ -88,8 +86,7 @@ int check_config(const vla_config* c, Dims* o) {
   D.n_pages = D.max_pages * D.Bmax;
   D.Mmax = (size_t)D.Bmax * D.Smax;
   D.Nmax = std::max(std::max(3 * D.d, 2 * D.Fp), D.Ap);
-  D.qblk_max = D.Bmax * ((D.Smax + kQBlock - 1) / kQBlock);
-  D.meta_ints = 2 * D.Mmax + 4 * (size_t)D.Bmax + (size_t)D.Bmax * D.max_pages + 2 * (size_t)D.qblk_max +
+  D.meta_ints = 2 * D.Mmax + 4 * (size_t)D.Bmax + (size_t)D.Bmax * D.max_pages +
                 (size_t)D.Bmax * D.nact;
   return VLA_OK;
 }
@@ -139,7 +136,7 @@ struct vla_model {
   hipEvent_t meta_event;
   bool meta_pending;
   // device views into meta_dev
-  int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *page_table, *qblocks, *head_rows;
+  int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *page_table, *head_rows;
   // decode state
   int state_batch;
   bool state_valid;
@@ -213,7 +210,6 @@ void set_meta_views(vla_model* m, int32_t* base) {
   m->env_prefix = p; p += D.Bmax;
   m->env_prompt_off = p; p += D.Bmax;
   m->page_table = p; p += (size_t)D.Bmax * D.max_pages;
-  m->qblocks = p; p += 2 * (size_t)D.qblk_max;
   m->head_rows = p;
 }
 
@@ -275,7 +271,6 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   const bool tf = actions != nullptr;
   std::vector<int> prefix(B), rows(B);
   size_t M = 0;
-  int nq = 0;
   for (int b = 0; b < B; ++b) {
     if (lens_host[b] < 0) return fail(VLA_EINVAL, "negative prompt length");
     prefix[b] = D.nvis + lens_host[b];
@@ -283,7 +278,6 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     if (prefix[b] + D.nact > D.Smax) return fail(VLA_ESHAPE, "n_visual + prompt + n_actions exceeds max_seq");
     rows[b] = prefix[b] + (tf ? D.nact : 0);
     M += rows[b];
-    nq += (rows[b] + kQBlock - 1) / kQBlock;
   }
   // host metadata -> pinned staging -> one async upload
   if (m->meta_pending) {
@@ -298,10 +292,9 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   int32_t* hpre = h + meta_index(m, m->env_prefix);
   int32_t* hpo = h + meta_index(m, m->env_prompt_off);
   int32_t* hpt = h + meta_index(m, m->page_table);
-  int32_t* hq = h + meta_index(m, m->qblocks);
   int32_t* hh = h + meta_index(m, m->head_rows);
   size_t r = 0;
-  int po = 0, qi = 0;
+  int po = 0;
   for (int b = 0; b < B; ++b) {
     hr0[b] = (int32_t)r;
     hl[b] = rows[b];
@@ -315,10 +308,6 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     // pages of env b are interleaved with the other environments' pages
     const int np = (prefix[b] + D.nact + kPage - 1) / kPage;
     for (int p = 0; p < D.max_pages; ++p) hpt[(size_t)b * D.max_pages + p] = p < np ? p * B + b : 0;
-    for (int q0 = 0; q0 < rows[b]; q0 += kQBlock, ++qi) {
-      hq[2 * qi] = b;
-      hq[2 * qi + 1] = q0;
-    }
     if (tf) {
       for (int i = 0; i < D.nact; ++i) hh[b * D.nact + i] = hr0[b] + prefix[b] - 1 + i;
     } else {
@@ -347,8 +336,8 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
     g.d_model = D.d; g.n_heads = D.H; g.head_dim = D.hd;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 3.0 * D.d, D.d), launch_gemm(g, kEpiQkvRope, s));
-    PrefillAttnArgs pa{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, m->qblocks,
-                       nq, D.d, D.H, D.hd, m->scale};
+    PrefillAttnArgs pa{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
+                       B, D.d, D.H, D.hd, m->scale};
     PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, attn_flops, launch_attn_prefill(pa, s));
     GemmArgs go{};
     go.A = m->u; go.W = w.wo; go.M = Mi; go.N = D.d; go.K = D.d; go.C = m->x; go.ldc = D.d;
