@@ -254,15 +254,57 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
   constexpr int LPK = HD / 8;          // lanes per key row
   constexpr int KPP = 256 / LPK;       // keys per pass
   constexpr int G = 256 / HD;          // feature groups in P*V
+  constexpr int HALF = HD / 2;
   __shared__ float sc[kMaxKeys];
-  __shared__ float qs[HD];
+  __shared__ float qs[HD], kn[HD], vn[HD];  // this token's rotated q, k and its v (bf16 values)
   __shared__ float red[4];
   __shared__ float op[G][HD];
   const int head = blockIdx.x, b = blockIdx.y;
   const int H = a.n_heads, tid = threadIdx.x;
-  const int n = a.env_prefix[b] + a.step;  // keys 0 .. n-1
+  const int n = a.env_prefix[b] + a.step;  // keys 0 .. n-1; key n-1 is this step's token
+  const int pos = n - 1;
   const int32_t* pt = a.page_table + b * a.max_pages;
-  if (tid < HD) qs[tid] = bf2f(a.q[(size_t)b * a.d + head * HD + tid]);
+
+  // ---- q, k, v of the token for this head: one thread per rotary pair of
+  // q and k (columns permuted per head as for the prefill GEMM's epilogue:
+  // pair (32 blk + c, HALF + 32 blk + c) sits in columns 64 blk + c and
+  // 64 blk + c + 32 of the head) and per pair of v features (e, e + HALF)
+  if (tid < 3 * HALF) {
+    const int region = tid / HALF, e = tid % HALF;
+    const int N = 3 * a.d;
+    int col1, col2;
+    if (region < 2) {
+      col1 = region * a.d + head * HD + 64 * (e / 32) + e % 32;
+      col2 = col1 + 32;
+    } else {
+      col1 = 2 * a.d + head * HD + e;
+      col2 = col1 + HALF;
+    }
+    const float x1 = skinny_sum(a.part, a.plan, a.B, N, b, col1);
+    const float x2 = skinny_sum(a.part, a.plan, a.B, N, b, col2);
+    const int page = pt[pos / kPage], slot = pos % kPage;
+    if (region == 2) {
+      const bf16_t v1 = f2bf(x1), v2 = f2bf(x2);
+      bf16_t* vb = a.kv.v + ((size_t)page * H + head) * HD * kPage + slot;
+      vb[(size_t)e * kPage] = v1;
+      vb[(size_t)(e + HALF) * kPage] = v2;
+      vn[e] = bf2f(v1);
+      vn[e + HALF] = bf2f(v2);
+    } else {
+      const float2 cs = a.rope[pos * HALF + e];
+      const bf16_t r1 = f2bf(x1 * cs.x - x2 * cs.y), r2 = f2bf(x1 * cs.y + x2 * cs.x);
+      if (region == 0) {
+        qs[e] = bf2f(r1);
+        qs[e + HALF] = bf2f(r2);
+      } else {
+        bf16_t* kr = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD;
+        kr[e] = r1;
+        kr[e + HALF] = r2;
+        kn[e] = bf2f(r1);
+        kn[e + HALF] = bf2f(r2);
+      }
+    }
+  }
   __syncthreads();
 
   const int part = tid % LPK;
@@ -273,10 +315,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
     const int key = base + tid / LPK;
     float acc = 0.f;
     if (key < n) {
-      const int page = pt[key / kPage];
-      const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + key % kPage) * HD + part * 8;
       float kf[8];
-      unpack8(*reinterpret_cast<const uint4*>(kp), kf);
+      if (key < pos) {
+        const int page = pt[key / kPage];
+        const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + key % kPage) * HD + part * 8;
+        unpack8(*reinterpret_cast<const uint4*>(kp), kf);
+      } else {  // this step's token
+#pragma unroll
+        for (int j = 0; j < 8; ++j) kf[j] = kn[part * 8 + j];
+      }
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc += qv[j] * kf[j];
     }
@@ -313,9 +360,10 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
     unpack8(*reinterpret_cast<const uint4*>(vp), vf);
     unpack8(*reinterpret_cast<const uint4*>(vp + 8), vf + 8);
     const int lim = min(kPage, n - pg * kPage);
+    const float vnew = vn[i];
 #pragma unroll
     for (int j = 0; j < kPage; ++j)
-      if (j < lim) acc += sc[pg * kPage + j] * vf[j];
+      if (j < lim) acc += sc[pg * kPage + j] * (pg * kPage + j == pos ? vnew : vf[j]);  // the token's v from LDS
   }
   op[grp][i] = acc;
   __syncthreads();

@@ -178,14 +178,6 @@ __global__ __launch_bounds__(256) void embed_token_norm_kernel(const int32_t* to
   }
 }
 
-// Sum of the partial slots of column n of a skinny GEMM (N columns) at row m.
-__device__ __forceinline__ float skinny_sum(const float* __restrict__ part, const SkinnyPlan& p, int M, int N, int m,
-                                            int n) {
-  const int ns = skinny_slots(p, n >> 6);
-  float v = 0.f;
-  for (int s = 0; s < ns; ++s) v += part[((size_t)s * M + m) * N + n];
-  return v;
-}
 
 // One 1024-thread workgroup per row: 4 consecutive columns per thread and
 // pass (two passes cover d <= 8192), every partial slot's float4 in flight together.
@@ -254,50 +246,6 @@ __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restr
   auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
   *reinterpret_cast<uint2*>(h + frag_index(m, j, ldh)) =
       make_uint2(pack2bf(sw(gs.x, us.x), sw(gs.y, us.y)), pack2bf(sw(gs.z, us.z), sw(gs.w, us.w)));
-}
-
-// One thread per rotary pair of q and k, and per pair of v features.
-__global__ __launch_bounds__(256) void decode_qkv_kernel(DecodeQkvArgs a) {
-  const int b = blockIdx.y;
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  const int d = a.d, hd = a.head_dim, half = hd / 2, H = a.n_heads;
-  if (t >= 3 * (d / 2)) return;
-  const int region = t / (d / 2);
-  const int p = t - region * (d / 2);            // pair index within the region
-  const int head = p / half, e = p % half;       // e in [0, half)
-  const int N = 3 * d;
-  // permuted columns of the pair (see the prefill GEMM's RoPE epilogue)
-  const int blk = e / 32, c = e % 32;
-  int col1, col2;
-  if (region < 2) {
-    col1 = region * d + head * hd + 64 * blk + c;
-    col2 = col1 + 32;
-  } else {  // v keeps the natural order: features e and e + half
-    col1 = 2 * d + head * hd + e;
-    col2 = col1 + half;
-  }
-  const float x1 = skinny_sum(a.part, a.plan, a.B, N, b, col1);
-  const float x2 = skinny_sum(a.part, a.plan, a.B, N, b, col2);
-  const int pos = a.env_prefix[b] + a.step - 1;
-  if (region == 0) {
-    const float2 cs = a.rope[pos * half + e];
-    bf16_t* qr = a.q + (size_t)b * d + head * hd;
-    qr[e] = f2bf(x1 * cs.x - x2 * cs.y);
-    qr[e + half] = f2bf(x1 * cs.y + x2 * cs.x);
-    return;
-  }
-  const int page = a.page_table[b * a.max_pages + pos / kPage];
-  const int slot = pos % kPage;
-  if (region == 1) {
-    const float2 cs = a.rope[pos * half + e];
-    bf16_t* kr = a.kv.k + (((size_t)page * H + head) * kPage + slot) * hd;
-    kr[e] = f2bf(x1 * cs.x - x2 * cs.y);
-    kr[e + half] = f2bf(x1 * cs.y + x2 * cs.x);
-  } else {
-    bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + slot;
-    vb[(size_t)e * kPage] = f2bf(x1);
-    vb[(size_t)(e + half) * kPage] = f2bf(x2);
-  }
 }
 
 // ------------------------------------------------------------------ repacking
@@ -415,13 +363,6 @@ hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* 
   if (n == 0) return hipSuccess;
   if (2 * F > p.tiles * 64 || F % 32 != 0 || ldh < F) return hipErrorInvalidValue;
   hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, p, h, ldh, M, F);
-  return hipGetLastError();
-}
-
-hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s) {
-  if (a.B <= 0) return hipSuccess;
-  const int threads = 3 * (a.d / 2);
-  hipLaunchKernelGGL(decode_qkv_kernel, dim3((threads + 255) / 256, a.B), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

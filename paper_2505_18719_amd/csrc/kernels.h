@@ -86,6 +86,13 @@ __host__ __device__ inline int skinny_slots(const SkinnyPlan& p, int tile) {
   const int U = (p.tiles - p.dp_tiles) * p.chunks, t = tile - p.dp_tiles;
   return skinny_owner((t + 1) * p.chunks - 1, U, p.G) - skinny_owner(t * p.chunks, U, p.G) + 1;
 }
+// Sum of the partial slots of column n of a skinny GEMM (N columns) at row m.
+__device__ inline float skinny_sum(const float* __restrict__ part, const SkinnyPlan& p, int M, int N, int m, int n) {
+  const int ns = skinny_slots(p, n >> 6);
+  float v = 0.f;
+  for (int s = 0; s < ns; ++s) v += part[((size_t)s * M + m) * N + n];
+  return v;
+}
 // The plan for `workgroups` workgroups, with fewer if needed to keep every tile within `max_slots`.
 SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots);
 hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t s);
@@ -131,19 +138,6 @@ hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* 
 
 // Decode: sum QKV partials, RoPE at position env_prefix[b] + step - 1, store q
 // and append K/V of the new token to the page pool.
-struct DecodeQkvArgs {
-  const float* part;
-  SkinnyPlan plan;
-  bf16_t* q;
-  KvCache kv;
-  const int32_t* page_table;
-  int max_pages;
-  const int32_t* env_prefix;
-  int step;  // 1-based decode step: token position = env_prefix[b] + step - 1
-  const float2* rope;
-  int B, d, n_heads, head_dim;
-};
-hipError_t launch_decode_qkv(const DecodeQkvArgs& a, hipStream_t s);
 
 // Attention
 struct PrefillAttnArgs {
@@ -159,14 +153,21 @@ struct PrefillAttnArgs {
 };
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
 
+// Decode attention fused with the QKV projection's consumer: each workgroup
+// (head, environment) first sums the partial slots of its q, k, v columns,
+// rotates q and k, appends k and v to the page pool at the token's position,
+// then attends over keys 0 .. env_prefix[b] + step - 1 (the last one is the
+// token itself, taken from LDS with the same bf16 rounding).
 struct DecodeAttnArgs {
-  const bf16_t* q;  // [B, d]
-  bf16_t* o;        // [B, d] in frag layout
+  const float* part;   // QKV projection partial slots [plan.slots, B, 3 d] (q, k rows permuted per head)
+  SkinnyPlan plan;
+  const float2* rope;  // [pos][head_dim / 2] (cos, sin)
+  bf16_t* o;           // [B, d] in frag layout
   KvCache kv;
   const int32_t* page_table;
   int max_pages;
   const int32_t* env_prefix;
-  int step;  // keys 0 .. env_prefix[b] + step - 1
+  int step;  // 1-based decode step: token position = env_prefix[b] + step - 1
   int B, d, n_heads, head_dim;
   float scale;
 };

@@ -539,11 +539,8 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
         const LayerW& w = m->lw[l];
         SkinnyArgs sq{m->u, B, w.wqkv, 3 * D.d, D.d, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, m->plan_qkv, s));
-        DecodeQkvArgs qa{m->part, m->plan_qkv, m->q, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i,
-                         m->rope, B, D.d, D.H, D.hd};
-        VLA_CK(launch_decode_qkv(qa, s));
-        DecodeAttnArgs da{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix, i, B, D.d, D.H, D.hd,
-                          m->scale};
+        DecodeAttnArgs da{m->part, m->plan_qkv, m->rope, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix,
+                          i, B, D.d, D.H, D.hd, m->scale};
         PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
         SkinnyArgs so{m->u, B, w.wo, D.d, D.d, m->part};
         PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, m->plan_o, s));
