@@ -259,11 +259,13 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
   __shared__ float qs[HD], kn[HD], vn[HD];  // this token's rotated q, k and its v (bf16 values)
   __shared__ float red[4];
   __shared__ float op[G][HD];
+  __shared__ int ptl[kMaxPages];  // the environment's page table
   const int head = blockIdx.x, b = blockIdx.y;
   const int H = a.n_heads, tid = threadIdx.x;
   const int n = a.env_prefix[b] + a.step;  // keys 0 .. n-1; key n-1 is this step's token
   const int pos = n - 1;
   const int32_t* pt = a.page_table + b * a.max_pages;
+  if (tid < a.max_pages) ptl[tid] = pt[tid];
 
   // ---- q, k, v of the token for this head: one thread per rotary pair of
   // q and k (columns permuted per head as for the prefill GEMM's epilogue:
@@ -311,14 +313,14 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
   float qv[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) qv[j] = qs[part * 8 + j];
+  // scores: one key row per LPK lanes
   for (int base = 0; base < n; base += KPP) {
     const int key = base + tid / LPK;
     float acc = 0.f;
     if (key < n) {
       float kf[8];
       if (key < pos) {
-        const int page = pt[key / kPage];
-        const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + key % kPage) * HD + part * 8;
+        const bf16_t* kp = a.kv.k + (((size_t)ptl[key / kPage] * H + head) * kPage + key % kPage) * HD + part * 8;
         unpack8(*reinterpret_cast<const uint4*>(kp), kf);
       } else {  // this step's token
 #pragma unroll
@@ -352,15 +354,14 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
   s = red[0] + red[1] + red[2] + red[3];
 
   const int i = tid % HD, grp = tid / HD;
+  const float vnew = vn[i];
   float acc = 0.f;
   for (int pg = grp; pg * kPage < n; pg += G) {
-    const int page = pt[pg];
-    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + i) * kPage;
+    const bf16_t* vp = a.kv.v + (((size_t)ptl[pg] * H + head) * HD + i) * kPage;
     float vf[16];
     unpack8(*reinterpret_cast<const uint4*>(vp), vf);
     unpack8(*reinterpret_cast<const uint4*>(vp + 8), vf + 8);
     const int lim = min(kPage, n - pg * kPage);
-    const float vnew = vn[i];
 #pragma unroll
     for (int j = 0; j < kPage; ++j)
       if (j < lim) acc += sc[pg * kPage + j] * (pg * kPage + j == pos ? vnew : vf[j]);  // the token's v from LDS
