@@ -37,6 +37,19 @@ def test_prefill_gemm_matches_float64(M, N, K):
     _check_matmul(C, A, W, "gemm")
 
 
+def test_prefill_gemm_rows_independent_of_tiling():
+    """A row's result is bit-identical however many rows are multiplied with it
+    (one workgroup round at M = 256, forty tile rows and a partial last round
+    at M = 10240): the batch-composition invariance of the prefill GEMM."""
+    from paper_2505_18719_amd import vla
+    A, W = _rand_bf16((10240, 512), 11), _rand_bf16((2048, 512), 12, 0.02)
+    C_small = vla.debug_gemm(A[:256].contiguous(), W)
+    C_big = vla.debug_gemm(A, W)
+    torch.cuda.synchronize()
+    assert torch.equal(C_small, C_big[:256])
+    _check_matmul(C_big[-300:], A[-300:], W, "gemm-last-round")
+
+
 def test_prefill_gemm_7b_shape_sampled_rows():
     """QKV projection at the 7B batch-64 prefill shape (M = 18432 packed rows)."""
     from paper_2505_18719_amd import vla
