@@ -4,7 +4,8 @@ Imported by the test-suite, the smoke check and the benchmark's CPU-baseline
 leg; never by the library.  See ``vla_oracle`` for what it computes.
 """
 from .vla_oracle import (MODES, Weights, action_logits, apply_rope, as_weights, bf16_round,  # noqa: F401
-                         causal_attention, decoder_layer, forward_rows, prefill_logits,
+                         causal_attention, decoder_layer, forward_rows, lora_merge, merge_weights,
+                         prefill_logits,
                          prefix_embeddings, rms_norm, rollout, rollout_env, rope_angles,
                          sample_bin, silu, teacher_forced, teacher_forced_env, to_f64,
                          token_stats)

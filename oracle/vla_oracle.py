@@ -13,7 +13,9 @@ What it computes (VLA-RL, arXiv 2505.18719):
     Eq. 1 (Alg. 1, rollout phase), and the entropy of each token distribution
     (the rollout entropy monitored in Sec. 4.2);
   * the teacher-forced recompute of those log-probabilities for stored
-    actions, i.e. the numerator of the PPO ratio of Eq. 2.
+    actions, i.e. the numerator of the PPO ratio of Eq. 2;
+  * the weights the rollout runs on: the original checkpoint with the updated
+    LoRA adapters merged in, rounded to bf16 (Sec. 3.3, Rollout Phase).
 
 The decoder block is the standard Llama-2 one: pre-RMSNorm, rotary position
 embedding (half-split pairing), causal softmax attention, SwiGLU MLP and
@@ -351,3 +353,30 @@ def prefill_logits(cfg, w, vis, prompt_ids, prompt_lens, mode: str = "bf16",
     envs = list(range(len(prompts))) if envs is None else list(envs)
     rows = [forward_rows(cfg, W, prefix_embeddings(cfg, W, vis[b], prompts[b]), mode)[-1:] for b in envs]
     return action_logits(cfg, W, np.concatenate(rows), rnd)
+
+
+# ----------------------------------------------------------------------------
+# LoRA merge (Sec. 3.3, Rollout Phase: the updated LoRA weights are merged with
+# the original checkpoint before the rollout)
+# ----------------------------------------------------------------------------
+def lora_merge(w0, lora_a, lora_b, scale: float) -> np.ndarray:
+    """Merged weight of one linear layer, W = W0 + scale * B A (LoRA: a rank-r
+    update B [out, r] A [r, in] of W0 [out, in], scale = alpha / r), computed in
+    float64 from the original weights and rounded to bf16 (nearest even,
+    through float32 -- the precision the kernel rounds from).  Returns float64."""
+    return bf16_round(to_f64(w0) + float(scale) * (to_f64(lora_b) @ to_f64(lora_a)))
+
+
+def merge_weights(w: Dict[str, object], adapters: List[Dict[str, tuple]], scale: float,
+                  layers: Optional[Sequence[int]] = None) -> Dict[str, object]:
+    """A copy of the weight set ``w`` (bf16 torch tensors) with ``adapters[i]``
+    (per projection key: (A, B)) merged into layer ``layers[i]`` (all layers in
+    order by default)."""
+    layers = list(range(len(adapters))) if layers is None else list(layers)
+    out = {k: v for k, v in w.items() if k != "layers"}
+    out["layers"] = [dict(lw) for lw in w["layers"]]
+    for li, ad in zip(layers, adapters):
+        for k, (a, b) in ad.items():
+            m = lora_merge(w["layers"][li][k], a, b, scale)
+            out["layers"][li][k] = torch.from_numpy(m).to(torch.bfloat16)
+    return out

@@ -26,7 +26,7 @@ import numpy as np
 import torch
 
 # Stream ids of SeedSequence([seed, stream, ...]).
-_S_WEIGHT, _S_VIS, _S_PROMPT_LEN, _S_PROMPT_ID, _S_GUMBEL, _S_ACTIONS, _S_GAIN = range(7)
+_S_WEIGHT, _S_VIS, _S_PROMPT_LEN, _S_PROMPT_ID, _S_GUMBEL, _S_ACTIONS, _S_GAIN, _S_LORA = range(8)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -134,6 +134,28 @@ def make_weights(cfg: VlaConfig, seed: int = 0, device="cpu", std: float = 0.02,
                 lw[k] = _normal(shp, std, (seed, _S_WEIGHT, 100 + li, j), dev)
         w["layers"].append(lw)
     return w
+
+
+# Linear layers a LoRA adapter attaches to, with the weight-dict key of each.
+LORA_PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
+
+
+def make_lora(cfg: VlaConfig, rank: int, seed: int = 0, device="cpu", std: float = 0.02,
+              layers=None) -> List[Dict[str, tuple]]:
+    """Seeded LoRA adapters for every projection of the given layers (all by
+    default): per layer ``{key: (A [rank, in_features], B [out_features, rank])}``,
+    bf16, entries ~ N(0, std) (a trained adapter has both factors non-zero)."""
+    layers = range(cfg.n_layers) if layers is None else layers
+    shapes = layer_shapes(cfg)
+    out = []
+    for li in layers:
+        ad = {}
+        for j, k in enumerate(LORA_PROJECTIONS):
+            n_out, n_in = shapes[k]
+            ad[k] = (_normal((rank, n_in), std, (seed, _S_LORA, li, j, 0), torch.device(device)),
+                     _normal((n_out, rank), std, (seed, _S_LORA, li, j, 1), torch.device(device)))
+        out.append(ad)
+    return out
 
 
 def weights_to(w: Dict[str, object], device) -> Dict[str, object]:

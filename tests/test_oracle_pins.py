@@ -285,3 +285,74 @@ def test_rollout_outputs_are_action_tokens_and_consistent(pin_setup):
         for i in range(PIN.n_actions):
             s = r["logits"][b, i] / 1.5 + inp.gumbel[b, i]
             assert r["tokens"][b, i] - PIN.action_begin == int(np.argmax(s))
+
+
+# ---------------------------------------------------------------------------
+# LoRA merge (Sec. 3.3, Rollout Phase)
+# ---------------------------------------------------------------------------
+def _bf16(x):
+    return torch.as_tensor(np.asarray(x, dtype=np.float32)).to(torch.bfloat16)
+
+
+def test_lora_merge_zero_update_returns_the_checkpoint_exactly():
+    g = torch.Generator().manual_seed(21)
+    w0 = (torch.randn(48, 80, generator=g) * 0.02).to(torch.bfloat16)
+    a = (torch.randn(8, 80, generator=g) * 0.02).to(torch.bfloat16)
+    b = torch.zeros(48, 8, dtype=torch.bfloat16)
+    m = oracle.lora_merge(w0, a, b, 0.5)
+    assert np.array_equal(m, w0.double().numpy())
+
+
+def test_lora_merge_exact_rank_one_case():
+    """Rank 1 with values whose products and sums are exact in bf16:
+    W0 = 1/2 everywhere, B = [0, 1/8, 1/4, ...] (column), A = [1, 2, 4, ...]
+    (row), scale 2 -> W[i, j] = 1/2 + 2 * (i/8) * 2^j."""
+    rows, cols = 6, 5
+    w0 = _bf16(np.full((rows, cols), 0.5))
+    b = _bf16(np.arange(rows)[:, None] / 8.0)
+    a = _bf16(2.0 ** np.arange(cols)[None, :])
+    expect = 0.5 + 2.0 * (np.arange(rows)[:, None] / 8.0) * (2.0 ** np.arange(cols)[None, :])
+    assert np.array_equal(oracle.lora_merge(w0, a, b, 2.0), expect)
+
+
+def test_lora_merge_rounds_to_nearest_even():
+    """1 + 2^-8 lies halfway between the bf16 neighbours 1 and 1 + 2^-7: the
+    even one (1) wins; 1 + 3 * 2^-8 rounds up to the even 1 + 2^-6."""
+    w0 = _bf16([[1.0, 1.0]])
+    a = _bf16([[1.0, 3.0]])
+    b = _bf16([[2.0 ** -8]])
+    assert np.array_equal(oracle.lora_merge(w0, a, b, 1.0), [[1.0, 1.0 + 2.0 ** -6]])
+
+
+def test_lora_merge_matches_the_unmerged_lora_forward():
+    """The merged layer applied to inputs equals the LoRA forward pass
+    x W0^T + scale (x A^T) B^T up to the bf16 rounding of the merged weights
+    (relative error <= 2^-9 per element): catches a transposed product, a wrong
+    scale or sign, or factors used in the wrong order."""
+    g = torch.Generator().manual_seed(22)
+    out_f, in_f, r, scale = 96, 160, 16, 0.75
+    w0 = (torch.randn(out_f, in_f, generator=g) * 0.02).to(torch.bfloat16)
+    a = (torch.randn(r, in_f, generator=g) * 0.05).to(torch.bfloat16)
+    b = (torch.randn(out_f, r, generator=g) * 0.05).to(torch.bfloat16)
+    x = torch.randn(7, in_f, generator=g, dtype=torch.float64)
+    merged = torch.from_numpy(oracle.lora_merge(w0, a, b, scale))
+    lora = torch.nn.functional.linear(x, w0.double()) + scale * torch.nn.functional.linear(
+        torch.nn.functional.linear(x, a.double()), b.double())
+    got = torch.nn.functional.linear(x, merged)
+    exact_w = w0.double() + scale * (b.double() @ a.double())
+    bound = 2.0 ** -9 * (x.abs() @ exact_w.abs().t()) + 1e-12
+    assert bool(((got - lora).abs() <= bound).all())
+    # and the update is really there: dropping it is far outside the bound
+    assert bool(((torch.nn.functional.linear(x, w0.double()) - lora).abs() > bound).any())
+
+
+def test_merge_weights_touches_only_the_adapted_projections():
+    from paper_2505_18719_amd.inputs import make_lora
+    w = make_weights(PIN, seed=23)
+    ad = make_lora(PIN, 4, seed=23, layers=[1])
+    m = oracle.merge_weights(w, ad, 0.5, layers=[1])
+    for li, lw in enumerate(w["layers"]):
+        for k, t in lw.items():
+            same = torch.equal(m["layers"][li][k], t)
+            assert same == (li != 1 or k.endswith("norm")), (li, k)
+    assert torch.equal(m["embed"], w["embed"]) and torch.equal(m["lm_head"], w["lm_head"])
