@@ -147,6 +147,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=8, help="decoder layers in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher-forced", action="store_true")
+    ap.add_argument("--no-lora-merge", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain streaming kernel of known size before timing (HBM counter calibration)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -307,6 +308,36 @@ def main():
         result["teacher_forced"] = {"ms": tf_ms, "rows": int(Lb.sum()),
                                     "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                     "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
+
+    if not args.no_lora_merge:
+        # LoRA merge before a rollout (Sec. 3.3): every projection of every layer,
+        # rank 32, from the original checkpoint; timed after the rollout figures
+        rank = 32
+        adapters = I.make_lora(cfg, rank, seed=0, device=dev)
+        def merge_all():
+            for li, ad in enumerate(adapters):
+                for key, (a, b) in ad.items():
+                    model.lora_merge(li, key, w["layers"][li][key], a, b, 0.5)
+        merge_all()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(3):
+            merge_all()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        merge_ms = e0.elapsed_time(e1) / 3
+        Fp = (F + 255) // 256 * 256
+        # algorithmic bytes: the original weights read, the packed weights written, the adapters read
+        merge_bytes = L * 2.0 * (4 * d * d + 3 * d * F                # W0
+                                 + 4 * d * d + 2 * Fp * d + d * Fp    # packed (gate/up rows and down columns padded to Fp)
+                                 + rank * (4 * d + 2 * d + F)         # A factors [rank, in]
+                                 + rank * (4 * d + 2 * F + d))        # B factors [out, rank]
+        result["lora_merge"] = {"ms": merge_ms, "rank": rank, "projections": 7 * L,
+                                "achieved": merge_bytes / (merge_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                                "unit": "GB/s", "frac": merge_bytes / (merge_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                                "bytes": merge_bytes}
+        log(f"[bench] LoRA merge of all {7 * L} projections: {merge_ms:.2f} ms")
 
     if not args.no_cpu_baseline:
         log(f"[bench] oracle CPU baseline ({args.cpu_layers} layers of one environment)")

@@ -142,6 +142,33 @@ int vla_decode_actions(vla_model* m, int32_t batch, const float* gumbel, float t
                        int32_t* tokens, float* logp, float* entropy, float* step_logits,
                        void* stream);
 
+/* LoRA merge before a rollout (Sec. 3.3, Rollout Phase: the updated LoRA
+ * weights are merged with the original checkpoint): replaces one projection
+ * of one decoder layer in the handle's packed weights by
+ *     W = bf16(W0 + scale * B A)            (round to nearest even)
+ * where W0 is the ORIGINAL checkpoint weight of that projection (so repeated
+ * merges never accumulate: each starts from W0) and B A the adapter's rank-r
+ * update, summed over r in fp32.  Every other weight is left as it is.
+ *   layer       0 .. n_layers-1
+ *   projection  VLA_PROJ_* (q, k, v, o, gate, up, down)
+ *   w0          bf16 [out, in] row-major, the checkpoint weight as given to
+ *               vla_create (q, k, v, o: [d, d]; gate, up: [d_ffn, d];
+ *               down: [d, d_ffn]); read only
+ *   lora_a      bf16 [rank, in] row-major; lora_b bf16 [out, rank] row-major
+ *   rank        8 <= rank <= 64, a multiple of 8 (else VLA_EUNSUPPORTED)
+ *   scale       alpha / rank of the adapter (finite, else VLA_EINVAL)
+ * Asynchronous on `stream`; later calls on the same stream see the merged
+ * weights.  All pointers are device pointers owned by the caller. */
+#define VLA_PROJ_Q 0
+#define VLA_PROJ_K 1
+#define VLA_PROJ_V 2
+#define VLA_PROJ_O 3
+#define VLA_PROJ_GATE 4
+#define VLA_PROJ_UP 5
+#define VLA_PROJ_DOWN 6
+int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
+                   const void* lora_b, int32_t rank, float scale, void* stream);
+
 /* Teacher-forced pass (numerator of the PPO ratio, Eq. 2): one causal forward
  * over [visual ; prompt ; the n_actions given action tokens] per environment,
  * with no KV reuse, scoring token i by the logits at row L_b - 1 + i.

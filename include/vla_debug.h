@@ -42,7 +42,14 @@ int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, in
 /* Copy `bytes` of an internal buffer of the handle to `dst` (device):
  * which = 0 residual x fp32 [rows, d], 1 rotated q bf16 [rows, d], 2 / 3 the K / V
  * page pool of `layer` (bf16, page layouts of the KV cache), 4 the bf16
- * activation buffer [rows, d] in frag layout (see vla_debug_pack_frag). */
+ * activation buffer [rows, d] in frag layout (see vla_debug_pack_frag); the
+ * packed projection weights of `layer`, bf16 in frag layout: 5 [Wq; Wk; Wv]
+ * [3 d, d] (q and k rows of each head ordered so that each 64-row block holds
+ * rotary pairs 32 rows apart: block b = head rows [32b, 32b+32) then
+ * [hd/2 + 32b, hd/2 + 32b + 32)), 6 Wo [d, d], 7 [Wgate; Wup] [2 Fp, d]
+ * interleaved in blocks of 32 rows (gate rows 32 (r / 64) + r % 32 at r % 64 < 32,
+ * the matching up rows after them; rows past d_ffn zero), 8 Wdown [d, Fp]
+ * (columns past d_ffn zero); Fp = d_ffn rounded up to a multiple of 256. */
 struct vla_model;
 int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream);
 

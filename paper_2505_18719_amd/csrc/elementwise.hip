@@ -256,22 +256,29 @@ __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restr
 //               rotary pairs 32 rows apart: block b = rows [32b, 32b+32) then
 //               [half+32b, half+32b+32)
 //  kPackGateUp: [gate; up] interleaved in blocks of 32 rows, zero rows past src_rows
+// Source row of destination row r under a packing mode, or -1 for a zero
+// row; for kPackGateUp `part` receives 0 (gate) or 1 (up).
+__device__ __forceinline__ int pack_src_row(int mode, int r, int head_dim, int src_rows, int& part) {
+  part = 0;
+  if (mode == kPackRows) return r < src_rows ? r : -1;
+  if (mode == kPackQk) {
+    const int head = r / head_dim, p = r % head_dim, half = head_dim / 2;
+    const int blk = p / 64, c = p % 64;
+    return head * head_dim + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32);
+  }
+  part = (r % 64) < 32 ? 0 : 1;
+  const int j = 32 * (r / 64) + (r % 32);
+  return j < src_rows ? j : -1;
+}
+
 __global__ __launch_bounds__(256) void pack_frag_kernel(PackArgs a) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   const int kc = a.K / 8;
   if (i >= (size_t)a.rows * kc) return;
   const int r = (int)(i / kc), k = (int)(i % kc) * 8;
-  const bf16_t* src = nullptr;
-  if (a.mode == kPackRows) {
-    if (r < a.src_rows) src = a.src + (size_t)r * a.src_ld;
-  } else if (a.mode == kPackQk) {
-    const int hd = a.head_dim, head = r / hd, p = r % hd, half = hd / 2;
-    const int blk = p / 64, c = p % 64;
-    src = a.src + (size_t)(head * hd + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32)) * a.src_ld;
-  } else {
-    const int j = 32 * (r / 64) + (r % 32);
-    if (j < a.src_rows) src = ((r % 64) < 32 ? a.src : a.src2) + (size_t)j * a.src_ld;
-  }
+  int part;
+  const int j = pack_src_row(a.mode, r, a.head_dim, a.src_rows, part);
+  const bf16_t* src = j < 0 ? nullptr : (part ? a.src2 : a.src) + (size_t)j * a.src_ld;
   bf16_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = (src && k + e < a.src_cols) ? src[k + e] : (bf16_t)0;
@@ -363,6 +370,103 @@ hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* 
   if (n == 0) return hipSuccess;
   if (2 * F > p.tiles * 64 || F % 32 != 0 || ldh < F) return hipErrorInvalidValue;
   hipLaunchKernelGGL(reduce_swiglu_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, p, h, ldh, M, F);
+  return hipGetLastError();
+}
+
+// LoRA merge, one 256-thread workgroup per 64 destination rows x 64 K
+// columns.  The update B A of the tile is a 64 x 64 x rank product on MFMA:
+// wave w takes destination rows 16 w .. 16 w + 15, its A operand the 16 B rows
+// of their source rows (contiguous 16-byte reads), its B operand the adapter's
+// A factor staged transposed in LDS; the fp32 update is staged in LDS and each
+// thread then adds two 8-element chunks of it to the original weights, rounds
+// to bf16 and writes them in frag layout.
+__global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t at[64][72];  // A^T: [column][rank], padded rows
+  __shared__ float dw[64][68];                                // scale-free update B A of the tile
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int RK = (a.rank + 31) / 32 * 32;
+  // this thread's two 8-column chunks of the tile: the original weights are
+  // loaded first, so that their latency overlaps the update's computation
+  int crow[2], ccol[2], csrc[2];
+  bool cwrite[2];
+  uint4 w0v[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int e = tid + 256 * t;
+    crow[t] = r0 + e / 8;
+    ccol[t] = c0 + 8 * (e % 8);
+    int pt;
+    csrc[t] = crow[t] < a.rows ? pack_src_row(a.mode, crow[t], a.head_dim, a.src_rows, pt) : -1;
+    // rows past the matrix and the other projection's rows of [gate; up] are not written
+    cwrite[t] = crow[t] < a.rows && (a.mode != kPackGateUp || pt == a.part);
+    w0v[t] = make_uint4(0, 0, 0, 0);  // zero rows and columns of the packed layout
+    if (cwrite[t] && csrc[t] >= 0 && ccol[t] < a.src_cols)  // src_cols % 8 == 0: a chunk is wholly in or out
+      w0v[t] = *reinterpret_cast<const uint4*>(a.w0 + (size_t)csrc[t] * a.src_ld + ccol[t]);
+  }
+  // this lane's A-operand row (destination row r0 + 16 wave + lane % 16) of B, both rank halves
+  int part;
+  const int j = pack_src_row(a.mode, r0 + 16 * wave + (lane & 15), a.head_dim, a.src_rows, part);
+  uint4 bv[2];
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) {
+    const int k = 32 * kc + 8 * (lane >> 4);
+    bv[kc] = make_uint4(0, 0, 0, 0);
+    if (kc < RK / 32 && j >= 0 && r0 + 16 * wave + (lane & 15) < a.rows && k < a.rank)
+      bv[kc] = *reinterpret_cast<const uint4*>(a.b + (size_t)j * a.rank + k);
+  }
+  // A^T, zero past the rank and past the source columns: 8 columns of one rank row per 16-byte load
+  for (int e = tid; e < RK * 8; e += 256) {
+    const int kr = e / 8, c = 8 * (e % 8);
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (kr < a.rank && c0 + c < a.src_cols) v = *reinterpret_cast<const uint4*>(a.a + (size_t)kr * a.src_cols + c0 + c);
+    const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int x = 0; x < 8; ++x) at[c + x][kr] = (bf16_t)(vv[x >> 1] >> (16 * (x & 1)));
+  }
+  __syncthreads();
+  f32x4 acc[4];
+#pragma unroll
+  for (int jb = 0; jb < 4; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) {
+    if (kc < RK / 32) {
+      const int k = 32 * kc + 8 * (lane >> 4);
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const uint4 av = *reinterpret_cast<const uint4*>(&at[16 * jb + (lane & 15)][k]);
+        acc[jb] = mfma16(as_bf16x8(bv[kc]), as_bf16x8(av), acc[jb]);
+      }
+    }
+  }
+  // acc[jb][r]: update of row 16 wave + 4 (lane / 16) + r, column 16 jb + lane % 16
+#pragma unroll
+  for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dw[16 * wave + 4 * (lane >> 4) + r][16 * jb + (lane & 15)] = acc[jb][r];
+  __syncthreads();
+  // add the scaled update to the original weights, round to bf16, write in frag layout
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (!cwrite[t]) continue;
+    const int rr = crow[t] - r0, cc = ccol[t] - c0;
+    float w[8];
+    unpack8(w0v[t], w);
+    if (csrc[t] >= 0 && ccol[t] < a.src_cols) {
+#pragma unroll
+      for (int x = 0; x < 8; ++x) w[x] += a.scale * dw[rr][cc + x];
+    }
+    *reinterpret_cast<uint4*>(a.dst + frag_index(crow[t], ccol[t], a.K)) =
+        make_uint4(pack2bf(w[0], w[1]), pack2bf(w[2], w[3]), pack2bf(w[4], w[5]), pack2bf(w[6], w[7]));
+  }
+}
+
+hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  if (a.K % 64 != 0 || a.rank < 8 || a.rank > 64 || a.rank % 8 != 0 || a.src_ld % 8 != 0 || a.src_cols % 8 != 0 ||
+      (a.mode == kPackGateUp && (a.part < 0 || a.part > 1)))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lora_merge_kernel, dim3((a.rows + 63) / 64, a.K / 64), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

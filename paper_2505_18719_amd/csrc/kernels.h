@@ -205,6 +205,24 @@ struct PackArgs {
   int mode, head_dim;
 };
 hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s);
+// LoRA merge into a packed weight (frag layout, rows placed as launch_pack_frag
+// places them for `mode`): destination row r of source row j gets
+// bf16(w0[j, :] + scale * (b[j, :] a)) with a [rank, src_cols], b [src_rows, rank]
+// row-major bf16 and the rank sum accumulated in fp32.  For kPackGateUp only
+// the rows of `part` (0 gate, 1 up) are written.  Requires K % 64 == 0,
+// rank % 8 == 0, 8 <= rank <= 64, src_ld and src_cols multiples of 8.
+struct MergeArgs {
+  bf16_t* dst;
+  int rows, K;
+  const bf16_t* w0;
+  int src_ld, src_rows, src_cols;
+  int mode, head_dim, part;
+  const bf16_t* a;
+  const bf16_t* b;
+  int rank;
+  float scale;
+};
+hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

@@ -594,6 +594,48 @@ int vla_token_logprobs(vla_model* m, int32_t B, const void* vis, const int32_t* 
   return VLA_OK;
 }
 
+int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
+                   const void* lora_b, int32_t rank, float scale, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (!w0 || !lora_a || !lora_b) return fail(VLA_EINVAL, "NULL argument");
+  const Dims& D = m->D;
+  if (layer < 0 || layer >= D.L) return fail(VLA_EINVAL, "layer out of range");
+  if (projection < VLA_PROJ_Q || projection > VLA_PROJ_DOWN) return fail(VLA_EINVAL, "unknown projection");
+  if (!std::isfinite(scale)) return fail(VLA_EINVAL, "scale must be finite");
+  if (rank < 8 || rank > 64 || rank % 8 != 0) return fail(VLA_EUNSUPPORTED, "rank must be a multiple of 8 in [8, 64]");
+  const LayerW& w = m->lw[layer];
+  MergeArgs a{};
+  a.w0 = static_cast<const bf16_t*>(w0);
+  a.a = static_cast<const bf16_t*>(lora_a);
+  a.b = static_cast<const bf16_t*>(lora_b);
+  a.rank = rank;
+  a.scale = scale;
+  a.head_dim = D.hd;
+  a.part = 0;
+  const size_t qkv_part = frag_elems(D.d, D.d);  // [Wq; Wk; Wv] are consecutive d-row parts
+  switch (projection) {
+    case VLA_PROJ_Q: case VLA_PROJ_K: case VLA_PROJ_V:
+      a.dst = w.wqkv + (size_t)projection * qkv_part;
+      a.rows = D.d; a.K = D.d; a.src_ld = D.d; a.src_rows = D.d; a.src_cols = D.d;
+      a.mode = projection == VLA_PROJ_V ? kPackRows : kPackQk;
+      break;
+    case VLA_PROJ_O:
+      a.dst = w.wo; a.rows = D.d; a.K = D.d; a.src_ld = D.d; a.src_rows = D.d; a.src_cols = D.d; a.mode = kPackRows;
+      break;
+    case VLA_PROJ_GATE: case VLA_PROJ_UP:
+      a.dst = w.wgu; a.rows = 2 * D.Fp; a.K = D.d; a.src_ld = D.d; a.src_rows = D.F; a.src_cols = D.d;
+      a.mode = kPackGateUp; a.part = projection == VLA_PROJ_UP ? 1 : 0;
+      break;
+    default:  // VLA_PROJ_DOWN: K padded from d_ffn to Fp with zero columns
+      a.dst = w.wd; a.rows = D.d; a.K = D.Fp; a.src_ld = D.F; a.src_rows = D.d; a.src_cols = D.F; a.mode = kPackRows;
+      break;
+  }
+  if (a.src_cols % 8 != 0) return fail(VLA_EUNSUPPORTED, "input features must be a multiple of 8");
+  VLA_CK(launch_lora_merge(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
 int vla_read_device_flags(vla_model* m, void* stream, uint32_t* flags_host) {
   if (!m || !flags_host) return fail(VLA_EINVAL, "NULL argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -673,6 +715,10 @@ int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t
     case 2: src = m->kv[layer].k; avail = kv; break;
     case 3: src = m->kv[layer].v; avail = kv; break;
     case 4: src = m->u; avail = frag_elems(D.Mmax, D.d) * sizeof(bf16_t); break;
+    case 5: src = m->lw[layer].wqkv; avail = frag_elems(3 * D.d, D.d) * sizeof(bf16_t); break;
+    case 6: src = m->lw[layer].wo; avail = frag_elems(D.d, D.d) * sizeof(bf16_t); break;
+    case 7: src = m->lw[layer].wgu; avail = frag_elems(2 * D.Fp, D.d) * sizeof(bf16_t); break;
+    case 8: src = m->lw[layer].wd; avail = frag_elems(D.d, D.Fp) * sizeof(bf16_t); break;
     default: return fail(VLA_EINVAL, "unknown buffer");
   }
   if (bytes > avail) return fail(VLA_EINVAL, "read larger than the buffer");

@@ -23,7 +23,10 @@ FLAG_BAD_PROMPT_ID = 1
 FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
-           "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy", "vla_last_error")
+           "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
+           "vla_last_error")
+# projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
+PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
 DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
                  "vla_debug_set_layer_limit")
@@ -68,6 +71,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_prefill.argtypes = [vp, i32, vp, vp, vp, vp, vp]
     lib.vla_decode_actions.argtypes = [vp, i32, vp, f32, vp, vp, vp, vp, vp]
     lib.vla_token_logprobs.argtypes = [vp, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp]
+    lib.vla_lora_merge.argtypes = [vp, i32, i32, vp, vp, vp, i32, f32, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.vla_profile_begin.argtypes = [vp, ctypes.c_uint32]
     lib.vla_profile_end.argtypes = [vp, vp, vp, vp]
@@ -188,6 +192,16 @@ class VlaModel:
                                            _ptr(out["logp"]), _ptr(out["entropy"]), _ptr(out.get("logits")),
                                            _stream(self.device)))
         return out
+
+    def lora_merge(self, layer: int, projection: str, w0: torch.Tensor, lora_a: torch.Tensor,
+                   lora_b: torch.Tensor, scale: float) -> None:
+        """W = bf16(w0 + scale * lora_b @ lora_a) for one projection ('wq' ..
+        'wdown') of one layer; w0 is the original checkpoint weight."""
+        rank = int(lora_a.shape[0])
+        for t in (w0, lora_a, lora_b):
+            assert t.dtype == torch.bfloat16 and t.is_contiguous() and t.is_cuda
+        _check(self.lib.vla_lora_merge(self.handle, layer, PROJECTIONS.index(projection), _ptr(w0), _ptr(lora_a),
+                                       _ptr(lora_b), rank, float(scale), _stream(self.device)))
 
     def read_flags(self) -> int:
         v = ctypes.c_uint32()

@@ -1,0 +1,204 @@
+"""Parity of the LoRA merge (Sec. 3.3, Rollout Phase: the updated LoRA weights
+are merged with the original checkpoint before the rollout) with the CPU
+oracle: the packed weights the rollout reads, read back and unpacked on the
+host from their documented layout, and a rollout of the merged policy."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import LOGIT_TOL, LOGP_TOL, Setup, compare_rollout, log
+from paper_2505_18719_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+PROJ = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
+SCALE = 0.5   # alpha / rank of the adapter
+
+
+# ---------------------------------------------------------------- layouts
+def _fp(d_ffn):
+    return (d_ffn + 255) // 256 * 256
+
+
+def _frag_gather(buf, rows, K):
+    """Rows `rows` of a frag-layout bf16 matrix with K columns (vla_debug.h):
+    element (r, k) sits at ((((r//16) (K/32 + 1) + k//32) * 64) + r%16 + 16 ((k%32)//8)) * 8 + k%8."""
+    KB = K // 32 + 1
+    r = np.asarray(rows)[:, None]
+    k = np.arange(K)[None, :]
+    idx = ((((r >> 4) * KB + (k >> 5)) << 6) + (r & 15) + (((k & 31) >> 3) << 4)) * 8 + (k & 7)
+    raw = buf.view(torch.int16).cpu().numpy()[idx]
+    return torch.from_numpy(raw).view(torch.bfloat16).double().numpy()
+
+
+def _packed_source(cfg, which, r):
+    """(projection key, source row or -1 for a zero row) of packed row r."""
+    d, hd, F = cfg.d_model, cfg.head_dim, cfg.d_ffn
+    if which == 5:
+        part, rr = divmod(r, d)
+        if part == 2:
+            return "wv", rr
+        head, p = divmod(rr, hd)
+        blk, c = divmod(p, 64)
+        return ("wq", "wk")[part], head * hd + (32 * blk + c if c < 32 else hd // 2 + 32 * blk + c - 32)
+    if which == 6:
+        return "wo", r
+    if which == 7:
+        j = 32 * (r // 64) + r % 32
+        return ("wgate" if r % 64 < 32 else "wup"), (j if j < F else -1)
+    return "wdown", r
+
+
+def _packed_shape(cfg, which):
+    d, Fp = cfg.d_model, _fp(cfg.d_ffn)
+    return {5: (3 * d, d), 6: (d, d), 7: (2 * Fp, d), 8: (d, Fp)}[which]
+
+
+def _read_packed(model, cfg, which, layer):
+    R, K = _packed_shape(cfg, which)
+    n = (R + 15) // 16 * (K // 32 + 1) * 512
+    buf = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    model.debug_read(which, layer, buf)
+    torch.cuda.synchronize()
+    return buf
+
+
+def _check_packed(cfg, buf, which, rows, w0_layer, adapters, scale, label):
+    """Packed rows `rows` against the oracle merge of the source rows: exact,
+    except where the float64 value v lies within the fp32 accumulation error
+    e of the rank sum from a bf16 rounding boundary; there the result must be
+    a bf16 value in [bf16(v - e), bf16(v + e)] (where W0 and the update nearly
+    cancel, that interval spans several bf16 steps)."""
+    R, K = _packed_shape(cfg, which)
+    got = _frag_gather(buf, rows, K)
+    n_exact = n_edge = 0
+    for i, r in enumerate(rows):
+        key, j = _packed_source(cfg, which, int(r))
+        exp = np.zeros(K)
+        if j >= 0:
+            w0 = oracle.to_f64(w0_layer[key][j:j + 1])
+            ncol = w0.shape[1]
+            if adapters is not None and key in adapters:
+                a, b = oracle.to_f64(adapters[key][0]), oracle.to_f64(adapters[key][1][j:j + 1])
+                v = w0 + scale * (b @ a)
+                err = 2.0 ** -24 * (a.shape[0] + 4) * (np.abs(w0) + abs(scale) * (np.abs(b) @ np.abs(a)))
+                lo, hi = oracle.bf16_round(v - err), oracle.bf16_round(v + err)
+                m = oracle.lora_merge(w0_layer[key][j:j + 1], adapters[key][0], adapters[key][1][j:j + 1], scale)
+                g = got[i, :ncol]
+                ok = (g == m) | ((g >= lo) & (g <= hi))  # a rounding of some value within the fp32 error
+                if not ok.all():
+                    bad = np.where(~ok)[1][:3]
+                    detail = [(int(c), float(v[0, c]), float(m[0, c]), float(g[c]), float(lo[0, c]), float(hi[0, c]),
+                               float(err[0, c]), float(w0[0, c]), float((b @ a)[0, c])) for c in bad]
+                    raise AssertionError(f"{label} {key} row {j}: (col, exact, oracle, gpu, lo, hi, err, w0, BA) {detail}")
+                n_exact += int((g == m).sum())
+                n_edge += int((g != m).sum())
+                exp = None
+            else:
+                exp[:ncol] = w0[0]
+        if exp is not None:
+            assert np.array_equal(got[i], exp), (label, key, j)
+        elif got.shape[1] > w0.shape[1]:
+            assert not got[i, w0.shape[1]:].any(), (label, key, "padding columns")
+    log(f"[{label}] rows={len(rows)} merged elements exact={n_exact} rounding-boundary neighbours={n_edge}")
+    return n_exact, n_edge
+
+
+# ---------------------------------------------------------------- tests
+@pytest.fixture(scope="module")
+def tiny():
+    return Setup(inputs.TINY, seed=0)
+
+
+def _merge_all(S, adapters, scale, layers):
+    for li, ad in zip(layers, adapters):
+        for k in PROJ:
+            a, b = ad[k]
+            S.model.lora_merge(li, k, S.w["layers"][li][k], a, b, scale)
+
+
+@pytest.mark.parametrize("rank", [8, 32])
+def test_lora_merge_packed_weights_match_oracle(tiny, rank):
+    S, cfg = tiny, inputs.TINY
+    before0 = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}
+    ad = inputs.make_lora(cfg, rank, seed=rank, device="cuda", layers=[1])
+    _merge_all(S, ad, SCALE, [1])
+    adc = {k: (a.cpu(), b.cpu()) for k, (a, b) in ad[0].items()}
+    edge = 0
+    for which in (5, 6, 7, 8):
+        buf = _read_packed(S.model, cfg, which, 1)
+        R, _ = _packed_shape(cfg, which)
+        edge += _check_packed(cfg, buf, which, range(R), S.wc["layers"][1], adc, SCALE, f"tiny r{rank} w{which}")[1]
+        assert torch.equal(_read_packed(S.model, cfg, which, 0), before0[which]), "layer 0 must be untouched"
+    assert edge <= 8
+    # restore the checkpoint for the other tests of the module
+    _merge_all(S, [{k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}], SCALE, [1])
+
+
+def test_lora_merge_starts_from_the_original_and_a_zero_update_restores(tiny):
+    S, cfg = tiny, inputs.TINY
+    packed0 = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}
+    ad = inputs.make_lora(cfg, 16, seed=5, device="cuda", layers=[0])
+    _merge_all(S, ad, SCALE, [0])
+    once = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}
+    assert not torch.equal(once[5], packed0[5])
+    _merge_all(S, ad, SCALE, [0])  # merging again starts from the original: same bits
+    for w in once:
+        assert torch.equal(_read_packed(S.model, cfg, w, 0), once[w])
+    zero = [{k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}]
+    _merge_all(S, zero, SCALE, [0])
+    for w in packed0:
+        assert torch.equal(_read_packed(S.model, cfg, w, 0), packed0[w]), w
+
+
+def test_merged_policy_rollout_matches_oracle(tiny):
+    S, cfg = tiny, inputs.TINY
+    ad = inputs.make_lora(cfg, 32, seed=7, device="cuda")
+    _merge_all(S, ad, SCALE, range(cfg.n_layers))
+    try:
+        merged = oracle.as_weights(oracle.merge_weights(S.wc, [{k: (a.cpu(), b.cpu()) for k, (a, b) in d.items()}
+                                                             for d in ad], SCALE), cfg)
+        inp, dev = S.inputs(seed=9)
+        S.model.prefill(dev["vis"], dev["ids"], inp.prompt_lens)
+        out = S.model.decode_actions(dev["gumbel"], 1.5)
+        torch.cuda.synchronize()
+        st = compare_rollout(cfg, merged, inp, out, 1.5, label="tiny merged")
+        assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
+        # the merge changed the policy: the unmerged oracle is far from it
+        base = compare_rollout(cfg, S.W, inp, out, 1.5, label="tiny merged vs unmerged oracle")
+        assert base["dlogit"] > 10 * st["dlogit"]
+    finally:
+        _merge_all(S, [{k: (a, torch.zeros_like(b)) for k, (a, b) in d.items()} for d in ad], SCALE,
+                   range(cfg.n_layers))
+
+
+def test_lora_merge_errors(tiny):
+    from paper_2505_18719_amd.vla import VlaError
+    S = tiny
+    a, b = inputs.make_lora(inputs.TINY, 16, seed=1, device="cuda", layers=[0])[0]["wq"]
+    w0 = S.w["layers"][0]["wq"]
+    with pytest.raises(VlaError, match="VLA_EUNSUPPORTED"):
+        S.model.lora_merge(0, "wq", w0, a[:12].contiguous(), b[:, :12].contiguous(), SCALE)
+    with pytest.raises(VlaError, match="VLA_EINVAL"):
+        S.model.lora_merge(inputs.TINY.n_layers, "wq", w0, a, b, SCALE)
+    with pytest.raises(VlaError, match="VLA_EINVAL"):
+        S.model.lora_merge(0, "wq", w0, a, b, float("nan"))
+
+
+def test_lora_merge_7b_width_sampled_rows():
+    """One decoder layer at the OpenVLA-7B width (d 4096, FFN 11008, head_dim
+    128), rank 32: sampled rows of every packed projection, including the
+    first and last rows of each part and of each rotary block."""
+    cfg = inputs.L7B_B8.replace(name="7b_1layer", n_layers=1, batch=1)
+    S = Setup(cfg, seed=3, max_batch=1)
+    ad = inputs.make_lora(cfg, 32, seed=3, device="cuda")
+    _merge_all(S, ad, SCALE, [0])
+    adc = {k: (a.cpu(), b.cpu()) for k, (a, b) in ad[0].items()}
+    rng = np.random.default_rng(3)
+    for which in (5, 6, 7, 8):
+        R, _ = _packed_shape(cfg, which)
+        rows = sorted(set(rng.integers(0, R, 48).tolist()) | {0, 31, 32, 63, 64, R // 3, R // 3 - 1, R - 1})
+        buf = _read_packed(S.model, cfg, which, 0)
+        _check_packed(cfg, buf, which, rows, S.wc["layers"][0], adc, SCALE, f"7b w{which}")
+    S.model.close()

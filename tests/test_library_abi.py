@@ -72,3 +72,12 @@ def test_create_rejects_null_arguments_before_device_work(vla):
     assert lib.vla_prefill(None, 1, None, None, None, None, None) == -1
     assert lib.vla_decode_actions(None, 1, None, 1.0, None, None, None, None, None) == -1
     lib.vla_destroy(None)
+
+
+def test_lora_merge_validates_arguments_before_the_device(vla):
+    """Null handle, unknown projection, bad rank or scale are rejected by the
+    host code (no model or device memory is touched)."""
+    lib = vla.load_library()
+    p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    assert lib.vla_lora_merge(None, 0, 0, p, p, p, 8, 1.0, None) == -1
+    assert b"model is NULL" in lib.vla_last_error()
