@@ -8,4 +8,4 @@ from .vla_oracle import (MODES, Weights, action_logits, apply_rope, as_weights, 
                          prefill_logits,
                          prefix_embeddings, rms_norm, rollout, rollout_env, rope_angles,
                          sample_bin, silu, teacher_forced, teacher_forced_env, to_f64,
-                         token_stats)
+                         token_stats, values)

@@ -15,7 +15,11 @@ What it computes (VLA-RL, arXiv 2505.18719):
   * the teacher-forced recompute of those log-probabilities for stored
     actions, i.e. the numerator of the PPO ratio of Eq. 2;
   * the weights the rollout runs on: the original checkpoint with the updated
-    LoRA adapters merged in, rounded to bf16 (Sec. 3.3, Rollout Phase).
+    LoRA adapters merged in, rounded to bf16 (Sec. 3.3, Rollout Phase);
+  * the value estimate V(o_t, v_in) of Alg. 1 by a value model of the policy's
+    own architecture (the "homogeneous value model" of Fig. 2): the decoder
+    over the same prefix, then a linear value head on the final-normed hidden
+    state of the last prefix row.
 
 The decoder block is the standard Llama-2 one: pre-RMSNorm, rotary position
 embedding (half-split pairing), causal softmax attention, SwiGLU MLP and
@@ -353,6 +357,22 @@ def prefill_logits(cfg, w, vis, prompt_ids, prompt_lens, mode: str = "bf16",
     envs = list(range(len(prompts))) if envs is None else list(envs)
     rows = [forward_rows(cfg, W, prefix_embeddings(cfg, W, vis[b], prompts[b]), mode)[-1:] for b in envs]
     return action_logits(cfg, W, np.concatenate(rows), rnd)
+
+
+def values(cfg, w, vis, prompt_ids, prompt_lens, value_head, mode: str = "bf16",
+           envs: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Value estimates V(o_t, v_in) of Alg. 1 (one per selected environment)
+    by a value model with the decoder architecture of the policy and weights
+    ``w``: the final RMSNorm of the hidden state at the last prefix row (bf16
+    at the head's input in bf16 mode, as for the action head) dotted with the
+    value head [d]."""
+    W = as_weights(w, cfg)
+    rnd = _rounder(mode)
+    prompts = _split_prompts(prompt_ids, prompt_lens)
+    envs = list(range(len(prompts))) if envs is None else list(envs)
+    rows = [forward_rows(cfg, W, prefix_embeddings(cfg, W, vis[b], prompts[b]), mode)[-1:] for b in envs]
+    u = rnd(rms_norm(np.concatenate(rows), W.final_norm, cfg.rms_eps))
+    return u @ to_f64(value_head)
 
 
 # ----------------------------------------------------------------------------

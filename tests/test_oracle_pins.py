@@ -356,3 +356,48 @@ def test_merge_weights_touches_only_the_adapted_projections():
             same = torch.equal(m["layers"][li][k], t)
             assert same == (li != 1 or k.endswith("norm")), (li, k)
     assert torch.equal(m["embed"], w["embed"]) and torch.equal(m["lm_head"], w["lm_head"])
+
+
+# ---------------------------------------------------------------------------
+# Value model (Alg. 1: V_t <- V(o_t, v_in); a value model of the policy's own
+# architecture, Fig. 2)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode", ["ideal", "bf16"])
+def test_value_with_an_action_row_as_head_is_that_action_logit(pin_setup, mode):
+    """The value head and the action head read the same final-normed hidden
+    state of the last prefix row: with row k of the LM head's action rows as
+    the value head, the value is exactly the prefill's action logit k."""
+    w, inp = pin_setup
+    z = oracle.prefill_logits(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, mode=mode)
+    for k in (0, 3, PIN.action_bins - 1):
+        v = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens,
+                          w["lm_head"][PIN.action_begin + k], mode=mode)
+        np.testing.assert_allclose(v, z[:, k], rtol=0, atol=1e-13)
+
+
+def test_value_zero_blocks_reduce_to_a_dot_product():
+    """With W_o = W_down = 0 every layer is the identity: the value is the
+    head dotted with the RMS-normalised last prefix embedding."""
+    cfg = PIN.replace(batch=2)
+    w = make_weights(cfg, seed=19)
+    for lw in w["layers"]:
+        lw["wo"].zero_(); lw["wdown"].zero_()
+    inp = make_inputs(cfg, seed=19)
+    head = torch.linspace(-1, 1, cfg.d_model).to(torch.bfloat16)
+    v = oracle.values(cfg, w, inp.vis, inp.prompt_ids, inp.prompt_lens, head, mode="ideal")
+    for b in range(2):
+        x_last = inp.vis[b, -1].double().numpy() if inp.prompt_lens[b] == 0 else \
+            w["embed"][int(inp.env_prompt(b)[-1])].double().numpy()
+        u = x_last / np.sqrt(np.mean(x_last ** 2) + cfg.rms_eps)
+        assert v[b] == pytest.approx(float(head.double().numpy() @ u), rel=1e-12, abs=1e-12)
+
+
+def test_value_is_linear_in_the_head(pin_setup):
+    w, inp = pin_setup
+    g = torch.Generator().manual_seed(31)
+    h1 = (torch.randn(PIN.d_model, generator=g) * 0.02).to(torch.bfloat16)
+    h2 = (torch.randn(PIN.d_model, generator=g) * 0.02).to(torch.bfloat16)
+    v1 = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, h1, mode="ideal")
+    v2 = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, h2, mode="ideal")
+    v12 = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, h1.double() + h2.double(), mode="ideal")
+    np.testing.assert_allclose(v12, v1 + v2, rtol=1e-12, atol=1e-14)
