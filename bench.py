@@ -29,6 +29,28 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
+# Fields of the printed line and their types; `check_line` rejects a line that
+# lacks one or whose headline figures are not numbers.
+LINE_FIELDS = {"metric": str, "value": float, "unit": str, "n_gpus": int, "steps": int, "warmup": int,
+               "ms_per_step": float, "higher_is_better": bool, "scaling": str, "dtype": str, "data": str,
+               "config": dict, "roofline": dict}
+ROOFLINE_FIELDS = {"bound": str, "achieved": float, "peak": float, "unit": str, "frac": float}
+
+
+def check_line(result):
+    for key, t in LINE_FIELDS.items():
+        if not isinstance(result.get(key), t) or (t is not bool and isinstance(result.get(key), bool)):
+            raise ValueError(f"bench line field {key!r} must be {t.__name__}, got {result.get(key)!r:.80}")
+    for key, t in ROOFLINE_FIELDS.items():
+        if not isinstance(result["roofline"].get(key), t):
+            raise ValueError(f"roofline field {key!r} must be {t.__name__}")
+    if "cpu_baseline" in result and not isinstance(result["cpu_baseline"].get("value"), float):
+        raise ValueError("cpu_baseline value must be a number")
+    if "workload" not in result["config"]:
+        raise ValueError("config must name the workload")
+    return result
+
+
 # HBM traffic (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a plain streaming
 # kernel of known size) is kept in a profile summary together with hashes of
 # the kernel sources it was taken on; it is reported only while they match.
@@ -147,6 +169,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=8, help="decoder layers in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher-forced", action="store_true")
+    ap.add_argument("--no-value", action="store_true")
     ap.add_argument("--no-lora-merge", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain streaming kernel of known size before timing (HBM counter calibration)")
@@ -309,6 +332,29 @@ def main():
                                     "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                     "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
 
+    if not args.no_value:
+        # value estimate of every environment's prefix (Alg. 1), a value model of
+        # the policy's architecture: here the policy's trunk with a seeded head
+        inp, ids, _ = sets[0]
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        head = (torch.randn(d, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+        vals = model.value(inp.vis, ids, inp.prompt_lens, head)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(2):
+            model.value(inp.vis, ids, inp.prompt_lens, head, out=vals)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        v_ms = e0.elapsed_time(e1) / 2
+        Lp = inp.prefix_lens.astype(np.float64)
+        v_flops = 2 * layer_params * L * Lp.sum() + 2 * d * L * (Lp * (Lp + 1)).sum() + 2 * d * B
+        result["value_model"] = {"ms": v_ms, "rows": int(Lp.sum()),
+                                 "mfma_frac": v_flops / (v_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                 "values_per_s": B / (v_ms * 1e-3)}
+        log(f"[bench] value pass over {B} prefixes: {v_ms:.2f} ms")
+
     if not args.no_lora_merge:
         # LoRA merge before a rollout (Sec. 3.3): every projection of every layer,
         # rank 32, from the original checkpoint; timed after the rollout figures
@@ -343,7 +389,7 @@ def main():
         log(f"[bench] oracle CPU baseline ({args.cpu_layers} layers of one environment)")
         result["cpu_baseline"] = cpu_baseline(cfg, w, sets[0][0], args.cpu_layers, T)
     model.close()
-    print(json.dumps(result), flush=True)
+    print(json.dumps(check_line(result)), flush=True)
 
 
 if __name__ == "__main__":

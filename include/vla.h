@@ -142,6 +142,20 @@ int vla_decode_actions(vla_model* m, int32_t batch, const float* gumbel, float t
                        int32_t* tokens, float* logp, float* entropy, float* step_logits,
                        void* stream);
 
+/* Value estimates V_t = V(o_t, v_in) of Alg. 1 by a value model of the
+ * policy's own architecture (the "homogeneous value model" of Fig. 2): the
+ * decoder held by `m` (create the handle with the value model's weights) runs
+ * over [visual ; prompt] as in vla_prefill, then
+ *     values[b] = value_head . RMSNorm_final(h_b)     (fp32 accumulation)
+ * where h_b is the hidden state at the last prefix row L_b - 1 and the normed
+ * state is rounded to bf16 as at the action head's input.
+ *   vis_emb, prompt_ids, prompt_lens_host  as in vla_prefill
+ *   value_head  bf16 [d_model], read only
+ *   values      fp32 [batch] out
+ * Overwrites the handle's prefill state (a later decode needs a new prefill). */
+int vla_value(vla_model* m, int32_t batch, const void* vis_emb, const int32_t* prompt_ids,
+              const int32_t* prompt_lens_host, const void* value_head, float* values, void* stream);
+
 /* LoRA merge before a rollout (Sec. 3.3, Rollout Phase: the updated LoRA
  * weights are merged with the original checkpoint): replaces one projection
  * of one decoder layer in the handle's packed weights by

@@ -470,6 +470,31 @@ hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// One wave per row: 16-byte chunks of 8 consecutive K elements (contiguous in
+// frag layout), lane l taking chunks l, l + 64, ..., then a butterfly sum.
+__global__ __launch_bounds__(256) void value_head_kernel(const bf16_t* __restrict__ u, int R, int d,
+                                                         const bf16_t* __restrict__ head, float* __restrict__ values) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= R) return;
+  float acc = 0.f;
+  for (int c = lane; c < d / 8; c += 64) {
+    float uf[8], hf[8];
+    unpack8(*reinterpret_cast<const uint4*>(u + frag_index(r, 8 * c, d)), uf);
+    unpack8(*reinterpret_cast<const uint4*>(head + 8 * c), hf);
+#pragma unroll
+    for (int x = 0; x < 8; ++x) acc += uf[x] * hf[x];
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) values[r] = acc;
+}
+
+hipError_t launch_value_head(const bf16_t* u, int R, int d, const bf16_t* head, float* values, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (d % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(value_head_kernel, dim3((R + 3) / 4), dim3(256), 0, s, u, R, d, head, values);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   if (a.K % 32 != 0 || a.src_cols > a.K || !a.dst || !a.src || (a.mode == kPackGateUp && !a.src2))

@@ -136,9 +136,6 @@ hipError_t launch_reduce_sum(const float* part, const SkinnyPlan& p, float* z, i
 hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* h, int ldh, int M, int F,
                                 hipStream_t s);
 
-// Decode: sum QKV partials, RoPE at position env_prefix[b] + step - 1, store q
-// and append K/V of the new token to the page pool.
-
 // Attention
 struct PrefillAttnArgs {
   const bf16_t* q;  // [M, d]
@@ -223,6 +220,9 @@ struct MergeArgs {
   float scale;
 };
 hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s);
+// Value head: values[r] = sum_k u[r, k] * head[k] for R rows of u (bf16,
+// frag layout with K = d) and head bf16 [d]; fp32, fixed summation order.
+hipError_t launch_value_head(const bf16_t* u, int R, int d, const bf16_t* head, float* values, hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

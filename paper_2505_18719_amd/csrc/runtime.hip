@@ -443,9 +443,12 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
   const bf16_t* emb = static_cast<const bf16_t*>(w->embed);
   const bf16_t* lm = static_cast<const bf16_t*>(w->lm_head);
   CREATE_CK(hipMemcpyAsync(m->emb, emb, (size_t)D.V * D.d * 2, hipMemcpyDeviceToDevice, s));
-  // projection weights are stored in frag layout (see frag_index); the LM head keeps only the action rows
+  // projection weights are stored in frag layout (see frag_index); the LM head keeps only the action rows.
+  // The spare blocks are zeroed first, so that every byte of a packed weight is defined.
   auto pack = [&](bf16_t* dst, int rows, int K, const void* src, int src_ld, int src_rows, int src_cols, int mode,
                   const void* src2 = nullptr) {
+    const hipError_t e = launch_fill_zero(dst, frag_elems(rows, K) * sizeof(bf16_t), s);
+    if (e != hipSuccess) return e;
     PackArgs pa{dst, rows, K, static_cast<const bf16_t*>(src), static_cast<const bf16_t*>(src2), src_ld, src_rows,
                 src_cols, mode, D.hd};
     return launch_pack_frag(pa, s);
@@ -590,6 +593,26 @@ int vla_token_logprobs(vla_model* m, int32_t B, const void* vis, const int32_t* 
   sa.action_begin = m->cfg.action_begin; sa.logp = logp; sa.entropy = entropy; sa.logits_out = logits; sa.rows = R;
   sa.flags = m->flags;
   VLA_CK(launch_sampler(sa, s));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_value(vla_model* m, int32_t B, const void* vis, const int32_t* ids, const int32_t* lens_host,
+              const void* value_head, float* values, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (B < 0) return fail(VLA_EINVAL, "negative batch");
+  if (B > m->D.Bmax) return fail(VLA_ESHAPE, "batch > max_batch");
+  m->state_valid = false;  // the pass overwrites the prefill state
+  if (B == 0) return VLA_OK;
+  if (!lens_host || !value_head || !values || (m->D.nvis > 0 && !vis)) return fail(VLA_EINVAL, "NULL argument");
+  long long np = 0;
+  for (int b = 0; b < B; ++b) np += lens_host[b];
+  if (np > 0 && !ids) return fail(VLA_EINVAL, "prompt_ids is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int R = 0;
+  int rc = forward(m, B, vis, ids, lens_host, nullptr, s, &R);
+  if (rc) return rc;
+  VLA_CK(launch_value_head(m->u_head, R, m->D.d, static_cast<const bf16_t*>(value_head), values, s));
   g_err.clear();
   return VLA_OK;
 }

@@ -23,7 +23,7 @@ FLAG_BAD_PROMPT_ID = 1
 FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
-           "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
+           "vla_value", "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
            "vla_last_error")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
@@ -72,6 +72,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_decode_actions.argtypes = [vp, i32, vp, f32, vp, vp, vp, vp, vp]
     lib.vla_token_logprobs.argtypes = [vp, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp]
     lib.vla_lora_merge.argtypes = [vp, i32, i32, vp, vp, vp, i32, f32, vp]
+    lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.vla_profile_begin.argtypes = [vp, ctypes.c_uint32]
     lib.vla_profile_end.argtypes = [vp, vp, vp, vp]
@@ -191,6 +192,18 @@ class VlaModel:
                                            lens.ctypes.data_as(ctypes.c_void_p), _ptr(actions), float(temperature),
                                            _ptr(out["logp"]), _ptr(out["entropy"]), _ptr(out.get("logits")),
                                            _stream(self.device)))
+        return out
+
+    def value(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
+              value_head: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Value estimates [batch] of the decoder held by this handle with the given head."""
+        lens = np.ascontiguousarray(prompt_lens, dtype=np.int32)
+        B = int(lens.shape[0])
+        assert value_head.dtype == torch.bfloat16 and value_head.is_contiguous() and value_head.is_cuda
+        if out is None:
+            out = torch.empty(B, dtype=torch.float32, device=self.device)
+        _check(self.lib.vla_value(self.handle, B, _ptr(vis), _ptr(prompt_ids), lens.ctypes.data_as(ctypes.c_void_p),
+                                  _ptr(value_head), _ptr(out), _stream(self.device)))
         return out
 
     def lora_merge(self, layer: int, projection: str, w0: torch.Tensor, lora_a: torch.Tensor,

@@ -105,6 +105,28 @@ def _check_packed(cfg, buf, which, rows, w0_layer, adapters, scale, label):
     return n_exact, n_edge
 
 
+def _same_bits(x, y):
+    """Bitwise equality (torch.equal on bf16 compares values, and NaN != NaN)."""
+    return torch.equal(x.view(torch.int16), y.view(torch.int16))
+
+
+def _assert_same_packed(cfg, which, got, exp, msg):
+    """Bitwise equality of two packed buffers; on a mismatch, name the first
+    differing elements as (row, column) or as a spare block."""
+    if _same_bits(got, exp):
+        return
+    _, K = _packed_shape(cfg, which)
+    kb = K // 32 + 1
+    idx = torch.nonzero(got.view(torch.int16) != exp.view(torch.int16)).flatten().cpu().numpy()
+    where = []
+    for i in idx[:6]:
+        blk, lane_e = divmod(int(i), 512)
+        rb, kblk = divmod(blk, kb)
+        lane, e = divmod(lane_e, 8)
+        where.append("spare" if kblk == K // 32 else (16 * rb + lane % 16, 32 * kblk + 8 * (lane // 16) + e))
+    raise AssertionError(f"{msg}: {len(idx)} of {got.numel()} elements differ, first at {where}")
+
+
 # ---------------------------------------------------------------- tests
 @pytest.fixture(scope="module")
 def tiny():
@@ -116,6 +138,18 @@ def _merge_all(S, adapters, scale, layers):
         for k in PROJ:
             a, b = ad[k]
             S.model.lora_merge(li, k, S.w["layers"][li][k], a, b, scale)
+
+
+def test_packed_weights_spare_blocks_are_zero(tiny):
+    """Every byte of a packed weight is defined: the spare block that ends each
+    16-row block is zero after create (and a merge never writes it)."""
+    S, cfg = tiny, inputs.TINY
+    for which in (5, 6, 7, 8):
+        R, K = _packed_shape(cfg, which)
+        kb = K // 32 + 1
+        blocks = _read_packed(S.model, cfg, which, cfg.n_layers - 1).view(torch.int16).view(-1, kb, 512)
+        assert blocks.shape[0] == (R + 15) // 16
+        assert not blocks[:, kb - 1].any(), which
 
 
 @pytest.mark.parametrize("rank", [8, 32])
@@ -130,7 +164,7 @@ def test_lora_merge_packed_weights_match_oracle(tiny, rank):
         buf = _read_packed(S.model, cfg, which, 1)
         R, _ = _packed_shape(cfg, which)
         edge += _check_packed(cfg, buf, which, range(R), S.wc["layers"][1], adc, SCALE, f"tiny r{rank} w{which}")[1]
-        assert torch.equal(_read_packed(S.model, cfg, which, 0), before0[which]), "layer 0 must be untouched"
+        _assert_same_packed(cfg, which, _read_packed(S.model, cfg, which, 0), before0[which], "layer 0 must be untouched")
     assert edge <= 8
     # restore the checkpoint for the other tests of the module
     _merge_all(S, [{k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}], SCALE, [1])
@@ -142,14 +176,14 @@ def test_lora_merge_starts_from_the_original_and_a_zero_update_restores(tiny):
     ad = inputs.make_lora(cfg, 16, seed=5, device="cuda", layers=[0])
     _merge_all(S, ad, SCALE, [0])
     once = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}
-    assert not torch.equal(once[5], packed0[5])
+    assert not _same_bits(once[5], packed0[5])
     _merge_all(S, ad, SCALE, [0])  # merging again starts from the original: same bits
     for w in once:
-        assert torch.equal(_read_packed(S.model, cfg, w, 0), once[w])
+        _assert_same_packed(cfg, w, _read_packed(S.model, cfg, w, 0), once[w], "a second merge must give the same bits")
     zero = [{k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}]
     _merge_all(S, zero, SCALE, [0])
     for w in packed0:
-        assert torch.equal(_read_packed(S.model, cfg, w, 0), packed0[w]), w
+        _assert_same_packed(cfg, w, _read_packed(S.model, cfg, w, 0), packed0[w], "a zero update must restore the packing")
 
 
 def test_merged_policy_rollout_matches_oracle(tiny):
