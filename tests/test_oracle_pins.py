@@ -401,3 +401,143 @@ def test_value_is_linear_in_the_head(pin_setup):
     v2 = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, h2, mode="ideal")
     v12 = oracle.values(PIN, w, inp.vis, inp.prompt_ids, inp.prompt_lens, h1.double() + h2.double(), mode="ideal")
     np.testing.assert_allclose(v12, v1 + v2, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# learning phase: GAE (Alg. 1), PPO-clip (Eq. 2 with Eq. 1), log-prob gradient
+# ---------------------------------------------------------------------------
+from oracle import learn_oracle as lo  # noqa: E402
+
+
+def test_gae_worked_example_by_hand():
+    """M = 3, one environment, gamma = lambda = 1/2; d_2 = 1 ends the episode
+    between steps 1 and 2.  By hand: delta = (0.625, -0.25, 3),
+    A = (0.5625, -0.25, 3), returns A + V = (1.0625, 0, 4)."""
+    r = np.array([[1.0], [0.0], [2.0]])
+    v = np.array([[0.5], [0.25], [1.0], [4.0]])
+    d = np.array([[0], [0], [1], [0]], dtype=np.uint8)
+    adv, ret = lo.gae(r, v, d, 0.5, 0.5)
+    assert np.array_equal(adv[:, 0], [0.5625, -0.25, 3.0])
+    assert np.array_equal(ret[:, 0], [1.0625, 0.0, 4.0])
+
+
+def _gae_inputs(M, N, seed, p_done=0.1):
+    rng = np.random.default_rng(seed)
+    return (rng.normal(size=(M, N)), rng.normal(size=(M + 1, N)),
+            (rng.random((M + 1, N)) < p_done).astype(np.uint8))
+
+
+def test_gae_equals_the_explicit_discounted_sum_of_td_residuals():
+    """GAE's definition: A_t = sum_l (gamma lambda)^l delta_{t+l}, the sum cut
+    at the first episode end after t, by brute force over every (t, l)."""
+    M, N, g, lam = 23, 5, 0.97, 0.9
+    r, v, d = _gae_inputs(M, N, 1, p_done=0.15)
+    adv, _ = lo.gae(r, v, d, g, lam)
+    for n in range(N):
+        for t in range(M):
+            total, w = 0.0, 1.0
+            for s in range(t, M):
+                nonterminal = 1.0 - d[s + 1, n]
+                delta = r[s, n] + g * v[s + 1, n] * nonterminal - v[s, n]
+                total += w * delta
+                if nonterminal == 0.0:
+                    break
+                w *= g * lam
+            assert abs(adv[t, n] - total) <= 1e-12 * max(1.0, abs(total)), (t, n)
+
+
+def test_gae_lambda_one_is_the_bootstrapped_discounted_return():
+    """lambda = 1, no episode end: A_t + V_t = sum_{s >= t} gamma^(s-t) r_s + gamma^(M-t) V_M."""
+    M, N, g = 17, 3, 0.9
+    r, v, _ = _gae_inputs(M, N, 2)
+    d = np.zeros((M + 1, N), dtype=np.uint8)
+    _, ret = lo.gae(r, v, d, g, 1.0)
+    for t in range(M):
+        want = sum(g ** (s - t) * r[s] for s in range(t, M)) + g ** (M - t) * v[M]
+        assert np.allclose(ret[t], want, rtol=1e-12, atol=1e-12)
+
+
+def test_gae_special_cases():
+    M, N, g = 9, 4, 0.95
+    r, v, d = _gae_inputs(M, N, 3, p_done=0.3)
+    adv0, _ = lo.gae(r, v, d, g, 0.0)          # lambda = 0: one-step TD residual
+    cont = 1.0 - d[1:].astype(np.float64)
+    assert np.allclose(adv0, r + g * cont * v[1:] - v[:M], rtol=0, atol=1e-14)
+    advg, _ = lo.gae(r, v, d, 0.0, 0.7)        # gamma = 0: r_t - V_t
+    assert np.allclose(advg, r - v[:M], rtol=0, atol=1e-14)
+    ones = np.ones((M + 1, N), dtype=np.uint8)  # every step ends an episode
+    adv1, _ = lo.gae(r, v, ones, g, 0.9)
+    assert np.allclose(adv1, r - v[:M], rtol=0, atol=1e-14)
+
+
+def test_ppo_clip_hand_cases():
+    """eps = 0.2, one token per action (n = 4):
+    rho 1.5, A +1 -> clipped term 1.2, no gradient;
+    rho 0.9, A -2 -> -1.8, d loss / d logp = -rho A / n = 0.45;
+    rho 0.5, A -1 -> clipped term -0.8, no gradient;
+    rho 2.0, A -1 -> -2.0 (the unclipped term is the smaller), gradient 0.5.
+    J = (1.2 - 1.8 - 0.8 - 2.0) / 4 = -0.85."""
+    rho = np.array([1.5, 0.9, 0.5, 2.0])
+    a = np.array([1.0, -2.0, -1.0, -1.0])
+    loss, frac, g = lo.ppo_clip(np.log(rho)[:, None], np.zeros((4, 1)), a, 0.2)
+    assert abs(loss - 0.85) < 1e-12 and frac == 0.5
+    assert np.allclose(g[:, 0], [0.0, 0.45, 0.0, 0.5], rtol=0, atol=1e-12)
+
+
+def test_ppo_ratio_one_at_the_old_policy():
+    """theta = theta_old: rho = 1, nothing is clipped, J = mean A and the
+    gradient of every token is -A / n (Eq. 2's ratio is 1 at the old policy)."""
+    rng = np.random.default_rng(4)
+    lp = -rng.random((50, 7)) * 8
+    a = rng.normal(size=50)
+    loss, frac, g = lo.ppo_clip(lp, lp, a, 0.2)
+    assert abs(loss + a.mean()) < 1e-14 and frac == 0.0
+    assert np.allclose(g, np.repeat(-a[:, None] / 50, 7, axis=1), rtol=0, atol=1e-15)
+
+
+def test_ppo_gradient_matches_finite_differences():
+    rng = np.random.default_rng(5)
+    n, k, eps = 12, 7, 0.2
+    lo_ = -rng.random((n, k)) * 6
+    ln = lo_ + rng.normal(scale=0.15, size=(n, k))
+    a = rng.normal(size=n)
+    rho = np.exp(ln.sum(1) - lo_.sum(1))
+    assert np.all(np.minimum(abs(rho - 1.2), abs(rho - 0.8)) > 1e-3)  # away from the kinks
+    _, _, g = lo.ppo_clip(ln, lo_, a, eps)
+    h = 1e-6
+    for t in range(n):
+        for i in (0, k - 1):
+            up, dn = ln.copy(), ln.copy()
+            up[t, i] += h
+            dn[t, i] -= h
+            fd = (lo.ppo_clip(up, lo_, a, eps)[0] - lo.ppo_clip(dn, lo_, a, eps)[0]) / (2 * h)
+            assert abs(fd - g[t, i]) < 1e-8, (t, i)
+    assert 0 < (g == 0).all(axis=1).sum() < n  # both branches were exercised
+
+
+def test_logprob_grad_matches_finite_differences_of_the_token_logprob():
+    """Against finite differences of the rollout oracle's own log-prob
+    (token_stats), which shares no code with logprob_grad."""
+    rng = np.random.default_rng(6)
+    bins, T, begin = 256, 1.5, 1000
+    z = rng.normal(scale=1.5, size=(3, bins))
+    tok = begin + np.array([0, 77, 255])
+    dl = np.array([0.7, -1.3, 2.0])
+    dz = lo.logprob_grad(z, tok, begin, T, dl)
+    h = 1e-6
+    for r in range(3):
+        for j in (0, 5, int(tok[r] - begin), 255):
+            up, dn = z[r].copy(), z[r].copy()
+            up[j] += h
+            dn[j] -= h
+            fd = (vo.token_stats(up, int(tok[r] - begin), T)[0] - vo.token_stats(dn, int(tok[r] - begin), T)[0]) / (2 * h)
+            assert abs(dl[r] * fd - dz[r, j]) < 1e-8, (r, j)
+    assert np.allclose(dz.sum(axis=1), 0.0, atol=1e-14)  # softmax rows sum to one
+
+
+def test_logprob_grad_uniform_logits_closed_form():
+    bins, T = 256, 1.5
+    dz = lo.logprob_grad(np.full((1, bins), 0.3), [42], 0, T, [2.0])
+    want = np.full(bins, -2.0 / (T * bins))
+    want[42] += 2.0 / T
+    assert np.allclose(dz[0], want, rtol=0, atol=1e-15)
