@@ -170,6 +170,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher-forced", action="store_true")
     ap.add_argument("--no-value", action="store_true")
+    ap.add_argument("--no-learning", action="store_true")
     ap.add_argument("--no-lora-merge", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain streaming kernel of known size before timing (HBM counter calibration)")
@@ -354,6 +355,42 @@ def main():
                                  "mfma_frac": v_flops / (v_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                  "values_per_s": B / (v_ms * 1e-3)}
         log(f"[bench] value pass over {B} prefixes: {v_ms:.2f} ms")
+
+    if not args.no_learning:
+        # learning-phase kernels (Alg. 1 after the rollout, Eq. 2): GAE over a
+        # 512-step window of the 64 environments, PPO-clip and the logits
+        # gradient over a minibatch of 128 stored actions (7 tokens, 256 bins)
+        from paper_2505_18719_amd import vla as V
+        Ng, Mg, nb = B, 512, 128
+        r, vv, dd = (torch.from_numpy(x).to(dev) for x in I.rollout_window(Ng, Mg, seed=0))
+        old, new, adv = (torch.from_numpy(x).to(dev) for x in I.ppo_minibatch(nb, cfg.n_actions, seed=0))
+        zb = torch.randn(nb * cfg.n_actions, cfg.action_bins, device=dev)
+        tb = torch.randint(cfg.action_begin, cfg.action_begin + cfg.action_bins, (nb * cfg.n_actions,),
+                           device=dev, dtype=torch.int32)
+        adv_o, ret_o = V.gae(r, vv, dd, 0.99, 0.95)
+        st, gl = V.ppo_clip(new, old, adv, 0.2)
+        dzb = V.logprob_backward(zb, tb, cfg.action_begin, T, gl.reshape(-1))
+        reps = 50
+        times = {}
+        for name, fn in (("gae", lambda: V.gae(r, vv, dd, 0.99, 0.95, adv_o, ret_o)),
+                         ("ppo_clip", lambda: V.ppo_clip(new, old, adv, 0.2, gl, st)),
+                         ("logprob_backward", lambda: V.logprob_backward(zb, tb, cfg.action_begin, T,
+                                                                         gl.reshape(-1), dzb))):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times[name] = e0.elapsed_time(e1) / reps * 1e3
+        gae_bytes = 4 * Mg * Ng + 4 * (Mg + 1) * Ng + (Mg + 1) * Ng + 8 * Mg * Ng
+        result["learning"] = {"gae_us": times["gae"], "gae_envs": Ng, "gae_steps": Mg,
+                              "gae_gbs": gae_bytes / (times["gae"] * 1e-6) / 1e9,
+                              "ppo_clip_us": times["ppo_clip"], "ppo_actions": nb,
+                              "logprob_backward_us": times["logprob_backward"],
+                              "logprob_backward_rows": nb * cfg.n_actions}
+        log(f"[bench] learning kernels (us): " + ", ".join(f"{k} {v:.1f}" for k, v in times.items()))
 
     if not args.no_lora_merge:
         # LoRA merge before a rollout (Sec. 3.3): every projection of every layer,

@@ -223,6 +223,44 @@ hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s);
 // Value head: values[r] = sum_k u[r, k] * head[k] for R rows of u (bf16,
 // frag layout with K = d) and head bf16 [d]; fp32, fixed summation order.
 hipError_t launch_value_head(const bf16_t* u, int R, int d, const bf16_t* head, float* values, hipStream_t s);
+// Learning phase.  GAE over a window of n_steps steps of n_env environments,
+// time-major: rewards [M, N], values [M + 1, N] (row M the bootstrap value),
+// dones [M + 1, N] (row t = d_t; transition t continues iff d_{t+1} == 0);
+// advantages and returns (may be null) [M, N].
+struct GaeArgs {
+  const float* rewards;
+  const float* values;
+  const uint8_t* dones;
+  int n_env, n_steps;
+  float gamma, lam;
+  float* advantages;
+  float* returns;
+};
+hipError_t launch_gae(const GaeArgs& a, hipStream_t s);
+// PPO-clip over n actions of n_tokens tokens: stats[0] = -mean surrogate,
+// stats[1] = clipped fraction, dlogp [n, n_tokens] = d stats[0] / d logp_new.
+struct PpoArgs {
+  const float* logp_new;
+  const float* logp_old;
+  const float* advantages;
+  int n, n_tokens;
+  float eps;
+  float* stats;
+  float* dlogp;
+};
+hipError_t launch_ppo_clip(const PpoArgs& a, hipStream_t s);
+// dlogits[r, j] = dlogp[r] (1[j = k_r] - softmax(z_r / T)_j) / T, k_r = tokens[r] - action_begin
+// (a token outside [0, bins) gives a NaN row); bins <= 256.
+struct LogprobBwdArgs {
+  const float* logits;
+  const int32_t* tokens;
+  const float* dlogp;
+  int rows, bins, action_begin;
+  float temperature;
+  float* dlogits;
+};
+hipError_t launch_logprob_backward(const LogprobBwdArgs& a, hipStream_t s);
+
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

@@ -15,6 +15,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "vla.h"
+#include "vla_learn.h"
 
 using namespace vla;
 
@@ -655,6 +656,52 @@ int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* 
   }
   if (a.src_cols % 8 != 0) return fail(VLA_EUNSUPPORTED, "input features must be a multiple of 8");
   VLA_CK(launch_lora_merge(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_gae(int32_t n_env, int32_t n_steps, const float* rewards, const float* values, const uint8_t* dones,
+            float gamma, float lam, float* advantages, float* returns, void* stream) {
+  if (n_env < 0 || n_steps < 0) return fail(VLA_EINVAL, "negative size");
+  if (!(gamma >= 0.f && gamma <= 1.f) || !(lam >= 0.f && lam <= 1.f))
+    return fail(VLA_EINVAL, "gamma and lambda must lie in [0, 1]");
+  if ((size_t)(n_steps + 1) * (size_t)n_env >= (size_t)1 << 31) return fail(VLA_EUNSUPPORTED, "window too large");
+  if (n_env == 0 || n_steps == 0) {
+    g_err.clear();
+    return VLA_OK;
+  }
+  if (!rewards || !values || !dones || !advantages) return fail(VLA_EINVAL, "NULL argument");
+  GaeArgs a{rewards, values, dones, n_env, n_steps, gamma, lam, advantages, returns};
+  VLA_CK(launch_gae(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_ppo_clip(int32_t n, int32_t n_tokens, const float* logp_new, const float* logp_old,
+                 const float* advantages, float eps, float* stats, float* dlogp, void* stream) {
+  if (n < 1 || n_tokens < 1 || n_tokens > 16) return fail(VLA_EINVAL, "need n >= 1 and 1 <= n_tokens <= 16");
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(VLA_EINVAL, "eps must be finite and >= 0");
+  if (!logp_new || !logp_old || !advantages || !stats || !dlogp) return fail(VLA_EINVAL, "NULL argument");
+  if ((size_t)n * n_tokens >= (size_t)1 << 31) return fail(VLA_EUNSUPPORTED, "too many tokens");
+  PpoArgs a{logp_new, logp_old, advantages, n, n_tokens, eps, stats, dlogp};
+  VLA_CK(launch_ppo_clip(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_logprob_backward(int32_t rows, int32_t bins, int32_t action_begin, const float* logits,
+                         const int32_t* tokens, float temperature, const float* dlogp, float* dlogits,
+                         void* stream) {
+  if (rows < 0) return fail(VLA_EINVAL, "negative size");
+  if (bins < 1 || bins > 256) return fail(VLA_EUNSUPPORTED, "bins must be in [1, 256]");
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(VLA_EINVAL, "temperature must be > 0");
+  if (rows == 0) {
+    g_err.clear();
+    return VLA_OK;
+  }
+  if (!logits || !tokens || !dlogp || !dlogits) return fail(VLA_EINVAL, "NULL argument");
+  LogprobBwdArgs a{logits, tokens, dlogp, rows, bins, action_begin, temperature, dlogits};
+  VLA_CK(launch_logprob_backward(a, static_cast<hipStream_t>(stream)));
   g_err.clear();
   return VLA_OK;
 }

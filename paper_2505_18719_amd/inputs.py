@@ -26,7 +26,7 @@ import numpy as np
 import torch
 
 # Stream ids of SeedSequence([seed, stream, ...]).
-_S_WEIGHT, _S_VIS, _S_PROMPT_LEN, _S_PROMPT_ID, _S_GUMBEL, _S_ACTIONS, _S_GAIN, _S_LORA = range(8)
+_S_WEIGHT, _S_VIS, _S_PROMPT_LEN, _S_PROMPT_ID, _S_GUMBEL, _S_ACTIONS, _S_GAIN, _S_LORA, _S_LEARN = range(9)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -216,3 +216,27 @@ def stored_actions(cfg: VlaConfig, batch: int, seed: int = 0, step: int = 0) -> 
     rng = np.random.default_rng([seed, _S_ACTIONS, step])
     bins = rng.integers(0, cfg.action_bins, size=(batch, cfg.n_actions))
     return (bins + cfg.action_begin).astype(np.int32)
+
+
+def rollout_window(n_env: int, n_steps: int, seed: int = 0, p_done: float = 0.01):
+    """A synthetic window of Alg. 1's rollout buffer, time-major: rewards
+    [M, N] fp32 (a sparse success reward of 1 with probability p_done plus a
+    dense N(0, 0.1) process reward), values [M + 1, N] fp32 ~ U(0, 1) and
+    episode-start flags dones [M + 1, N] uint8 with P(1) = p_done."""
+    rng = np.random.default_rng([seed, _S_LEARN, n_env, n_steps])
+    dones = (rng.random((n_steps + 1, n_env)) < p_done).astype(np.uint8)
+    rewards = (rng.random((n_steps, n_env)) < p_done) + rng.normal(scale=0.1, size=(n_steps, n_env))
+    values = rng.random((n_steps + 1, n_env))
+    return rewards.astype(np.float32), values.astype(np.float32), dones
+
+
+def ppo_minibatch(n: int, n_tokens: int = 7, seed: int = 0, spread: float = 0.1):
+    """Token log-probabilities of n stored actions under the old policy
+    (negative, -Exp(mean 4), about the range of a 256-bin token at T = 1.5),
+    the same under an updated policy shifted by N(0, spread) per token, and
+    N(0, 1) advantages; all fp32 numpy."""
+    rng = np.random.default_rng([seed, _S_LEARN + 1, n, n_tokens])
+    old = -rng.exponential(scale=4.0, size=(n, n_tokens))
+    new = old + rng.normal(scale=spread, size=old.shape)
+    adv = rng.normal(size=n)
+    return old.astype(np.float32), new.astype(np.float32), adv.astype(np.float32)

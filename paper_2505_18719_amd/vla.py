@@ -24,7 +24,7 @@ FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
            "vla_value", "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
-           "vla_last_error")
+           "vla_last_error", "vla_gae", "vla_ppo_clip", "vla_logprob_backward")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
@@ -74,6 +74,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_lora_merge.argtypes = [vp, i32, i32, vp, vp, vp, i32, f32, vp]
     lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.vla_gae.argtypes = [i32, i32, vp, vp, vp, f32, f32, vp, vp, vp]
+    lib.vla_ppo_clip.argtypes = [i32, i32, vp, vp, vp, f32, vp, vp, vp]
+    lib.vla_logprob_backward.argtypes = [i32, i32, i32, vp, vp, f32, vp, vp, vp]
     lib.vla_profile_begin.argtypes = [vp, ctypes.c_uint32]
     lib.vla_profile_end.argtypes = [vp, vp, vp, vp]
     lib.vla_destroy.argtypes = [vp]
@@ -302,3 +305,65 @@ def debug_sample(z: torch.Tensor, gumbel: torch.Tensor, step: int, temperature: 
     _check(lib.vla_debug_sample(_ptr(z), B, A, na, step, action_begin, _ptr(gumbel), float(temperature),
                                 _ptr(tokens), _ptr(nxt), _ptr(logp), _ptr(ent), _ptr(logits), _stream(dev)))
     return {"tokens": tokens, "next": nxt, "logp": logp, "entropy": ent, "logits": logits}
+
+
+# ---------------------------------------------------------------- learning phase (vla_learn.h)
+def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
+    if t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} device tensor")
+    return t
+
+
+def gae(rewards: torch.Tensor, values: torch.Tensor, dones: torch.Tensor, gamma: float, lam: float,
+        advantages: Optional[torch.Tensor] = None, returns: Optional[torch.Tensor] = None):
+    """Advantages and returns [M, N] of Alg. 1's GAE step; rewards [M, N],
+    values [M + 1, N] fp32, dones [M + 1, N] uint8 (vla_gae)."""
+    lib = load_library()
+    M, N = rewards.shape
+    _dev(rewards, torch.float32, "rewards")
+    _dev(values, torch.float32, "values")
+    _dev(dones, torch.uint8, "dones")
+    if tuple(values.shape) != (M + 1, N) or tuple(dones.shape) != (M + 1, N):
+        raise ValueError("values and dones must be [M + 1, N]")
+    if advantages is None:
+        advantages = torch.empty(M, N, dtype=torch.float32, device=rewards.device)
+    if returns is None:
+        returns = torch.empty(M, N, dtype=torch.float32, device=rewards.device)
+    _check(lib.vla_gae(N, M, _ptr(rewards), _ptr(values), _ptr(dones), float(gamma), float(lam), _ptr(advantages),
+                       _ptr(returns), _stream(rewards.device)))
+    return advantages, returns
+
+
+def ppo_clip(logp_new: torch.Tensor, logp_old: torch.Tensor, advantages: torch.Tensor, eps: float,
+             dlogp: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
+    """(stats [loss, clipped fraction], dloss/dlogp_new [n, n_tokens]) of Eq. 2 (vla_ppo_clip)."""
+    lib = load_library()
+    n, k = logp_new.shape
+    for t, name in ((logp_new, "logp_new"), (logp_old, "logp_old"), (advantages, "advantages")):
+        _dev(t, torch.float32, name)
+    if tuple(logp_old.shape) != (n, k) or tuple(advantages.shape) != (n,):
+        raise ValueError("logp_old must be [n, n_tokens] and advantages [n]")
+    if dlogp is None:
+        dlogp = torch.empty(n, k, dtype=torch.float32, device=logp_new.device)
+    if stats is None:
+        stats = torch.empty(2, dtype=torch.float32, device=logp_new.device)
+    _check(lib.vla_ppo_clip(n, k, _ptr(logp_new), _ptr(logp_old), _ptr(advantages), float(eps), _ptr(stats),
+                            _ptr(dlogp), _stream(logp_new.device)))
+    return stats, dlogp
+
+
+def logprob_backward(logits: torch.Tensor, tokens: torch.Tensor, action_begin: int, temperature: float,
+                     dlogp: torch.Tensor, dlogits: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """dlogits [rows, bins] of the token log-probabilities (vla_logprob_backward)."""
+    lib = load_library()
+    rows, bins = logits.shape
+    _dev(logits, torch.float32, "logits")
+    _dev(tokens, torch.int32, "tokens")
+    _dev(dlogp, torch.float32, "dlogp")
+    if tokens.numel() != rows or dlogp.numel() != rows:
+        raise ValueError("tokens and dlogp need one entry per row")
+    if dlogits is None:
+        dlogits = torch.empty(rows, bins, dtype=torch.float32, device=logits.device)
+    _check(lib.vla_logprob_backward(rows, bins, int(action_begin), _ptr(logits), _ptr(tokens), float(temperature),
+                                    _ptr(dlogp), _ptr(dlogits), _stream(logits.device)))
+    return dlogits

@@ -81,3 +81,26 @@ def test_lora_merge_validates_arguments_before_the_device(vla):
     p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
     assert lib.vla_lora_merge(None, 0, 0, p, p, p, 8, 1.0, None) == -1
     assert b"model is NULL" in lib.vla_last_error()
+
+
+def test_learning_entry_points_validate_on_the_host(vla):
+    """vla_learn.h: bad sizes, parameters and null buffers are rejected, and
+    empty windows are no-ops, all before any device work."""
+    lib = vla.load_library()
+    p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    assert lib.vla_gae(4, 8, p, p, p, 1.5, 0.9, p, p, None) == -1
+    assert b"gamma" in lib.vla_last_error()
+    assert lib.vla_gae(4, 8, p, p, p, 0.99, float("nan"), p, p, None) == -1
+    assert lib.vla_gae(-1, 8, p, p, p, 0.99, 0.9, p, p, None) == -1
+    assert lib.vla_gae(0, 8, None, None, None, 0.99, 0.9, None, None, None) == 0
+    assert lib.vla_gae(4, 0, None, None, None, 0.99, 0.9, None, None, None) == 0
+    assert lib.vla_gae(4, 8, p, None, p, 0.99, 0.9, p, None, None) == -1
+    assert lib.vla_ppo_clip(0, 7, p, p, p, 0.2, p, p, None) == -1
+    assert lib.vla_ppo_clip(4, 17, p, p, p, 0.2, p, p, None) == -1
+    assert lib.vla_ppo_clip(4, 7, p, p, p, -0.1, p, p, None) == -1
+    assert lib.vla_ppo_clip(4, 7, p, p, p, float("inf"), p, p, None) == -1
+    assert lib.vla_ppo_clip(4, 7, p, p, None, 0.2, p, p, None) == -1
+    assert lib.vla_logprob_backward(4, 257, 0, p, p, 1.0, p, p, None) == -7
+    assert lib.vla_logprob_backward(4, 256, 0, p, p, 0.0, p, p, None) == -1
+    assert lib.vla_logprob_backward(0, 256, 0, None, None, 1.5, None, None, None) == 0
+    assert lib.vla_logprob_backward(4, 256, 0, p, None, 1.5, p, p, None) == -1
