@@ -7,7 +7,7 @@ gradient).
 """
 from . import learn_oracle  # noqa: F401
 from .vla_oracle import (MODES, Weights, action_logits, apply_rope, as_weights, bf16_round,  # noqa: F401
-                         causal_attention, decoder_layer, forward_rows, lora_merge, merge_weights,
+                         causal_attention, decoder_layer, extract_actions, forward_rows, lora_merge, merge_weights,
                          prefill_logits,
                          prefix_embeddings, rms_norm, rollout, rollout_env, rope_angles,
                          sample_bin, silu, teacher_forced, teacher_forced_env, to_f64,

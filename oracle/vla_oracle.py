@@ -16,6 +16,8 @@ What it computes (VLA-RL, arXiv 2505.18719):
     actions, i.e. the numerator of the PPO ratio of Eq. 2;
   * the weights the rollout runs on: the original checkpoint with the updated
     LoRA adapters merged in, rounded to bf16 (Sec. 3.3, Rollout Phase);
+  * the post-processing f of Alg. 1 / Sec. 3.3 that turns the action tokens
+    into a continuous robot action (each token a bin of one action dimension);
   * the value estimate V(o_t, v_in) of Alg. 1 by a value model of the policy's
     own architecture (the "homogeneous value model" of Fig. 2): the decoder
     over the same prefix, then a linear value head on the final-normed hidden
@@ -400,3 +402,17 @@ def merge_weights(w: Dict[str, object], adapters: List[Dict[str, tuple]], scale:
             m = lora_merge(w["layers"][li][k], a, b, scale)
             out["layers"][li][k] = torch.from_numpy(m).to(torch.bfloat16)
     return out
+
+
+def extract_actions(tokens, action_begin: int, bins: int, lo, hi) -> np.ndarray:
+    """Continuous actions a = f(v_out) of Alg. 1: token i of an environment's
+    action sequence is a bin of action dimension i (Sec. 3.3), bin
+    k = token - action_begin of `bins` uniform bins over [lo_i, hi_i] (the
+    per-dimension range the policy's actions were discretised over), and the
+    action value is that bin's centre lo_i + (k + 1/2) (hi_i - lo_i) / bins.
+    tokens [n, n_dims]; lo, hi [n_dims]; tokens outside the bins give NaN."""
+    k = np.asarray(tokens, dtype=np.int64) - action_begin
+    lo = np.asarray(lo, dtype=np.float64)
+    hi = np.asarray(hi, dtype=np.float64)
+    a = lo + (k + 0.5) * (hi - lo) / bins
+    return np.where((k >= 0) & (k < bins), a, np.nan)

@@ -541,3 +541,32 @@ def test_logprob_grad_uniform_logits_closed_form():
     want = np.full(bins, -2.0 / (T * bins))
     want[42] += 2.0 / T
     assert np.allclose(dz[0], want, rtol=0, atol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# action extraction f (Alg. 1): action tokens -> continuous action
+# ---------------------------------------------------------------------------
+def test_extract_actions_hand_values():
+    """4 bins over [-1, 1] have centres -0.75, -0.25, 0.25, 0.75; over [0, 2]
+    the centres shift by 1; a token outside the bins gives NaN."""
+    a = oracle.extract_actions([[10, 13, 11], [12, 9, 14]], 10, 4, [-1, 0, -1], [1, 2, 1])
+    assert np.array_equal(a[0], [-0.75, 1.75, -0.25])
+    assert a[1, 0] == 0.25 and np.isnan(a[1, 1]) and np.isnan(a[1, 2])
+
+
+def test_extract_actions_inverts_an_independent_discretiser():
+    """Discretise random continuous actions into 256 uniform bins per
+    dimension (floor of the scaled offset); the extracted action is the
+    centre of the bin the value fell in, so within half a bin width of it."""
+    rng = np.random.default_rng(7)
+    lo = rng.uniform(-2, 0, size=7)
+    hi = lo + rng.uniform(0.1, 3, size=7)
+    x = lo + rng.random((500, 7)) * (hi - lo)
+    w = (hi - lo) / 256
+    k = np.minimum(np.floor((x - lo) / w), 255).astype(np.int64)
+    a = oracle.extract_actions(k + 31808, 31808, 256, lo, hi)
+    assert np.all(np.abs(a - x) <= w / 2 + 1e-12)
+    assert np.all((a > lo + k * w) & (a < lo + (k + 1) * w))
+    centres = oracle.extract_actions(np.arange(256)[:, None] + np.zeros((1, 7), int), 0, 256, lo, hi)
+    assert np.all(np.diff(centres, axis=0) > 0)
+    assert np.allclose(centres.mean(axis=0), (lo + hi) / 2, rtol=0, atol=1e-12)
