@@ -384,6 +384,21 @@ def main():
             e1.record(stream)
             torch.cuda.synchronize()
             times[name] = e0.elapsed_time(e1) / reps * 1e3
+        # action extraction f of Alg. 1 on the batch's 7 tokens per environment
+        tok_e = torch.randint(cfg.action_begin, cfg.action_begin + cfg.action_bins, (B, cfg.n_actions),
+                              device=dev, dtype=torch.int32)
+        lo_e = torch.full((cfg.n_actions,), -1.0, device=dev)
+        hi_e = torch.full((cfg.n_actions,), 1.0, device=dev)
+        act_e = V.extract_actions(tok_e, cfg.action_begin, cfg.action_bins, lo_e, hi_e)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            V.extract_actions(tok_e, cfg.action_begin, cfg.action_bins, lo_e, hi_e, act_e)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        result["action_extraction"] = {"us": e0.elapsed_time(e1) / reps * 1e3, "environments": B,
+                                       "dims": cfg.n_actions}
         gae_bytes = 4 * Mg * Ng + 4 * (Mg + 1) * Ng + (Mg + 1) * Ng + 8 * Mg * Ng
         result["learning"] = {"gae_us": times["gae"], "gae_envs": Ng, "gae_steps": Mg,
                               "gae_gbs": gae_bytes / (times["gae"] * 1e-6) / 1e9,

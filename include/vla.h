@@ -142,6 +142,24 @@ int vla_decode_actions(vla_model* m, int32_t batch, const float* gumbel, float t
                        int32_t* tokens, float* logp, float* entropy, float* step_logits,
                        void* stream);
 
+/* Action extraction a_t = f(v_out) of Alg. 1 (Sec. 3.3: each action token
+ * is a discrete bin of one dimension of the robot action space).  Token i of
+ * an environment's sequence is dimension i; its bin k = token - action_begin
+ * of `bins` uniform bins over [range_lo[i], range_hi[i]] maps to the bin
+ * centre
+ *     actions[r, i] = range_lo[i] + (k + 1/2) (range_hi[i] - range_lo[i]) / bins
+ * (fp32).  The ranges are those the policy's actions were discretised over
+ * (for OpenVLA the 1st and 99th percentiles of each dimension of the
+ * training actions); the caller supplies them.  Needs no model handle.
+ *   n                 environments (rows); n_dims  action dimensions per row
+ *   tokens            int32 [n, n_dims] vocabulary ids (e.g. from vla_decode_actions)
+ *   bins              1 <= bins <= 256
+ *   range_lo, range_hi fp32 [n_dims]
+ *   actions           fp32 [n, n_dims] out; NaN where a token is outside the bins
+ * n == 0 is a no-op. */
+int vla_extract_actions(int32_t n, int32_t n_dims, const int32_t* tokens, int32_t action_begin, int32_t bins,
+                        const float* range_lo, const float* range_hi, float* actions, void* stream);
+
 /* Value estimates V_t = V(o_t, v_in) of Alg. 1 by a value model of the
  * policy's own architecture (the "homogeneous value model" of Fig. 2): the
  * decoder held by `m` (create the handle with the value model's weights) runs

@@ -290,6 +290,19 @@ __global__ __launch_bounds__(256) void pack_frag_kernel(PackArgs a) {
   *reinterpret_cast<uint4*>(a.dst + frag_index(r, k, a.K)) = o;
 }
 
+// a[r, i] = lo_i + (k + 1/2) (hi_i - lo_i) / bins for bin k = tokens[r, i] - action_begin,
+// NaN outside the bins; one thread per element.
+__global__ void extract_actions_kernel(const int32_t* __restrict__ tokens, int n_elems, int n_dims, int action_begin,
+                                       int bins, const float* __restrict__ lo, const float* __restrict__ hi,
+                                       float* __restrict__ out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_elems) return;
+  const int dim = i % n_dims;
+  const int k = tokens[i] - action_begin;
+  const float l = lo[dim];
+  out[i] = (k >= 0 && k < bins) ? l + ((float)k + 0.5f) * (hi[dim] - l) / (float)bins : __builtin_nanf("");
+}
+
 __global__ void bf16_to_f32_kernel(float* dst, const bf16_t* src, int n) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i < n) dst[i] = bf2f(src[i]);
@@ -506,6 +519,15 @@ hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s) {
 
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s) {
   hipLaunchKernelGGL(bf16_to_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_extract_actions(const int32_t* tokens, int n, int n_dims, int action_begin, int bins,
+                                  const float* lo, const float* hi, float* actions, hipStream_t s) {
+  const int n_elems = n * n_dims;
+  if (n_elems <= 0) return hipSuccess;
+  hipLaunchKernelGGL(extract_actions_kernel, dim3((n_elems + 255) / 256), dim3(256), 0, s, tokens, n_elems, n_dims,
+                     action_begin, bins, lo, hi, actions);
   return hipGetLastError();
 }
 

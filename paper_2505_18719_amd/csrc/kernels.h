@@ -261,6 +261,10 @@ struct LogprobBwdArgs {
 };
 hipError_t launch_logprob_backward(const LogprobBwdArgs& a, hipStream_t s);
 
+// Action extraction: actions[r, i] = lo[i] + (k + 1/2) (hi[i] - lo[i]) / bins, k = tokens[r, i] - action_begin
+// (NaN outside the bins); tokens and actions [n, n_dims].
+hipError_t launch_extract_actions(const int32_t* tokens, int n, int n_dims, int action_begin, int bins,
+                                  const float* lo, const float* hi, float* actions, hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

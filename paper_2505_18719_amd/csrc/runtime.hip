@@ -660,6 +660,22 @@ int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* 
   return VLA_OK;
 }
 
+int vla_extract_actions(int32_t n, int32_t n_dims, const int32_t* tokens, int32_t action_begin, int32_t bins,
+                        const float* range_lo, const float* range_hi, float* actions, void* stream) {
+  if (n < 0 || n_dims < 1) return fail(VLA_EINVAL, "need n >= 0 and n_dims >= 1");
+  if (bins < 1 || bins > 256) return fail(VLA_EUNSUPPORTED, "bins must be in [1, 256]");
+  if ((size_t)n * n_dims >= (size_t)1 << 31) return fail(VLA_EUNSUPPORTED, "too many actions");
+  if (n == 0) {
+    g_err.clear();
+    return VLA_OK;
+  }
+  if (!tokens || !range_lo || !range_hi || !actions) return fail(VLA_EINVAL, "NULL argument");
+  VLA_CK(launch_extract_actions(tokens, n, n_dims, action_begin, bins, range_lo, range_hi, actions,
+                                static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
 int vla_gae(int32_t n_env, int32_t n_steps, const float* rewards, const float* values, const uint8_t* dones,
             float gamma, float lam, float* advantages, float* returns, void* stream) {
   if (n_env < 0 || n_steps < 0) return fail(VLA_EINVAL, "negative size");

@@ -24,7 +24,7 @@ FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
            "vla_value", "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
-           "vla_last_error", "vla_gae", "vla_ppo_clip", "vla_logprob_backward")
+           "vla_last_error", "vla_extract_actions", "vla_gae", "vla_ppo_clip", "vla_logprob_backward")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
@@ -74,6 +74,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_lora_merge.argtypes = [vp, i32, i32, vp, vp, vp, i32, f32, vp]
     lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.vla_extract_actions.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, vp]
     lib.vla_gae.argtypes = [i32, i32, vp, vp, vp, f32, f32, vp, vp, vp]
     lib.vla_ppo_clip.argtypes = [i32, i32, vp, vp, vp, f32, vp, vp, vp]
     lib.vla_logprob_backward.argtypes = [i32, i32, i32, vp, vp, f32, vp, vp, vp]
@@ -305,6 +306,23 @@ def debug_sample(z: torch.Tensor, gumbel: torch.Tensor, step: int, temperature: 
     _check(lib.vla_debug_sample(_ptr(z), B, A, na, step, action_begin, _ptr(gumbel), float(temperature),
                                 _ptr(tokens), _ptr(nxt), _ptr(logp), _ptr(ent), _ptr(logits), _stream(dev)))
     return {"tokens": tokens, "next": nxt, "logp": logp, "entropy": ent, "logits": logits}
+
+
+def extract_actions(tokens: torch.Tensor, action_begin: int, bins: int, range_lo: torch.Tensor,
+                    range_hi: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Continuous actions [n, n_dims] from action tokens (vla_extract_actions)."""
+    lib = load_library()
+    n, k = tokens.shape
+    if tokens.dtype != torch.int32 or not tokens.is_cuda or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 device tensor")
+    for t in (range_lo, range_hi):
+        if t.dtype != torch.float32 or not t.is_cuda or t.numel() != k:
+            raise ValueError("ranges must be fp32 device tensors of n_dims entries")
+    if out is None:
+        out = torch.empty(n, k, dtype=torch.float32, device=tokens.device)
+    _check(lib.vla_extract_actions(n, k, _ptr(tokens), int(action_begin), int(bins), _ptr(range_lo),
+                                   _ptr(range_hi), _ptr(out), _stream(tokens.device)))
+    return out
 
 
 # ---------------------------------------------------------------- learning phase (vla_learn.h)

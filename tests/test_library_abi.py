@@ -104,3 +104,12 @@ def test_learning_entry_points_validate_on_the_host(vla):
     assert lib.vla_logprob_backward(4, 256, 0, p, p, 0.0, p, p, None) == -1
     assert lib.vla_logprob_backward(0, 256, 0, None, None, 1.5, None, None, None) == 0
     assert lib.vla_logprob_backward(4, 256, 0, p, None, 1.5, p, p, None) == -1
+
+
+def test_extract_actions_validates_on_the_host(vla):
+    lib = vla.load_library()
+    p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    assert lib.vla_extract_actions(4, 0, p, 0, 256, p, p, p, None) == -1
+    assert lib.vla_extract_actions(4, 7, p, 0, 300, p, p, p, None) == -7
+    assert lib.vla_extract_actions(4, 7, p, 0, 256, None, p, p, None) == -1
+    assert lib.vla_extract_actions(0, 7, None, 0, 256, None, None, None, None) == 0
