@@ -137,7 +137,10 @@ int vla_prefill(vla_model* m, int32_t batch, const void* vis_emb, const int32_t*
  *   logp         fp32 [batch, n_actions] out: log softmax(z_i / T)[k_i]
  *   entropy      fp32 [batch, n_actions] out, or NULL: entropy of softmax(z_i / T)
  *   step_logits  fp32 [batch, n_actions, action_bins] out, or NULL: z_i
- * The decode consumes the prefill state: a second call needs a new prefill. */
+ * The decode consumes the prefill state: a second call needs a new prefill.
+ * Batches above 128 environments run the decoder layers once per chunk of
+ * at most 128 environments (each chunk streams the weights again); results
+ * do not depend on the chunking. */
 int vla_decode_actions(vla_model* m, int32_t batch, const float* gumbel, float temperature,
                        int32_t* tokens, float* logp, float* entropy, float* step_logits,
                        void* stream);

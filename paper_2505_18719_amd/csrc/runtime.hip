@@ -536,26 +536,36 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
     if (i > 0) {
       VLA_CK(launch_embed_token_norm(m->next_tok, m->emb, m->x, m->u, m->lw[0].attn_norm, eps, B, D.d, D.V, m->flags,
                                      s));
-      // KV bytes read by one layer's decode attention at this step (K and V rows of every key)
-      double kv_bytes = 0.0;
-      for (int b = 0; b < B; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + i);
-      for (int l = 0; l < D.L; ++l) {
-        const LayerW& w = m->lw[l];
-        SkinnyArgs sq{m->u, B, w.wqkv, 3 * D.d, D.d, m->part};
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, B), launch_skinny(sq, m->plan_qkv, s));
-        DecodeAttnArgs da{m->part, m->plan_qkv, m->rope, m->u, m->kv[l], m->page_table, D.max_pages, m->env_prefix,
-                          i, B, D.d, D.H, D.hd, m->scale};
-        PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
-        SkinnyArgs so{m->u, B, w.wo, D.d, D.d, m->part};
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, B), launch_skinny(so, m->plan_o, s));
-        VLA_CK(launch_reduce_residual_norm(m->part, m->plan_o, m->x, m->u, w.mlp_norm, eps, B, D.d, s));
-        SkinnyArgs sg{m->u, B, w.wgu, 2 * D.Fp, D.d, m->part};
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, B), launch_skinny(sg, m->plan_gu, s));
-        VLA_CK(launch_reduce_swiglu(m->part, m->plan_gu, m->h, D.Fp, B, D.Fp, s));
-        SkinnyArgs sd{m->h, B, w.wd, D.d, D.Fp, m->part};
-        PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, B), launch_skinny(sd, m->plan_d, s));
-        const float* gnext = (l + 1 < D.L) ? m->lw[l + 1].attn_norm : m->final_norm;
-        VLA_CK(launch_reduce_residual_norm(m->part, m->plan_d, m->x, m->u, gnext, eps, B, D.d, s));
+      // The decode GEMMs take at most kSkinnyRows rows: larger batches run the
+      // layer stack once per chunk of environments (each chunk streams the weights).
+      for (int r0 = 0; r0 < B; r0 += kSkinnyRows) {
+        const int rows = std::min(kSkinnyRows, B - r0);
+        float* x = m->x + (size_t)r0 * D.d;
+        bf16_t* u = m->u + frag_index(r0, 0, D.d);  // r0 is a multiple of 16: whole frag blocks
+        bf16_t* h = m->h + frag_index(r0, 0, D.Fp);
+        const int32_t* ptab = m->page_table + (size_t)r0 * D.max_pages;
+        const int32_t* eprefix = m->env_prefix + r0;
+        // KV bytes read by one layer's decode attention at this step (K and V rows of every key)
+        double kv_bytes = 0.0;
+        for (int b = r0; b < r0 + rows; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + i);
+        for (int l = 0; l < D.L; ++l) {
+          const LayerW& w = m->lw[l];
+          SkinnyArgs sq{u, rows, w.wqkv, 3 * D.d, D.d, m->part};
+          PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, rows), launch_skinny(sq, m->plan_qkv, s));
+          DecodeAttnArgs da{m->part, m->plan_qkv, m->rope, u, m->kv[l], ptab, D.max_pages, eprefix,
+                            i, rows, D.d, D.H, D.hd, m->scale};
+          PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
+          SkinnyArgs so{u, rows, w.wo, D.d, D.d, m->part};
+          PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.d, rows), launch_skinny(so, m->plan_o, s));
+          VLA_CK(launch_reduce_residual_norm(m->part, m->plan_o, x, u, w.mlp_norm, eps, rows, D.d, s));
+          SkinnyArgs sg{u, rows, w.wgu, 2 * D.Fp, D.d, m->part};
+          PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(2.0 * D.F, D.d, rows), launch_skinny(sg, m->plan_gu, s));
+          VLA_CK(launch_reduce_swiglu(m->part, m->plan_gu, h, D.Fp, rows, D.Fp, s));
+          SkinnyArgs sd{h, rows, w.wd, D.d, D.Fp, m->part};
+          PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(D.d, D.F, rows), launch_skinny(sd, m->plan_d, s));
+          const float* gnext = (l + 1 < D.L) ? m->lw[l + 1].attn_norm : m->final_norm;
+          VLA_CK(launch_reduce_residual_norm(m->part, m->plan_d, x, u, gnext, eps, rows, D.d, s));
+        }
       }
       int rc = head_logits(m, m->u, B, m->logits_dec, s);
       if (rc) return rc;
