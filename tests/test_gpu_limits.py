@@ -58,3 +58,17 @@ def test_environment_in_the_second_chunk_alone_is_bit_identical(lim):
         torch.cuda.synchronize()
         for k in full:
             assert torch.equal(one[k][0], full[k][b]), (b, k)
+
+
+def test_max_batch_512_rollout_matches_oracle():
+    """The largest batch a handle accepts (512: four decode chunks), sequences up to 320 rows."""
+    cfg = LIMITS.replace(name="tiny_limits_b512", batch=512)
+    S = Setup(cfg, seed=22)
+    inp, dev = S.inputs(seed=22)
+    S.model.prefill(dev["vis"], dev["ids"], inp.prompt_lens)
+    out = S.model.decode_actions(dev["gumbel"], 1.5)
+    torch.cuda.synchronize()
+    envs = [0, 255, 384, 511, int(np.argmax(inp.prompt_lens))]
+    st = compare_rollout(cfg, S.W, inp, out, 1.5, envs=envs, label="b512")
+    S.model.close()
+    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
