@@ -383,8 +383,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(DecodeAttnArgs a) {
 __global__ __launch_bounds__(256) void sampler_kernel(SamplerArgs a) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int nrows = a.gumbel ? a.rows : a.rows;
-  if (row >= nrows) return;
+  if (row >= a.rows) return;
   const float* z = a.z + (size_t)row * a.A;
   float zv[4], zt[4];
   float m = -INFINITY;

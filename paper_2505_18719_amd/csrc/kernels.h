@@ -174,7 +174,6 @@ hipError_t launch_attn_decode(const DecodeAttnArgs& a, hipStream_t s);
 struct SamplerArgs {
   const float* z;          // [rows, A] logits
   int A;
-  float inv_t;             // unused; the kernel divides by temperature
   float temperature;
   // sampling mode (gumbel != null): row b, step i
   const float* gumbel;     // [B, n_actions, A]
