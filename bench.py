@@ -37,6 +37,19 @@ LINE_FIELDS = {"metric": str, "value": float, "unit": str, "n_gpus": int, "steps
 ROOFLINE_FIELDS = {"bound": str, "achieved": float, "peak": float, "unit": str, "frac": float}
 
 
+def pass_flops(d, F, L, Lb, n_out):
+    """Algorithmic flops of one forward pass over sequences of Lb rows: every
+    layer's QKV projection and every layer but the last over all rows; the last
+    layer's attention, O projection and MLP over the n_out rows per sequence
+    whose output is read (the last prefix row, or the scoring rows)."""
+    Lb = np.asarray(Lb, dtype=np.float64)
+    rows = Lb.sum()
+    last = np.concatenate([np.arange(lb - n_out, lb) for lb in Lb.astype(np.int64)]).astype(np.float64)
+    gemm = 2 * 3 * d * d * L * rows + 2 * (d * d + 3 * d * F) * ((L - 1) * rows + n_out * len(Lb))
+    attn = 2 * d * (L - 1) * (Lb * (Lb + 1)).sum() + 4 * d * (last + 1).sum()
+    return gemm + attn
+
+
 def check_line(result):
     for key, t in LINE_FIELDS.items():
         if not isinstance(result.get(key), t) or (t is not bool and isinstance(result.get(key), bool)):
@@ -258,8 +271,7 @@ def main():
     for k in range(args.steps):
         inp = sets[(args.warmup + k) % n_sets][0]
         Lb = inp.prefix_lens.astype(np.float64)
-        prefill_flops += 2 * layer_params * L * Lb.sum() + 2 * d * L * (Lb * (Lb + 1)).sum() \
-            + 2 * d * cfg.action_bins * B
+        prefill_flops += pass_flops(d, F, L, Lb, 1) + 2 * d * cfg.action_bins * B
         for t in range(1, cfg.n_actions):
             decode_bytes += 2 * layer_params * L + 2 * cfg.action_bins * d \
                 + 4 * d * L * (Lb + t).sum() + 2 * d * B  # weights + head rows + KV + embeddings
@@ -328,7 +340,7 @@ def main():
         torch.cuda.synchronize()
         tf_ms = e0.elapsed_time(e1) / 2
         Lb = inp.prefix_lens.astype(np.float64) + cfg.n_actions
-        tf_flops = 2 * layer_params * L * Lb.sum() + 2 * d * L * (Lb * (Lb + 1)).sum()
+        tf_flops = pass_flops(d, F, L, Lb, cfg.n_actions) + 2 * d * cfg.action_bins * B * cfg.n_actions
         result["teacher_forced"] = {"ms": tf_ms, "rows": int(Lb.sum()),
                                     "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                     "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
@@ -350,7 +362,7 @@ def main():
         torch.cuda.synchronize()
         v_ms = e0.elapsed_time(e1) / 2
         Lp = inp.prefix_lens.astype(np.float64)
-        v_flops = 2 * layer_params * L * Lp.sum() + 2 * d * L * (Lp * (Lp + 1)).sum() + 2 * d * B
+        v_flops = pass_flops(d, F, L, Lp, 1) + 2 * d * B
         result["value_model"] = {"ms": v_ms, "rows": int(Lp.sum()),
                                  "mfma_frac": v_flops / (v_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                  "values_per_s": B / (v_ms * 1e-3)}

@@ -55,7 +55,10 @@ int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst,
 
 /* Make later prefill / teacher-forced passes run only the first `n_layers`
  * decoder layers (0 restores all), so that the residual after any layer can
- * be read with vla_debug_read for layer-by-layer parity. */
+ * be read with vla_debug_read for layer-by-layer parity.  With a limit set
+ * (even n_layers), every row of every layer run is computed; without one,
+ * the last layer computes its attention output, O projection and MLP only
+ * for the rows read afterwards (the same bits for those rows). */
 int vla_debug_set_layer_limit(struct vla_model* m, int32_t n_layers);
 
 #ifdef __cplusplus

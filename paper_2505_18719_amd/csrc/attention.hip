@@ -241,11 +241,13 @@ __global__ __launch_bounds__(512, 1) void attn_prefill_kernel(PrefillAttnArgs a)
     default: WAIT_VMCNT(10); break;
   }
   __syncthreads();
-  attn_tiles<HD>(a, klds, vlds, 0, q1, L, row0, head, wave, lane);
+  // query tiles below the first needed row are skipped (their keys are still loaded: later rows see them)
+  const int qlo = a.env_q0 ? min(max(a.env_q0[env], 0), L - 1) / 16 : 0;
+  if (qlo < q1) attn_tiles<HD>(a, klds, vlds, qlo, q1, L, row0, head, wave, lane);
   if (q1 < nq) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    attn_tiles<HD>(a, klds, vlds, q1, nq, L, row0, head, wave, lane);
+    attn_tiles<HD>(a, klds, vlds, max(qlo, q1), nq, L, row0, head, wave, lane);
   }
 }
 

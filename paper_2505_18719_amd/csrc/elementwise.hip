@@ -303,6 +303,21 @@ __global__ void extract_actions_kernel(const int32_t* __restrict__ tokens, int n
   out[i] = (k >= 0 && k < bins) ? l + ((float)k + 0.5f) * (hi[dim] - l) / (float)bins : __builtin_nanf("");
 }
 
+// Row i of the compact buffers takes row rows[i]: the fp32 residual row and the
+// bf16 frag-layout row (8 elements = 16 bytes per thread step).
+__global__ void gather_rows_kernel(const float* __restrict__ x, const bf16_t* __restrict__ o,
+                                   const int32_t* __restrict__ rows, int d, float* __restrict__ xc,
+                                   bf16_t* __restrict__ oc) {
+  const int i = blockIdx.x, r = rows[i];
+  for (int k = 8 * threadIdx.x; k < d; k += 8 * 256) {
+    const float4* xs = reinterpret_cast<const float4*>(x + (size_t)r * d + k);
+    float4* xd = reinterpret_cast<float4*>(xc + (size_t)i * d + k);
+    xd[0] = xs[0];
+    xd[1] = xs[1];
+    *reinterpret_cast<uint4*>(oc + frag_index(i, k, d)) = *reinterpret_cast<const uint4*>(o + frag_index(r, k, d));
+  }
+}
+
 __global__ void bf16_to_f32_kernel(float* dst, const bf16_t* src, int n) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i < n) dst[i] = bf2f(src[i]);
@@ -528,6 +543,14 @@ hipError_t launch_extract_actions(const int32_t* tokens, int n, int n_dims, int 
   if (n_elems <= 0) return hipSuccess;
   hipLaunchKernelGGL(extract_actions_kernel, dim3((n_elems + 255) / 256), dim3(256), 0, s, tokens, n_elems, n_dims,
                      action_begin, bins, lo, hi, actions);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const float* x, const bf16_t* o, const int32_t* rows, int R, int d, float* xc,
+                              bf16_t* oc, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (d % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(R), dim3(256), 0, s, x, o, rows, d, xc, oc);
   return hipGetLastError();
 }
 

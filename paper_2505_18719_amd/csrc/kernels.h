@@ -147,6 +147,8 @@ struct PrefillAttnArgs {
   const int32_t* env_len;     // [B] rows of env b in this pass (<= 320)
   int n_env, d, n_heads, head_dim;
   float scale;
+  const int32_t* env_q0;      // [B] first query row of env b whose output is needed, or null for all;
+                              // the 16-row query tiles below its tile are skipped
 };
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
 
@@ -264,6 +266,10 @@ hipError_t launch_logprob_backward(const LogprobBwdArgs& a, hipStream_t s);
 // (NaN outside the bins); tokens and actions [n, n_dims].
 hipError_t launch_extract_actions(const int32_t* tokens, int n, int n_dims, int action_begin, int bins,
                                   const float* lo, const float* hi, float* actions, hipStream_t s);
+// Gather R rows: xc[i] = x[rows[i]] (fp32, d columns) and row i of oc = row rows[i] of o
+// (both bf16 frag layout with K = d; d % 8 == 0).
+hipError_t launch_gather_rows(const float* x, const bf16_t* o, const int32_t* rows, int R, int d, float* xc,
+                              bf16_t* oc, hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

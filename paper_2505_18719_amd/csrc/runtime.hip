@@ -87,7 +87,7 @@ int check_config(const vla_config* c, Dims* o) {
   D.n_pages = D.max_pages * D.Bmax;
   D.Mmax = (size_t)D.Bmax * D.Smax;
   D.Nmax = std::max(std::max(3 * D.d, 2 * D.Fp), D.Ap);
-  D.meta_ints = 2 * D.Mmax + 4 * (size_t)D.Bmax + (size_t)D.Bmax * D.max_pages +
+  D.meta_ints = 2 * D.Mmax + 5 * (size_t)D.Bmax + (size_t)D.Bmax * D.max_pages +
                 (size_t)D.Bmax * D.nact;
   return VLA_OK;
 }
@@ -130,6 +130,10 @@ struct vla_model {
   float* logits_dec;  // [Bmax, A]
   float* logits_tf;   // [Bmax * nact, A]
   bf16_t* u_head;     // [Bmax * nact, d]
+  // the last layer's rows that are read afterwards (at most Bmax * nact), compacted
+  float* xc;          // residual [Bmax * nact, d]
+  bf16_t* uc;         // attention output / norm output, frag layout
+  bf16_t* hc;         // SwiGLU output, frag layout (K = Fp)
   int32_t* next_tok;  // [Bmax]
   uint32_t* flags;
   int32_t* meta_dev;
@@ -137,7 +141,7 @@ struct vla_model {
   hipEvent_t meta_event;
   bool meta_pending;
   // device views into meta_dev
-  int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *page_table, *head_rows;
+  int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *env_q0, *page_table, *head_rows;
   // decode state
   int state_batch;
   bool state_valid;
@@ -191,6 +195,9 @@ void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
   M.logits_dec = L.take<float>((size_t)D.Bmax * D.A);
   M.logits_tf = L.take<float>((size_t)D.Bmax * D.nact * D.A);
   M.u_head = L.take<bf16_t>(frag_elems((size_t)D.Bmax * D.nact, D.d));
+  M.xc = L.take<float>((size_t)D.Bmax * D.nact * D.d);
+  M.uc = L.take<bf16_t>(frag_elems((size_t)D.Bmax * D.nact, D.d));
+  M.hc = L.take<bf16_t>(frag_elems((size_t)D.Bmax * D.nact, D.Fp));
   M.next_tok = L.take<int32_t>(D.Bmax);
   M.flags = L.take<uint32_t>(4);
   M.meta_dev = L.take<int32_t>(D.meta_ints);
@@ -210,6 +217,7 @@ void set_meta_views(vla_model* m, int32_t* base) {
   m->env_len = p; p += D.Bmax;
   m->env_prefix = p; p += D.Bmax;
   m->env_prompt_off = p; p += D.Bmax;
+  m->env_q0 = p; p += D.Bmax;
   m->page_table = p; p += (size_t)D.Bmax * D.max_pages;
   m->head_rows = p;
 }
@@ -292,6 +300,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   int32_t* hl = h + meta_index(m, m->env_len);
   int32_t* hpre = h + meta_index(m, m->env_prefix);
   int32_t* hpo = h + meta_index(m, m->env_prompt_off);
+  int32_t* hq0 = h + meta_index(m, m->env_q0);
   int32_t* hpt = h + meta_index(m, m->page_table);
   int32_t* hh = h + meta_index(m, m->head_rows);
   size_t r = 0;
@@ -300,6 +309,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     hr0[b] = (int32_t)r;
     hl[b] = rows[b];
     hpre[b] = prefix[b];
+    hq0[b] = prefix[b] - 1;  // the rows read after the last layer start at the last prefix row
     hpo[b] = po;
     po += lens_host[b];
     for (int t = 0; t < rows[b]; ++t, ++r) {
@@ -330,31 +340,55 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   // the prefill GEMMs read their activations (u, attention output, h) in frag layout
   VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
   const int n_layers = m->layer_limit > 0 ? std::min(m->layer_limit, D.L) : D.L;
+  // Only the rows read afterwards (head_rows: the last prefix row, or the n_actions
+  // scoring rows, of each environment) need the last layer's output; its other rows
+  // only feed the KV cache through the QKV projection.  Every row's computation is
+  // independent of which other rows run with it, so results are the same bits.
+  // (A layer limit set through the debug interface computes every row.)
+  const bool prune = m->layer_limit == 0;
+  const int R = tf ? B * D.nact : B;
+  double attn_flops_last = 0.0;  // q.k and p.v of the needed query rows only
+  for (int b = 0; b < B; ++b)
+    for (int t = prefix[b] - 1; t < rows[b]; ++t) attn_flops_last += 4.0 * D.d * (t + 1);
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
+    const bool last = prune && l == D.L - 1;
     GemmArgs g{};
     g.A = m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
     g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
     g.d_model = D.d; g.n_heads = D.H; g.head_dim = D.hd;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 3.0 * D.d, D.d), launch_gemm(g, kEpiQkvRope, s));
     PrefillAttnArgs pa{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
-                       B, D.d, D.H, D.hd, m->scale};
-    PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, attn_flops, launch_attn_prefill(pa, s));
+                       B, D.d, D.H, D.hd, m->scale, last ? m->env_q0 : nullptr};
+    PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, last ? attn_flops_last : attn_flops, launch_attn_prefill(pa, s));
+    // the rest of the layer runs on all rows, or on the compacted needed rows of the last layer
+    const int Ml = last ? R : Mi;
+    float* x = m->x;
+    bf16_t* u = m->u;
+    bf16_t* hbuf = m->h;
+    if (last) {
+      VLA_CK(launch_gather_rows(m->x, m->u, m->head_rows, R, D.d, m->xc, m->uc, s));
+      x = m->xc;
+      u = m->uc;
+      hbuf = m->hc;
+    }
     GemmArgs go{};
-    go.A = m->u; go.W = w.wo; go.M = Mi; go.N = D.d; go.K = D.d; go.C = m->x; go.ldc = D.d;
-    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.d), launch_gemm(go, kEpiResidual, s));
-    VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, w.mlp_norm, eps, m->u, D.d, Mi, D.d, s, true));
+    go.A = u; go.W = w.wo; go.M = Ml; go.N = D.d; go.K = D.d; go.C = x; go.ldc = D.d;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.d), launch_gemm(go, kEpiResidual, s));
+    VLA_CK(launch_rmsnorm(x, D.d, nullptr, w.mlp_norm, eps, u, D.d, Ml, D.d, s, true));
     GemmArgs gg{};
-    gg.A = m->u; gg.W = w.wgu; gg.M = Mi; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = m->h; gg.ldh = D.Fp;
-    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
+    gg.A = u; gg.W = w.wgu; gg.M = Ml; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = hbuf; gg.ldh = D.Fp;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
     GemmArgs gd{};
-    gd.A = m->h; gd.W = w.wd; gd.M = Mi; gd.N = D.d; gd.K = D.Fp; gd.C = m->x; gd.ldc = D.d;
-    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
+    gd.A = hbuf; gd.W = w.wd; gd.M = Ml; gd.N = D.d; gd.K = D.Fp; gd.C = x; gd.ldc = D.d;
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
     if (l + 1 < D.L)
       VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
   }
-  const int R = tf ? B * D.nact : B;
-  VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
+  if (prune)
+    VLA_CK(launch_rmsnorm(m->xc, D.d, nullptr, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
+  else
+    VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
   *out_rows = R;
   return VLA_OK;
 }
