@@ -130,7 +130,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int wm = wave & 1, wn = wave >> 1;  // 128-row half, 64-column quarter of the tile
-  const int KB = frag_kb(K);
+  const int KB = frag_kb(wave < 4 ? (a.ka ? a.ka : K) : (a.kw ? a.kw : K));  // frag row stride of the copied operand
   const int last_rb_a = (M + 15) / 16 - 1, last_rb_w = N / 16 - 1;
 
   // copies: wave w moves blocks 4 w .. 4 w + 3 of a step's 32 (waves 0-3: A, 4-7: W)
@@ -254,8 +254,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   // frag-layout operands, 32-bit byte offsets into them
-  if (a.K % BK != 0 || a.N % 64 != 0 || (long long)frag_elems(a.M, a.K) * 2 >= (1ll << 31) ||
-      (long long)frag_elems(a.N, a.K) * 2 >= (1ll << 31))
+  const int ka = a.ka ? a.ka : a.K, kw = a.kw ? a.kw : a.K;
+  if (a.K % BK != 0 || a.N % 64 != 0 || ka < a.K || kw < a.K || ka % 32 != 0 || kw % 32 != 0 ||
+      (long long)frag_elems(a.M, ka) * 2 >= (1ll << 31) || (long long)frag_elems(a.N, kw) * 2 >= (1ll << 31))
     return hipErrorInvalidValue;
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   const dim3 grid(tm * tn), block(NT);

@@ -42,6 +42,7 @@ struct GemmArgs {
   const bf16_t* A;  // [M, K] in frag layout
   const bf16_t* W;  // [N, K] in frag layout
   int M, N, K;
+  int ka, kw;       // K of A's and W's frag allocations when wider than the contraction (0: K)
   float* C;
   int ldc;
   bf16_t* H;

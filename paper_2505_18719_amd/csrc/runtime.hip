@@ -377,10 +377,13 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.d), launch_gemm(go, kEpiResidual, s));
     VLA_CK(launch_rmsnorm(x, D.d, nullptr, w.mlp_norm, eps, u, D.d, Ml, D.d, s, true));
     GemmArgs gg{};
-    gg.A = u; gg.W = w.wgu; gg.M = Ml; gg.N = 2 * D.Fp; gg.K = D.d; gg.H = hbuf; gg.ldh = D.Fp;
+    // [gate; up] interleaved in 64-row blocks: only the blocks holding real rows are computed; the
+    // down projection's contraction stops at the last real feature (h and Wdown stay Fp wide)
+    gg.A = u; gg.W = w.wgu; gg.M = Ml; gg.N = 64 * ((D.F + 31) / 32); gg.K = D.d; gg.H = hbuf; gg.ldh = D.Fp;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
     GemmArgs gd{};
-    gd.A = hbuf; gd.W = w.wd; gd.M = Ml; gd.N = D.d; gd.K = D.Fp; gd.C = x; gd.ldc = D.d;
+    gd.A = hbuf; gd.W = w.wd; gd.M = Ml; gd.N = D.d; gd.K = 32 * ((D.F + 31) / 32); gd.ka = D.Fp; gd.kw = D.Fp;
+    gd.C = x; gd.ldc = D.d;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
     if (l + 1 < D.L)
       VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
