@@ -15,7 +15,7 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # GPU tests need a GPU; elsewhere they are skipped with a clear reason
-    # unless explicitly selected (the GPU machine runs `-m gpu`).
+    # unless explicitly selected with `-m gpu` on a machine that has one.
     try:
         import torch
         have_gpu = torch.cuda.is_available()
