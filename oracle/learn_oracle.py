@@ -16,7 +16,11 @@ Sec. 3.3 "Learning Phase"), in float64 numpy:
     to every token log-probability;
   * the gradient of a token log-probability log softmax(z / T)[k] over the
     action bins with respect to the action logits z, which carries the
-    surrogate's gradient back into the teacher-forced pass.
+    surrogate's gradient back into the teacher-forced pass;
+  * the backward of that pass: the gradients of the PPO-clip loss with
+    respect to the LoRA factors A, B of every adapted projection (the policy
+    is trained through LoRA adapters merged as W0 + s B A, Sec. 3.3), by the
+    chain rule through the head, the final RMSNorm and every decoder block.
 
 Readings where the paper is silent: d_t flags that o_t is the first
 observation of a new episode, so the transition from step t to step t+1
@@ -95,3 +99,153 @@ def logprob_grad(logits, tokens, action_begin: int, temperature: float, dlogp) -
     onehot = np.zeros_like(p)
     onehot[np.arange(z.shape[0]), k] = 1.0
     return np.asarray(dlogp, dtype=np.float64)[:, None] * (onehot - p) / temperature
+
+
+# ----------------------------------------------------------------------------
+# backward of the teacher-forced pass: gradients of the PPO-clip loss with
+# respect to the LoRA factors (Sec. 3.3: the policy is trained through LoRA
+# adapters; the Learning Phase minimises -J of Eq. 2)
+# ----------------------------------------------------------------------------
+from . import vla_oracle as vo  # noqa: E402
+
+PROJ = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
+
+
+def merged_layers(w, adapters, scale: float, mode: str = "ideal"):
+    """Per-layer float64 weights W0 + s B A (rounded to bf16 in "bf16" mode,
+    the weights a rollout after the merge runs on); norms unchanged."""
+    out = []
+    for li, lw0 in enumerate(w["layers"]):
+        lw = {k: vo.to_f64(t) for k, t in lw0.items()}
+        for k, (a, b) in (adapters[li] if adapters is not None else {}).items():
+            m = lw[k] + scale * (vo.to_f64(b) @ vo.to_f64(a))
+            lw[k] = vo.bf16_round(m) if mode == "bf16" else m
+        out.append(lw)
+    return out
+
+
+def _layer_forward(cfg, lw, x, rnd):
+    """One decoder block on a whole sequence, keeping what the backward reads."""
+    L, d = x.shape
+    H, hd = cfg.n_heads, cfg.head_dim
+    pos = np.arange(L)
+    c = {"x": x}
+    c["u1"] = u1 = rnd(vo.rms_norm(x, lw["attn_norm"], cfg.rms_eps))
+    q = rnd(vo.apply_rope((u1 @ lw["wq"].T).reshape(L, H, hd), pos, cfg.rope_base))
+    k = rnd(vo.apply_rope((u1 @ lw["wk"].T).reshape(L, H, hd), pos, cfg.rope_base))
+    v = rnd((u1 @ lw["wv"].T).reshape(L, H, hd))
+    o, p = vo.causal_attention(q, k, v, pos, pos, return_probs=True)
+    c.update(q=q, k=k, v=v, p=p)
+    c["o"] = o = rnd(o.reshape(L, d))
+    c["xm"] = xm = x + o @ lw["wo"].T
+    c["u2"] = u2 = rnd(vo.rms_norm(xm, lw["mlp_norm"], cfg.rms_eps))
+    c["g"], c["up"] = u2 @ lw["wgate"].T, u2 @ lw["wup"].T
+    c["h"] = h = rnd(vo.silu(c["g"]) * c["up"])
+    return xm + h @ lw["wdown"].T, c
+
+
+def rms_norm_backward(x, gain, eps: float, dy):
+    """dx of y = x r gain, r = (mean(x^2) + eps)^(-1/2), over the last axis."""
+    d = x.shape[-1]
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+    gd = dy * gain
+    return r * gd - x * r ** 3 * np.sum(x * gd, axis=-1, keepdims=True) / d
+
+
+def rope_backward(dy, pos, base: float):
+    """Gradient through the rotary embedding: the transposed (inverse) rotation
+    of each (i, i + hd/2) pair."""
+    return vo.apply_rope(dy, -np.asarray(pos, dtype=np.float64), base)
+
+
+def _layer_backward(cfg, lw, c, dout, dw):
+    """Backward of one block: returns dx and adds dL/dW of every projection to dw."""
+    x, L = c["x"], c["x"].shape[0]
+    H, hd = cfg.n_heads, cfg.head_dim
+    pos = np.arange(L)
+    # MLP
+    dh = dout @ lw["wdown"]
+    dw["wdown"] += dout.T @ c["h"]
+    g, up = c["g"], c["up"]
+    sg = 1.0 / (1.0 + np.exp(-g))
+    dg = dh * up * sg * (1.0 + g * (1.0 - sg))   # d silu(g) / dg = s (1 + g (1 - s))
+    dup = dh * g * sg
+    du2 = dg @ lw["wgate"] + dup @ lw["wup"]
+    dw["wgate"] += dg.T @ c["u2"]
+    dw["wup"] += dup.T @ c["u2"]
+    dxm = dout + rms_norm_backward(c["xm"], lw["mlp_norm"], cfg.rms_eps, du2)
+    # attention
+    do = dxm @ lw["wo"]
+    dw["wo"] += dxm.T @ c["o"]
+    doh = np.transpose(do.reshape(L, H, hd), (1, 0, 2))
+    qh, kh, vh = (np.transpose(c[n], (1, 0, 2)) for n in ("q", "k", "v"))
+    p = c["p"]                                        # [H, L, L]
+    scale = 1.0 / np.sqrt(hd)
+    dv = np.matmul(np.transpose(p, (0, 2, 1)), doh)   # P^T dO
+    dp = np.matmul(doh, np.transpose(vh, (0, 2, 1)))  # dO V^T
+    ds = p * (dp - np.sum(dp * p, axis=-1, keepdims=True))
+    dq = np.matmul(ds, kh) * scale
+    dk = np.matmul(np.transpose(ds, (0, 2, 1)), qh) * scale
+    dq = rope_backward(np.transpose(dq, (1, 0, 2)), pos, cfg.rope_base).reshape(L, -1)
+    dk = rope_backward(np.transpose(dk, (1, 0, 2)), pos, cfg.rope_base).reshape(L, -1)
+    dv = np.transpose(dv, (1, 0, 2)).reshape(L, -1)
+    u1 = c["u1"]
+    du1 = dq @ lw["wq"] + dk @ lw["wk"] + dv @ lw["wv"]
+    dw["wq"] += dq.T @ u1
+    dw["wk"] += dk.T @ u1
+    dw["wv"] += dv.T @ u1
+    return dxm + rms_norm_backward(x, lw["attn_norm"], cfg.rms_eps, du1)
+
+
+def ppo_lora_grads(cfg, w, adapters, scale: float, vis, prompt_ids, prompt_lens, actions, logp_old,
+                   advantages, eps: float, temperature: float, mode: str = "ideal"):
+    """Loss -J of Eq. 2 over a minibatch of stored actions and its gradients
+    with respect to every LoRA factor, through the teacher-forced pass.
+
+    The policy's weights are W = W0 + s B A (Sec. 3.3); the action
+    log-probabilities are the sums of the teacher-forced token log-probabilities
+    (Eq. 1) over [visual ; prompt ; stored actions] (as vla_token_logprobs
+    scores them), and the loss is ppo_clip's.  "ideal": float64 throughout;
+    "bf16": the forward rounds where the rollout path stores bf16 (the
+    backward is the exact chain rule through those values, a rounding treated
+    as the identity).  Returns {"loss", "clip_frac", "logp", "grads"}, grads[l]
+    = {projection: (dA, dB)} for the adapted projections of layer l.
+    """
+    rnd = vo._rounder(mode)
+    layers = merged_layers(w, adapters, scale, mode)
+    W = vo.as_weights(w, cfg)
+    prompts = vo._split_prompts(np.asarray(prompt_ids), np.asarray(prompt_lens))
+    a0, na, B = cfg.action_begin, cfg.n_actions, len(prompts)
+    acts = np.asarray(actions, dtype=np.int64).reshape(B, na)
+    # forward of every sequence, keeping the caches
+    runs = []
+    logp = np.zeros((B, na))
+    for b in range(B):
+        x = np.concatenate([vo.prefix_embeddings(cfg, W, vis[b], prompts[b]), W.embed_rows(acts[b])])
+        L = x.shape[0] - na
+        caches = []
+        for lw in layers:
+            x, c = _layer_forward(cfg, lw, x, rnd)
+            caches.append(c)
+        hrows = x[L - 1:L - 1 + na]
+        z = vo.action_logits(cfg, W, hrows, rnd)
+        for i in range(na):
+            logp[b, i] = vo.token_stats(z[i], int(acts[b, i]) - a0, temperature)[0]
+        runs.append((L, x, caches, z))
+    loss, frac, dlogp = ppo_clip(logp, logp_old, advantages, eps)
+    dws = [{k: np.zeros_like(lw[k]) for k in PROJ} for lw in layers]
+    for b, (L, xL, caches, z) in enumerate(runs):
+        dz = logprob_grad(z, acts[b], a0, temperature, dlogp[b])
+        du = dz @ W.lm_action
+        dx = np.zeros_like(xL)
+        dx[L - 1:L - 1 + na] = rms_norm_backward(xL[L - 1:L - 1 + na], W.final_norm, cfg.rms_eps, du)
+        for li in range(len(layers) - 1, -1, -1):
+            dx = _layer_backward(cfg, layers[li], caches[li], dx, dws[li])
+    grads = []
+    for li in range(len(layers)):
+        gl = {}
+        for k, (a, bm) in (adapters[li] if adapters is not None else {}).items():
+            a, bm = vo.to_f64(a), vo.to_f64(bm)
+            gl[k] = (scale * bm.T @ dws[li][k], scale * dws[li][k] @ a.T)
+        grads.append(gl)
+    return {"loss": loss, "clip_frac": frac, "logp": logp, "grads": grads}

@@ -570,3 +570,88 @@ def test_extract_actions_inverts_an_independent_discretiser():
     centres = oracle.extract_actions(np.arange(256)[:, None] + np.zeros((1, 7), int), 0, 256, lo, hi)
     assert np.all(np.diff(centres, axis=0) > 0)
     assert np.allclose(centres.mean(axis=0), (lo + hi) / 2, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# backward of the teacher-forced pass: LoRA gradients of the PPO-clip loss
+# ---------------------------------------------------------------------------
+from paper_2505_18719_amd.inputs import VlaConfig, make_lora  # noqa: E402
+
+BWD_CFG = VlaConfig("bwd_pin", n_layers=2, d_model=32, n_heads=2, d_ffn=48, vocab=80, action_bins=16,
+                    n_actions=3, n_visual=4, batch=3, prompt_min=0, prompt_max=5)
+
+
+def _bwd_setup(seed=0):
+    cfg = BWD_CFG
+    w = make_weights(cfg, seed=seed, device="cpu")
+    inp = make_inputs(cfg, seed=seed, prompt_lens=[2, 5, 0])
+    ad = make_lora(cfg, 4, seed=seed, device="cpu", std=0.2)
+    rng = np.random.default_rng(seed)
+    acts = cfg.action_begin + rng.integers(0, cfg.action_bins, size=(cfg.batch, cfg.n_actions))
+    adv = rng.normal(size=cfg.batch)
+    return cfg, w, inp, ad, acts, adv
+
+
+def _fd_loss(cfg, w, inp, ad, s, acts, logp_old, adv, eps, T):
+    """The loss from the forward oracle on fp64-merged weights (no backward code)."""
+    w2 = dict(w)
+    w2["layers"] = [{k: torch.from_numpy(v) for k, v in lw.items()} for lw in lo.merged_layers(w, ad, s)]
+    logp = oracle.teacher_forced(cfg, w2, inp.vis, inp.prompt_ids, inp.prompt_lens, acts, T, mode="ideal")["logp"]
+    return lo.ppo_clip(logp, logp_old, adv, eps)[0]
+
+
+def test_lora_grads_match_central_differences_of_the_forward_oracle():
+    """Every projection of both layers, both factors: the analytic gradient of
+    -J (Eq. 2 through the teacher-forced pass) against central differences of
+    the loss computed by the forward oracle alone; one action clipped."""
+    cfg, w, inp, ad, acts, adv = _bwd_setup()
+    s, eps, T = 0.5, 0.2, 1.5
+    ad = [{k: (lo.vo.to_f64(a), lo.vo.to_f64(b)) for k, (a, b) in layer.items()} for layer in ad]
+    base = lo.ppo_lora_grads(cfg, w, ad, s, inp.vis, inp.prompt_ids, inp.prompt_lens, acts,
+                             np.zeros((cfg.batch, cfg.n_actions)), adv, eps, T)
+    rng = np.random.default_rng(1)
+    logp_old = base["logp"] + rng.normal(scale=0.02, size=base["logp"].shape)
+    logp_old[0] -= 0.2 if adv[0] > 0 else -0.2     # action 0 beyond the clip edge on its side
+    res = lo.ppo_lora_grads(cfg, w, ad, s, inp.vis, inp.prompt_ids, inp.prompt_lens, acts, logp_old, adv, eps, T)
+    assert res["clip_frac"] == 1.0 / cfg.batch
+    assert abs(res["loss"] - _fd_loss(cfg, w, inp, ad, s, acts, logp_old, adv, eps, T)) < 1e-12
+    h, worst = 1e-5, 0.0
+    for li in range(cfg.n_layers):
+        for k in lo.PROJ:
+            for f in (0, 1):  # A, then B
+                g = res["grads"][li][k][f]
+                scale_g = max(np.abs(g).max(), 1e-12)
+                for idx in [tuple(rng.integers(0, n) for n in g.shape) for _ in range(2)]:
+                    pert = [{kk: (a.copy(), b.copy()) for kk, (a, b) in layer.items()} for layer in ad]
+                    pert[li][k][f][idx] += h
+                    up = _fd_loss(cfg, w, inp, pert, s, acts, logp_old, adv, eps, T)
+                    pert[li][k][f][idx] -= 2 * h
+                    dn = _fd_loss(cfg, w, inp, pert, s, acts, logp_old, adv, eps, T)
+                    fd = (up - dn) / (2 * h)
+                    worst = max(worst, abs(fd - g[idx]) / scale_g)
+                    assert abs(fd - g[idx]) <= 1e-6 * scale_g + 1e-10, (li, k, f, idx, fd, g[idx])
+    assert worst < 1e-6
+
+
+def test_lora_grads_ratio_one_is_the_policy_gradient():
+    """At theta = theta_old (logp_old = logp_new) nothing is clipped and the
+    gradient is -(1/n) sum_b A_b grad log pi(a_b): with one unit advantage on
+    one action and zeros elsewhere it is -(1/n) times that action's
+    log-probability gradient, which is linear in the advantages."""
+    cfg, w, inp, ad, acts, adv = _bwd_setup(seed=2)
+    s, eps, T = 0.5, 0.2, 1.5
+    zero = np.zeros((cfg.batch, cfg.n_actions))
+    lp = lo.ppo_lora_grads(cfg, w, ad, s, inp.vis, inp.prompt_ids, inp.prompt_lens, acts, zero, adv, eps, T)["logp"]
+    full = lo.ppo_lora_grads(cfg, w, ad, s, inp.vis, inp.prompt_ids, inp.prompt_lens, acts, lp, adv, eps, T)
+    assert full["clip_frac"] == 0.0 and abs(full["loss"] + adv.mean()) < 1e-12
+    parts = []
+    for b in range(cfg.batch):
+        e = np.zeros(cfg.batch)
+        e[b] = adv[b]
+        parts.append(lo.ppo_lora_grads(cfg, w, ad, s, inp.vis, inp.prompt_ids, inp.prompt_lens, acts, lp, e, eps,
+                                       T)["grads"])
+    for li in range(cfg.n_layers):
+        for k in lo.PROJ:
+            for f in (0, 1):
+                tot = sum(p[li][k][f] for p in parts)
+                assert np.allclose(full["grads"][li][k][f], tot, rtol=1e-10, atol=1e-14)
