@@ -5,7 +5,8 @@
  * of Eq. 1, with the gradients that carry that objective back to the logits
  * of the teacher-forced pass (vla_token_logprobs).
  *
- * These calls need no model handle.  Conventions are those of vla.h: device
+ * All calls but vla_ppo_lora_grads (which runs the decoder held by a model
+ * handle) need no handle.  Conventions are those of vla.h: device
  * pointers, `hipStream_t` passed as `void*`, asynchronous on that stream,
  * no device allocation, status codes VLA_* with vla_last_error().
  */
@@ -71,6 +72,53 @@ int vla_ppo_clip(int32_t n, int32_t n_tokens, const float* logp_new, const float
 int vla_logprob_backward(int32_t rows, int32_t bins, int32_t action_begin, const float* logits,
                          const int32_t* tokens, float temperature, const float* dlogp, float* dlogits,
                          void* stream);
+
+/* LoRA adapters of the policy (Sec. 3.3: the policy is trained through LoRA
+ * adapters, merged as W = W0 + scale * B A) and the buffers for their
+ * gradients: host arrays of n_layers * 7 device pointers, layer-major, the
+ * projections in VLA_PROJ_* order (q, k, v, o, gate, up, down).  A NULL entry
+ * of `a` marks a projection without an adapter; its gradients are not written. */
+typedef struct vla_lora {
+  int32_t rank;            /* 1 <= rank <= 64 */
+  float scale;             /* alpha / rank */
+  const void* const* a;    /* bf16 [rank, in] row-major */
+  const void* const* b;    /* bf16 [out, rank] row-major */
+  float* const* grad_a;    /* fp32 [rank, in] out: dL/dA */
+  float* const* grad_b;    /* fp32 [out, rank] out: dL/dB */
+} vla_lora;
+
+/* Bytes of the training workspace vla_ppo_lora_grads needs for a handle of
+ * this configuration (the inputs of every layer for max_batch * max_seq rows,
+ * one layer's activations and gradients, transposed operands). */
+int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
+
+/* Gradient of one PPO update (Eq. 2, Sec. 3.3 Learning Phase) with respect to
+ * the LoRA factors.  The handle's packed weights must be the policy being
+ * updated, i.e. the merge of these adapters (vla_lora_merge).  Runs the
+ * teacher-forced pass over [visual ; prompt ; stored actions] (as
+ * vla_token_logprobs, every row of every layer), the PPO-clip loss on the
+ * action log-probabilities (vla_ppo_clip) and its gradient down to the
+ * action logits (vla_logprob_backward), then the backward of the whole pass:
+ * the head and final RMSNorm of the scoring rows, and for each layer from the
+ * top a recompute of its forward from its saved input, the gradient GEMMs
+ * against its transposed weights, RMSNorm, SwiGLU and causal-attention (with
+ * rotary) backward, and dL/dA = scale B^T G, dL/dB = scale G A^T from the
+ * projection's weight gradient G = dY^T X.
+ *   batch, vis_emb, prompt_ids, prompt_lens_host, action_tokens  as in
+ *                vla_token_logprobs
+ *   logp_old     fp32 [batch, n_actions] token log-probs of the rollout policy
+ *   advantages   fp32 [batch]
+ *   eps, temperature  clipping parameter (>= 0) and sampling temperature (> 0)
+ *   lora         adapters and gradient buffers (see vla_lora)
+ *   train_ws     device memory of >= vla_train_workspace_size bytes, 256-byte aligned
+ *   stats        fp32 [2] out: loss -J and clipped fraction
+ *   logp_new     fp32 [batch, n_actions] out, or NULL: the teacher-forced log-probs
+ * Gradient operands of the GEMMs are rounded to bf16 as the forward's
+ * activations are (fp32 accumulation).  Overwrites the handle's prefill state. */
+int vla_ppo_lora_grads(struct vla_model* m, int32_t batch, const void* vis_emb, const int32_t* prompt_ids,
+                       const int32_t* prompt_lens_host, const int32_t* action_tokens, const float* logp_old,
+                       const float* advantages, float eps, float temperature, const vla_lora* lora,
+                       void* train_ws, size_t train_ws_bytes, float* stats, float* logp_new, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,550 @@
+// Backward of the teacher-forced pass (the PPO update's gradient through the
+// decoder, Sec. 3.3 "Learning Phase"): layout conversions for the backward
+// GEMMs, RMSNorm and SwiGLU backward, and the causal attention backward with
+// the inverse rotary embedding.
+#include "common.h"
+#include "kernels.h"
+
+namespace vla {
+
+namespace {
+
+// dst (bf16 frag [R, kdst]) = x (fp32 row-major, row stride ld) for columns < n; the
+// other columns up to kdst and the rows of the last 16-row block past R are zero.
+__global__ void to_frag_kernel(const float* __restrict__ x, int ld, int R, int n, int kdst, bf16_t* __restrict__ dst) {
+  const int kc = kdst / 8;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int Rp = (R + 15) & ~15;
+  if (i >= (size_t)Rp * kc) return;
+  const int r = (int)(i / kc), k = (int)(i % kc) * 8;
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (r < R && k + e < n) ? x[(size_t)r * ld + k + e] : 0.f;
+  uint4 o;
+  o.x = pack2bf(v[0], v[1]);
+  o.y = pack2bf(v[2], v[3]);
+  o.z = pack2bf(v[4], v[5]);
+  o.w = pack2bf(v[6], v[7]);
+  *reinterpret_cast<uint4*>(dst + frag_index(r, k, kdst)) = o;
+}
+
+// dst[k, r] = src[r, k] into a bf16 frag matrix [K rows, Kd] (Kd >= R, multiple of 32;
+// columns R .. Kd and the rows of the last 16-row block past K zero).  The source is
+// fp32 row-major (row stride ld) or a bf16 frag matrix of frag width ld.  One
+// 64 x 64 tile per 256-thread workgroup through LDS.
+template <bool SRC_F32>
+__global__ __launch_bounds__(256) void transpose_frag_kernel(const void* __restrict__ src, int ld, int R, int K,
+                                                             int Kd, bf16_t* __restrict__ dst) {
+  __shared__ float t[64][65];
+  const int r0 = blockIdx.x * 64, k0 = blockIdx.y * 64, tid = threadIdx.x;
+  // load: thread reads 8 consecutive k of one source row (two rows per thread)
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int rr = tid / 8 + 32 * h, kk = (tid % 8) * 8;
+    const int r = r0 + rr;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = k0 + kk + e;
+      float v = 0.f;
+      if (r < R && k < K) {
+        if (SRC_F32) v = static_cast<const float*>(src)[(size_t)r * ld + k];
+        else v = bf2f(static_cast<const bf16_t*>(src)[frag_index(r, k, ld)]);
+      }
+      t[rr][kk + e] = v;
+    }
+  }
+  __syncthreads();
+  // store: thread writes 8 consecutive destination columns (source rows) of one destination row
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int kk = tid / 8 + 32 * h, rr = (tid % 8) * 8;
+    const int k = k0 + kk, r = r0 + rr;
+    const int Kp = (K + 15) & ~15;
+    if (k >= Kp || r >= Kd) continue;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (k < K) ? t[rr + e][kk] : 0.f;
+    uint4 o;
+    o.x = pack2bf(v[0], v[1]);
+    o.y = pack2bf(v[2], v[3]);
+    o.z = pack2bf(v[4], v[5]);
+    o.w = pack2bf(v[6], v[7]);
+    *reinterpret_cast<uint4*>(dst + frag_index(k, r, Kd)) = o;
+  }
+}
+
+// RMSNorm backward of y = x r g, r = (mean(x^2) + eps)^(-1/2), for one row per
+// workgroup: dx = dres + r (g dy) - x r^3 (sum x g dy) / d.  dres may be null;
+// dx_frag (bf16 frag, K = d) may be null.
+__global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restrict__ x, const float* __restrict__ g,
+                                                          float eps, const float* __restrict__ dy,
+                                                          const float* __restrict__ dres, float* __restrict__ dx,
+                                                          bf16_t* __restrict__ dx_frag, int d) {
+  __shared__ float red[2][4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const float* xr = x + (size_t)row * d;
+  const float* dyr = dy + (size_t)row * d;
+  float ss = 0.f, dot = 0.f;
+  for (int k = tid; k < d; k += 256) {
+    const float xv = xr[k];
+    ss += xv * xv;
+    dot += xv * g[k] * dyr[k];
+  }
+  ss = wave_sum(ss);
+  dot = wave_sum(dot);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = ss;
+    red[1][tid >> 6] = dot;
+  }
+  __syncthreads();
+  ss = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+  dot = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+  const float r = 1.f / sqrtf(ss / d + eps);
+  const float c = r * r * r * dot / d;
+  for (int k = 8 * tid; k < d; k += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const size_t i = (size_t)row * d + k + e;
+      v[e] = (dres ? dres[i] : 0.f) + r * g[k + e] * dy[i] - xr[k + e] * c;
+      dx[i] = v[e];
+    }
+    if (dx_frag) {
+      uint4 o;
+      o.x = pack2bf(v[0], v[1]);
+      o.y = pack2bf(v[2], v[3]);
+      o.z = pack2bf(v[4], v[5]);
+      o.w = pack2bf(v[6], v[7]);
+      *reinterpret_cast<uint4*>(dx_frag + frag_index(row, k, d)) = o;
+    }
+  }
+}
+
+// SwiGLU backward for h = silu(g) up, with g, up the fp32 gate/up pre-activations
+// in the packed interleaved order (columns 64 (j / 32) + j % 32 and +32 of cgu) and
+// dh fp32 [M, F] (row stride ldh): writes d[g; up] as bf16 frag in that same order
+// (K = 2 Fp) and the forward h = bf16(silu(g) up) as bf16 frag (K = Fp).
+__global__ void swiglu_bwd_kernel(const float* __restrict__ cgu, int ldc, const float* __restrict__ dh, int ldh,
+                                  int M, int F, int Fp, bf16_t* __restrict__ dgu, bf16_t* __restrict__ h) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int fc = Fp / 8;  // 8-feature chunks per row
+  if (i >= (size_t)M * fc) return;
+  const int m = (int)(i / fc), j0 = (int)(i % fc) * 8;  // features j0 .. j0 + 7 (one 32-block)
+  const int cg = 64 * (j0 / 32) + j0 % 32;
+  float dgv[8], duv[8], hv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int j = j0 + e;
+    if (j < F) {
+      const float gg = cgu[(size_t)m * ldc + cg + e], up = cgu[(size_t)m * ldc + cg + 32 + e];
+      const float s = 1.f / (1.f + expf(-gg));
+      const float d = dh[(size_t)m * ldh + j];
+      dgv[e] = d * up * s * (1.f + gg * (1.f - s));
+      duv[e] = d * gg * s;
+      hv[e] = gg / (1.f + expf(-gg)) * up;  // the forward epilogue's expression
+    } else {
+      dgv[e] = duv[e] = hv[e] = 0.f;
+    }
+  }
+  uint4 o;
+  o.x = pack2bf(dgv[0], dgv[1]); o.y = pack2bf(dgv[2], dgv[3]); o.z = pack2bf(dgv[4], dgv[5]); o.w = pack2bf(dgv[6], dgv[7]);
+  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg, 2 * Fp)) = o;
+  o.x = pack2bf(duv[0], duv[1]); o.y = pack2bf(duv[2], duv[3]); o.z = pack2bf(duv[4], duv[5]); o.w = pack2bf(duv[6], duv[7]);
+  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg + 32, 2 * Fp)) = o;
+  o.x = pack2bf(hv[0], hv[1]); o.y = pack2bf(hv[2], hv[3]); o.z = pack2bf(hv[4], hv[5]); o.w = pack2bf(hv[6], hv[7]);
+  *reinterpret_cast<uint4*>(h + frag_index(m, j0, Fp)) = o;
+}
+
+// ---- causal attention backward ------------------------------------------------
+// Per (environment, head) workgroup of 4 waves.  With P = softmax(scale q k^T)
+// (causal), dP = dO V^T, D_t = sum_j P_tj dP_tj and dS = P (dP - D):
+//   pass 1 (queries): dq_t = scale sum_j dS_tj k_j, and the row statistics
+//                     lse_t = log sum_j exp(scale q_t.k_j), D_t;
+//   pass 2 (keys):    dk_j = scale sum_t dS_tj q_t, dv_j = sum_t P_tj dO_t.
+// q and k are the rotated values the forward attended with; the gradients are
+// taken back through the rotary embedding (the inverse rotation at each row's
+// position) and written as bf16 into the [q; k; v] gradient matrix in the
+// packed weight's column order (frag layout, K = 3 d).
+constexpr int kBwdKeys = 320;  // longest sequence (one environment)
+
+template <int HD>
+__device__ __forceinline__ int bwd_swz(int row) { return row & (HD / 8 - 1); }
+// LDS element (row, f) of a [kBwdKeys, HD] bf16 tile whose 16-byte chunks are swizzled per row
+template <int HD>
+__device__ __forceinline__ int bwd_lds(int row, int f) {
+  return (row * (HD / 8) + ((f >> 3) ^ bwd_swz<HD>(row))) * 8 + (f & 7);
+}
+// packed column of natural feature f of a rotated head (q, k): pairs (i, i + HD/2) of each
+// 32-feature block sit 32 columns apart in 64-column groups
+template <int HD>
+__device__ __forceinline__ int qk_packed_col(int f) {
+  constexpr int half = HD / 2;
+  return f < half ? 64 * (f >> 5) + (f & 31) : 64 * ((f - half) >> 5) + 32 + ((f - half) & 31);
+}
+
+template <int HD>
+__device__ __forceinline__ void bwd_load_q_do(const AttnBwdArgs& a, int row, int head, float* q, float* dov) {
+  const bf16_t* qp = a.q + (size_t)row * a.d + head * HD;
+  const float* dp = a.dout + (size_t)row * a.d + head * HD;
+#pragma unroll
+  for (int c = 0; c < HD / 8; ++c) {
+    float f8[8];
+    unpack8(*reinterpret_cast<const uint4*>(qp + 8 * c), f8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[8 * c + e] = f8[e];
+    const float4 x0 = *reinterpret_cast<const float4*>(dp + 8 * c);
+    const float4 x1 = *reinterpret_cast<const float4*>(dp + 8 * c + 4);
+    dov[8 * c + 0] = x0.x; dov[8 * c + 1] = x0.y; dov[8 * c + 2] = x0.z; dov[8 * c + 3] = x0.w;
+    dov[8 * c + 4] = x1.x; dov[8 * c + 5] = x1.y; dov[8 * c + 6] = x1.z; dov[8 * c + 7] = x1.w;
+  }
+}
+
+// dot of a register row with LDS row `row` of tile t (bf16, swizzled chunks)
+template <int HD>
+__device__ __forceinline__ float bwd_dot(const bf16_t* t, int row, const float* v) {
+  float acc = 0.f;
+#pragma unroll
+  for (int c = 0; c < HD / 8; ++c) {
+    float f8[8];
+    unpack8(*reinterpret_cast<const uint4*>(t + (row * (HD / 8) + (c ^ bwd_swz<HD>(row))) * 8), f8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += v[8 * c + e] * f8[e];
+  }
+  return acc;
+}
+
+// write the gradient of feature pair (f, f + HD/2) of row `row` (position pos) back
+// through the rotation, into region `region` (0 q, 1 k) of the [q; k; v] gradient
+template <int HD>
+__device__ __forceinline__ void bwd_store_rot(const AttnBwdArgs& a, int row, int pos, int head, int region, int f,
+                                              float g1, float g2) {
+  const float2 cs = a.rope[pos * (HD / 2) + f];
+  const float p1 = g1 * cs.x + g2 * cs.y, p2 = -g1 * cs.y + g2 * cs.x;
+  const int base = region * a.d + head * HD;
+  const int K3 = 3 * a.d;
+  a.dqkv[frag_index(row, base + qk_packed_col<HD>(f), K3)] = f2bf(p1);
+  a.dqkv[frag_index(row, base + qk_packed_col<HD>(f + HD / 2), K3)] = f2bf(p2);
+}
+
+template <int HD>
+__global__ __launch_bounds__(256, 1) void attn_bwd_q_kernel(AttnBwdArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t ks[kBwdKeys * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t vs[kBwdKeys * HD];
+  constexpr int NS = kBwdKeys / 64;  // key slots per lane
+  const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
+  const int L = a.env_len[env], row0 = a.env_row0[env];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t* pt = a.page_table + env * a.max_pages;
+  // K rows (key-major in the cache) and V (feature-major pages) into key-major LDS
+  for (int i = tid; i < L * (HD / 8); i += 256) {
+    const int j = i / (HD / 8), c = i % (HD / 8);
+    const int page = pt[j / kPage], slot = j % kPage;
+    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * c;
+    *reinterpret_cast<uint4*>(ks + (j * (HD / 8) + (c ^ bwd_swz<HD>(j))) * 8) = *reinterpret_cast<const uint4*>(kp);
+    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * c) * kPage + slot;
+    bf16_t v8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v8[e] = vp[e * kPage];
+    uint4 o;
+    o.x = v8[0] | (uint32_t(v8[1]) << 16); o.y = v8[2] | (uint32_t(v8[3]) << 16);
+    o.z = v8[4] | (uint32_t(v8[5]) << 16); o.w = v8[6] | (uint32_t(v8[7]) << 16);
+    *reinterpret_cast<uint4*>(vs + (j * (HD / 8) + (c ^ bwd_swz<HD>(j))) * 8) = o;
+  }
+  __syncthreads();
+  for (int t = wave; t < L; t += 4) {
+    float q[HD], dov[HD];
+    bwd_load_q_do<HD>(a, row0 + t, head, q, dov);
+    float sv[NS], dpv[NS];
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      const int j = lane + 64 * i;
+      sv[i] = -INFINITY;
+      dpv[i] = 0.f;
+      if (j <= t) {
+        sv[i] = a.scale * bwd_dot<HD>(ks, j, q);
+        dpv[i] = bwd_dot<HD>(vs, j, dov);
+      }
+      m = fmaxf(m, sv[i]);
+    }
+    m = wave_max(m);
+    float l = 0.f;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      sv[i] = lane + 64 * i <= t ? expf(sv[i] - m) : 0.f;
+      l += sv[i];
+    }
+    l = wave_sum(l);
+    const float inv = 1.f / l;
+    float dd = 0.f;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      sv[i] *= inv;  // P
+      dd += sv[i] * dpv[i];
+    }
+    dd = wave_sum(dd);
+#pragma unroll
+    for (int i = 0; i < NS; ++i) dpv[i] = sv[i] * (dpv[i] - dd);  // dS
+    if (lane == 0) {
+      a.stats[((size_t)(row0 + t) * H + head) * 2] = m + logf(l);
+      a.stats[((size_t)(row0 + t) * H + head) * 2 + 1] = dd;
+    }
+    // dq over features f = lane (+ 64): dS_j is read from the lane holding key j
+    constexpr int FPL = HD / 64;  // features per lane
+    float dq[FPL];
+#pragma unroll
+    for (int u = 0; u < FPL; ++u) dq[u] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      const int jend = min(t + 1, 64 * (i + 1));
+      for (int j = 64 * i; j < jend; ++j) {
+        const float ds = __builtin_amdgcn_readlane(__float_as_int(dpv[i]), j - 64 * i);
+#pragma unroll
+        for (int u = 0; u < FPL; ++u) dq[u] += __int_as_float(ds) * bf2f(ks[bwd_lds<HD>(j, lane + 64 * u)]);
+      }
+    }
+    // back through the rotation: pair (f, f + HD/2) is (lane, lane + 64) at HD 128, lanes f and f + 32 at HD 64
+    if (HD == 128) {
+      bwd_store_rot<HD>(a, row0 + t, t, head, 0, lane, a.scale * dq[0], a.scale * dq[FPL - 1]);
+    } else {
+      const float partner = __shfl_xor(dq[0], 32, kWave);
+      if (lane < 32) bwd_store_rot<HD>(a, row0 + t, t, head, 0, lane, a.scale * dq[0], a.scale * partner);
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256, 1) void attn_bwd_kv_kernel(AttnBwdArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t qs[kBwdKeys * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t os[kBwdKeys * HD];  // dO rounded to bf16
+  constexpr int NS = kBwdKeys / 64;
+  const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
+  const int L = a.env_len[env], row0 = a.env_row0[env];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t* pt = a.page_table + env * a.max_pages;
+  for (int i = tid; i < L * (HD / 8); i += 256) {
+    const int t = i / (HD / 8), c = i % (HD / 8);
+    const int at = (t * (HD / 8) + (c ^ bwd_swz<HD>(t))) * 8;
+    *reinterpret_cast<uint4*>(qs + at) =
+        *reinterpret_cast<const uint4*>(a.q + (size_t)(row0 + t) * a.d + head * HD + 8 * c);
+    const float* dp = a.dout + (size_t)(row0 + t) * a.d + head * HD + 8 * c;
+    const float4 x0 = *reinterpret_cast<const float4*>(dp), x1 = *reinterpret_cast<const float4*>(dp + 4);
+    uint4 o;
+    o.x = pack2bf(x0.x, x0.y); o.y = pack2bf(x0.z, x0.w); o.z = pack2bf(x1.x, x1.y); o.w = pack2bf(x1.z, x1.w);
+    *reinterpret_cast<uint4*>(os + at) = o;
+  }
+  __syncthreads();
+  for (int j = wave; j < L; j += 4) {
+    // this key's k and v (the cache's bf16 values)
+    const int page = pt[j / kPage], slot = j % kPage;
+    float kf[HD], vf[HD];
+    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD;
+    const bf16_t* vp = a.kv.v + ((size_t)page * H + head) * HD * kPage + slot;
+#pragma unroll
+    for (int c = 0; c < HD / 8; ++c) {
+      float f8[8];
+      unpack8(*reinterpret_cast<const uint4*>(kp + 8 * c), f8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kf[8 * c + e] = f8[e];
+    }
+#pragma unroll
+    for (int f = 0; f < HD; ++f) vf[f] = bf2f(vp[f * kPage]);
+    float pv[NS], dsv[NS];
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      const int t = j + lane + 64 * i;
+      pv[i] = dsv[i] = 0.f;
+      if (t < L) {
+        const float* st = a.stats + ((size_t)(row0 + t) * H + head) * 2;
+        const float p = expf(a.scale * bwd_dot<HD>(qs, t, kf) - st[0]);
+        pv[i] = p;
+        dsv[i] = p * (bwd_dot<HD>(os, t, vf) - st[1]);
+      }
+    }
+    constexpr int FPL = HD / 64;
+    float dk[FPL], dv[FPL];
+#pragma unroll
+    for (int u = 0; u < FPL; ++u) dk[u] = dv[u] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      const int tend = min(L, j + 64 * (i + 1));
+      for (int t = j + 64 * i; t < tend; ++t) {
+        const float ds = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsv[i]), t - j - 64 * i));
+        const float p = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pv[i]), t - j - 64 * i));
+#pragma unroll
+        for (int u = 0; u < FPL; ++u) {
+          dk[u] += ds * bf2f(qs[bwd_lds<HD>(t, lane + 64 * u)]);
+          dv[u] += p * bf2f(os[bwd_lds<HD>(t, lane + 64 * u)]);
+        }
+      }
+    }
+    const int row = row0 + j, K3 = 3 * a.d;
+#pragma unroll
+    for (int u = 0; u < FPL; ++u)
+      a.dqkv[frag_index(row, 2 * a.d + head * HD + lane + 64 * u, K3)] = f2bf(dv[u]);
+    if (HD == 128) {
+      bwd_store_rot<HD>(a, row, j, head, 1, lane, a.scale * dk[0], a.scale * dk[FPL - 1]);
+    } else {
+      const float partner = __shfl_xor(dk[0], 32, kWave);
+      if (lane < 32) bwd_store_rot<HD>(a, row, j, head, 1, lane, a.scale * dk[0], a.scale * partner);
+    }
+  }
+}
+
+// ---- LoRA gradients from a weight gradient ---------------------------------------
+// With W = W0 + s B A and G = dL/dW [out, in]: dL/dA = s B^T G, dL/dB = s G A^T.
+// G is given transposed, column o0 + o of dwt holding output o in the packed row
+// order of `mode` (grad_row maps it to the natural row, or -1 for a padding row
+// or the other half of [gate; up]).  64 x 64 output tiles of fp32 FMAs through LDS.
+__device__ __forceinline__ int grad_row(const LoraGradArgs& a, int o) {
+  int part;
+  const int j = pack_src_row(a.mode, o, a.head_dim, a.out, part);
+  return (j >= 0 && (a.mode != kPackGateUp || part == a.part)) ? j : -1;
+}
+
+__global__ __launch_bounds__(256) void lora_da_kernel(LoraGradArgs a) {
+  __shared__ float ws[64][33];  // dwt[i0 + ii, o]
+  __shared__ float bs[32][65];  // B[grad_row(o), c]
+  const int i0 = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  float acc[4][4] = {};
+  for (int ob = 0; ob < a.n_cols; ob += 32) {
+    for (int e = tid; e < 64 * 32; e += 256) {
+      const int ii = e / 32, oo = e % 32;
+      ws[ii][oo] = (i0 + ii < a.in && ob + oo < a.n_cols) ? a.dwt[(size_t)(i0 + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
+      const int c = e % 64, o2 = e / 64;
+      const int nr = ob + o2 < a.n_cols ? grad_row(a, ob + o2) : -1;
+      bs[o2][c] = (nr >= 0 && c < a.r) ? bf2f(a.b[(size_t)nr * a.r + c]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int oo = 0; oo < 32; ++oo)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] += ws[ty * 4 + u][oo] * bs[oo][tx * 4 + v];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = i0 + ty * 4 + u, c = tx * 4 + v;
+      if (i < a.in && c < a.r) a.da[(size_t)c * a.in + i] = a.scale * acc[u][v];
+    }
+}
+
+__global__ __launch_bounds__(256) void lora_db_kernel(LoraGradArgs a) {
+  __shared__ float ws[32][65];  // dwt[i, o0 + ob + oo]
+  __shared__ float as[32][65];  // A[c, i]
+  const int ob = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  float acc[4][4] = {};
+  for (int ib = 0; ib < a.in; ib += 32) {
+    for (int e = tid; e < 32 * 64; e += 256) {
+      const int ii = e / 64, oo = e % 64;
+      ws[ii][oo] = (ib + ii < a.in && ob + oo < a.n_cols) ? a.dwt[(size_t)(ib + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
+      const int c = e % 64, i2 = e / 64;
+      as[i2][c] = (c < a.r && ib + i2 < a.in) ? bf2f(a.a[(size_t)c * a.in + ib + i2]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int ii = 0; ii < 32; ++ii)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] += ws[ii][ty * 4 + u] * as[ii][tx * 4 + v];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int o = ob + ty * 4 + u;
+    const int nr = o < a.n_cols ? grad_row(a, o) : -1;
+    if (nr < 0) continue;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int c = tx * 4 + v;
+      if (c < a.r) a.db[(size_t)nr * a.r + c] = a.scale * acc[u][v];
+    }
+  }
+}
+
+// dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), fp32 rows of d
+template <bool SCATTER>
+__global__ void move_rows_kernel(const float* __restrict__ src, const int32_t* __restrict__ rows, int d,
+                                 float* __restrict__ dst) {
+  const int i = blockIdx.x, r = rows[i];
+  for (int k = threadIdx.x; k < d; k += 256) {
+    if (SCATTER) dst[(size_t)r * d + k] = src[(size_t)i * d + k];
+    else dst[(size_t)i * d + k] = src[(size_t)r * d + k];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s) {
+  if (a.r < 1 || a.r > 64 || a.in <= 0 || a.n_cols <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lora_da_kernel, dim3((a.in + 63) / 64), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(lora_db_kernel, dim3((a.n_cols + 63) / 64), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d, float* dst, bool scatter,
+                            hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (scatter) hipLaunchKernelGGL(move_rows_kernel<true>, dim3(R), dim3(256), 0, s, src, rows, d, dst);
+  else hipLaunchKernelGGL(move_rows_kernel<false>, dim3(R), dim3(256), 0, s, src, rows, d, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s) {
+  if (a.n_env <= 0) return hipSuccess;
+  const dim3 grid(a.n_env, a.n_heads), block(256);
+  if (a.head_dim == 128) {
+    hipLaunchKernelGGL(attn_bwd_q_kernel<128>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_kv_kernel<128>, grid, block, 0, s, a);
+  } else if (a.head_dim == 64) {
+    hipLaunchKernelGGL(attn_bwd_q_kernel<64>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_kv_kernel<64>, grid, block, 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_to_frag(const float* x, int ld, int R, int n, int kdst, bf16_t* dst, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (kdst % 32 != 0 || n > kdst) return hipErrorInvalidValue;
+  const size_t work = (size_t)((R + 15) & ~15) * (kdst / 8);
+  hipLaunchKernelGGL(to_frag_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, x, ld, R, n, kdst, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_frag(const void* src, bool src_f32, int ld, int R, int K, int Kd, bf16_t* dst,
+                                 hipStream_t s) {
+  if (R <= 0 || K <= 0) return hipSuccess;
+  if (Kd % 32 != 0 || Kd < R) return hipErrorInvalidValue;
+  // tiles cover rows up to Kd (zero columns) and destination rows up to K rounded to 16
+  const dim3 grid((Kd + 63) / 64, (((K + 15) & ~15) + 63) / 64);
+  if (src_f32) hipLaunchKernelGGL(transpose_frag_kernel<true>, grid, dim3(256), 0, s, src, ld, R, K, Kd, dst);
+  else hipLaunchKernelGGL(transpose_frag_kernel<false>, grid, dim3(256), 0, s, src, ld, R, K, Kd, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const float* dy, const float* dres,
+                              float* dx, bf16_t* dx_frag, int M, int d, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (d % 8 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_bwd_kernel, dim3(M), dim3(256), 0, s, x, g, eps, dy, dres, dx, dx_frag, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
+                             bf16_t* h, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (Fp % 32 != 0 || F > Fp) return hipErrorInvalidValue;
+  const size_t work = (size_t)M * (Fp / 8);
+  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, cgu, ldc, dh, ldh, M,
+                     F, Fp, dgu, h);
+  return hipGetLastError();
+}
+
+}  // namespace vla

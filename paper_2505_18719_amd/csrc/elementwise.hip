@@ -256,21 +256,6 @@ __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restr
 //               rotary pairs 32 rows apart: block b = rows [32b, 32b+32) then
 //               [half+32b, half+32b+32)
 //  kPackGateUp: [gate; up] interleaved in blocks of 32 rows, zero rows past src_rows
-// Source row of destination row r under a packing mode, or -1 for a zero
-// row; for kPackGateUp `part` receives 0 (gate) or 1 (up).
-__device__ __forceinline__ int pack_src_row(int mode, int r, int head_dim, int src_rows, int& part) {
-  part = 0;
-  if (mode == kPackRows) return r < src_rows ? r : -1;
-  if (mode == kPackQk) {
-    const int head = r / head_dim, p = r % head_dim, half = head_dim / 2;
-    const int blk = p / 64, c = p % 64;
-    return head * head_dim + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32);
-  }
-  part = (r % 64) < 32 ? 0 : 1;
-  const int j = 32 * (r / 64) + (r % 32);
-  return j < src_rows ? j : -1;
-}
-
 __global__ __launch_bounds__(256) void pack_frag_kernel(PackArgs a) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   const int kc = a.K / 8;

@@ -195,6 +195,20 @@ hipError_t launch_sampler(const SamplerArgs& a, hipStream_t s);
 
 // Weight packing (one-time, at create): dst [rows, K] in frag layout (see frag_index)
 enum PackMode { kPackRows = 0, kPackQk = 1, kPackGateUp = 2 };
+// Source row of destination row r under a packing mode, or -1 for a zero
+// row; for kPackGateUp `part` receives 0 (gate) or 1 (up).
+__device__ inline int pack_src_row(int mode, int r, int head_dim, int src_rows, int& part) {
+  part = 0;
+  if (mode == kPackRows) return r < src_rows ? r : -1;
+  if (mode == kPackQk) {
+    const int head = r / head_dim, p = r % head_dim, half = head_dim / 2;
+    const int blk = p / 64, c = p % 64;
+    return head * head_dim + (c < 32 ? 32 * blk + c : half + 32 * blk + c - 32);
+  }
+  part = (r % 64) < 32 ? 0 : 1;
+  const int j = 32 * (r / 64) + (r % 32);
+  return j < src_rows ? j : -1;
+}
 struct PackArgs {
   bf16_t* dst;
   int rows, K;
@@ -271,6 +285,53 @@ hipError_t launch_extract_actions(const int32_t* tokens, int n, int n_dims, int 
 // (both bf16 frag layout with K = d; d % 8 == 0).
 hipError_t launch_gather_rows(const float* x, const bf16_t* o, const int32_t* rows, int R, int d, float* xc,
                               bf16_t* oc, hipStream_t s);
+// Backward of the teacher-forced pass.
+// dst (bf16 frag [R, kdst]) = fp32 row-major x (row stride ld), columns >= n zero
+hipError_t launch_to_frag(const float* x, int ld, int R, int n, int kdst, bf16_t* dst, hipStream_t s);
+// dst (bf16 frag [K rows, Kd]) = transpose of src [R, K]: fp32 row-major (src_f32, row
+// stride ld) or bf16 frag of frag width ld; columns R .. Kd zero (Kd % 32 == 0, Kd >= R)
+hipError_t launch_transpose_frag(const void* src, bool src_f32, int ld, int R, int K, int Kd, bf16_t* dst,
+                                 hipStream_t s);
+// dx = dres + RMSNorm backward of dy at x (gain g), one row per workgroup; dres, dx_frag may be null
+hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const float* dy, const float* dres,
+                              float* dx, bf16_t* dx_frag, int M, int d, hipStream_t s);
+// SwiGLU backward from the fp32 interleaved gate/up pre-activations and dh: d[g; up] (bf16 frag,
+// K = 2 Fp, the packed interleaved order) and the forward h (bf16 frag, K = Fp)
+hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
+                             bf16_t* h, hipStream_t s);
+struct AttnBwdArgs {
+  const bf16_t* q;        // [M, d] rotated queries of the forward
+  const float* dout;      // [M, d] gradient of the attention output
+  KvCache kv;             // rotated keys and values of the forward
+  const int32_t* page_table;
+  int max_pages;
+  const int32_t* env_row0;
+  const int32_t* env_len;  // <= 320
+  int n_env, d, n_heads, head_dim;
+  float scale;
+  const float2* rope;     // [pos][head_dim / 2] (cos, sin)
+  float* stats;           // [M, n_heads, 2] scratch: log-sum-exp and D of each query row
+  bf16_t* dqkv;           // [M, 3 d] bf16 frag (K = 3 d): gradients of q, k (before rotation, packed order), v
+};
+hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s);
+// LoRA gradients of one projection from its weight gradient, given transposed:
+// dA = s B^T G [r, in] and dB = s G A^T [out, r] (fp32, row-major, overwritten)
+struct LoraGradArgs {
+  const float* dwt;  // [in rows, ldw]: column o0 + o = output o in the packed order of `mode`
+  int ldw, o0, n_cols;
+  int in, out;       // natural sizes of the projection
+  int mode, head_dim, part;  // PackMode of its packed rows; part 0 gate / 1 up for kPackGateUp
+  const bf16_t* a;   // [r, in] row-major
+  const bf16_t* b;   // [out, r] row-major
+  int r;             // 1 .. 64
+  float scale;
+  float* da;
+  float* db;
+};
+hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s);
+// fp32 rows of d: dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), i < R
+hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d, float* dst, bool scatter,
+                            hipStream_t s);
 hipError_t launch_bf16_to_f32(float* dst, const bf16_t* src, int n, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

@@ -274,8 +274,11 @@ int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t
 
 // Shared forward over a packed ragged batch: prefill (actions == nullptr) or
 // teacher-forced (each environment's rows extended by its action tokens).
+// save_x (training): per-layer device buffers that receive each layer's input
+// residual; a training pass computes every row of the last layer.
 int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, const int32_t* lens_host,
-            const int32_t* actions, hipStream_t s, int* out_rows) {
+            const int32_t* actions, hipStream_t s, int* out_rows, float* const* save_x = nullptr,
+            int* out_M = nullptr) {
   const Dims& D = m->D;
   const bool tf = actions != nullptr;
   std::vector<int> prefix(B), rows(B);
@@ -345,7 +348,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   // only feed the KV cache through the QKV projection.  Every row's computation is
   // independent of which other rows run with it, so results are the same bits.
   // (A layer limit set through the debug interface computes every row.)
-  const bool prune = m->layer_limit == 0;
+  const bool prune = m->layer_limit == 0 && save_x == nullptr;
   const int R = tf ? B * D.nact : B;
   double attn_flops_last = 0.0;  // q.k and p.v of the needed query rows only
   for (int b = 0; b < B; ++b)
@@ -353,6 +356,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     const bool last = prune && l == D.L - 1;
+    if (save_x) VLA_CK(hipMemcpyAsync(save_x[l], m->x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
     GemmArgs g{};
     g.A = m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
     g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
@@ -393,6 +397,140 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   else
     VLA_CK(launch_rmsnorm(m->x, D.d, m->head_rows, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
   *out_rows = R;
+  if (out_M) *out_M = Mi;
+  return VLA_OK;
+}
+
+// ---- training (backward of the teacher-forced pass) --------------------------
+// Buffers of the caller's training workspace.
+struct TrainBufs {
+  std::vector<float*> xs;  // per-layer input residual [Mmax, d]
+  float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *dwt, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp;
+  bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t;
+};
+
+void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
+  const size_t Mx = D.Mmax, d = D.d;
+  const int A32 = round_up(D.A, 32), Mk = round_up((int)D.Mmax, 32);
+  const size_t Rh = (size_t)D.Bmax * D.nact;
+  t.xs.resize(D.L);
+  for (int l = 0; l < D.L; ++l) t.xs[l] = L.take<float>(Mx * d);
+  t.dx = L.take<float>(Mx * d);
+  t.dxm = L.take<float>(Mx * d);
+  t.du = L.take<float>(Mx * d);
+  t.dob = L.take<float>(Mx * d);
+  t.xm = L.take<float>(Mx * d);
+  t.cgu = L.take<float>(Mx * 2 * D.Fp);
+  t.dh = L.take<float>(Mx * D.Fp);
+  t.dwt = L.take<float>(std::max(d * 3 * d, std::max(d * 2 * D.Fp, (size_t)D.Fp * d)));
+  t.stats = L.take<float>(Mx * D.H * 2);
+  t.dz = L.take<float>(Rh * D.A);
+  t.du_h = L.take<float>(Rh * d);
+  t.xc = L.take<float>(Rh * d);
+  t.dxc = L.take<float>(Rh * d);
+  t.logp = L.take<float>(Rh);
+  t.dlogp = L.take<float>(Rh);
+  t.dxf = L.take<bf16_t>(frag_elems(Mx, d));
+  t.dxmf = L.take<bf16_t>(frag_elems(Mx, d));
+  t.u1 = L.take<bf16_t>(frag_elems(Mx, d));
+  t.ob = L.take<bf16_t>(frag_elems(Mx, d));
+  t.u2 = L.take<bf16_t>(frag_elems(Mx, d));
+  t.hb = L.take<bf16_t>(frag_elems(Mx, D.Fp));
+  t.dgu = L.take<bf16_t>(frag_elems(Mx, 2 * D.Fp));
+  t.dqkv = L.take<bf16_t>(frag_elems(Mx, 3 * D.d));
+  t.wt = L.take<bf16_t>(std::max(std::max(frag_elems(D.Fp, D.d), frag_elems(D.d, 2 * D.Fp)),
+                                 std::max(frag_elems(D.d, D.d), frag_elems(D.d, 3 * D.d))));
+  t.xt = L.take<bf16_t>(frag_elems(std::max(D.d, D.Fp), Mk));
+  t.dyt = L.take<bf16_t>(frag_elems(std::max(3 * D.d, 2 * D.Fp), Mk));
+  t.dzf = L.take<bf16_t>(frag_elems(Rh, A32));
+  t.wact_t = L.take<bf16_t>(frag_elems(D.d, A32));
+  L.off = align_up(L.off, 256);
+}
+
+// C (fp32, ldc) = A W^T on the prefill GEMM
+hipError_t gemm_f32(const bf16_t* A, int ka, const bf16_t* W, int kw, int M, int N, int K, float* C, int ldc,
+                    hipStream_t s) {
+  GemmArgs g{};
+  g.A = A; g.W = W; g.M = M; g.N = N; g.K = K; g.ka = ka; g.kw = kw; g.C = C; g.ldc = ldc;
+  return launch_gemm(g, kEpiStoreF32, s);
+}
+
+// Backward of decoder layer l: t.dx holds dL/d(layer output) [M, d] and receives
+// dL/d(layer input); LoRA gradients of the adapted projections are written.
+int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lora* lora, hipStream_t s) {
+  const Dims& D = m->D;
+  const LayerW& w = m->lw[l];
+  const float eps = m->cfg.rms_eps;
+  const int d = D.d, Fp = D.Fp, F64 = round_up(D.F, 64), Fg = 64 * ((D.F + 31) / 32);
+  const int Mk = round_up(M, 32);
+  // recompute the layer's forward from its saved input
+  VLA_CK(launch_rmsnorm(t.xs[l], d, nullptr, w.attn_norm, eps, t.u1, d, M, d, s, true));
+  GemmArgs g{};
+  g.A = t.u1; g.W = w.wqkv; g.M = M; g.N = 3 * d; g.K = d;
+  g.q = m->q; g.ldq = d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
+  g.d_model = d; g.n_heads = D.H; g.head_dim = D.hd;
+  VLA_CK(launch_gemm(g, kEpiQkvRope, s));
+  PrefillAttnArgs pa{m->q, t.ob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
+                     B, d, D.H, D.hd, m->scale, nullptr};
+  VLA_CK(launch_attn_prefill(pa, s));
+  VLA_CK(hipMemcpyAsync(t.xm, t.xs[l], (size_t)M * d * sizeof(float), hipMemcpyDeviceToDevice, s));
+  GemmArgs go{};
+  go.A = t.ob; go.W = w.wo; go.M = M; go.N = d; go.K = d; go.C = t.xm; go.ldc = d;
+  VLA_CK(launch_gemm(go, kEpiResidual, s));
+  VLA_CK(launch_rmsnorm(t.xm, d, nullptr, w.mlp_norm, eps, t.u2, d, M, d, s, true));
+  VLA_CK(gemm_f32(t.u2, 0, w.wgu, 0, M, Fg, d, t.cgu, 2 * Fp, s));
+  // MLP: dh = dy Wd, SwiGLU backward, du2 = d[g; up] Wgu, RMSNorm backward
+  VLA_CK(launch_to_frag(t.dx, d, M, d, d, t.dxf, s));
+  VLA_CK(launch_transpose_frag(w.wd, false, Fp, d, Fp, d, t.wt, s));
+  VLA_CK(gemm_f32(t.dxf, 0, t.wt, 0, M, F64, d, t.dh, Fp, s));
+  VLA_CK(launch_swiglu_bwd(t.cgu, 2 * Fp, t.dh, Fp, M, D.F, Fp, t.dgu, t.hb, s));
+  VLA_CK(launch_transpose_frag(w.wgu, false, d, 2 * Fp, d, 2 * Fp, t.wt, s));
+  VLA_CK(gemm_f32(t.dgu, 2 * Fp, t.wt, 2 * Fp, M, d, Fg, t.du, d, s));
+  VLA_CK(launch_rmsnorm_bwd(t.xm, w.mlp_norm, eps, t.du, t.dx, t.dxm, t.dxmf, M, d, s));
+  // attention: do = dxm Wo, attention backward, du1 = d[q; k; v] Wqkv
+  VLA_CK(launch_transpose_frag(w.wo, false, d, d, d, d, t.wt, s));
+  VLA_CK(gemm_f32(t.dxmf, 0, t.wt, 0, M, d, d, t.dob, d, s));
+  AttnBwdArgs ab{m->q, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
+                 m->scale, m->rope, t.stats, t.dqkv};
+  VLA_CK(launch_attn_bwd(ab, s));
+  VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
+  VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
+  // LoRA gradients: dW^T = X^T dY on the GEMM, then dA = s B^T dW, dB = s dW A^T
+  auto adapted = [&](int p) { return lora->a[l * 7 + p] != nullptr; };
+  auto grad = [&](int p, int ldw, int o0, int n_cols, int in, int out, int mode, int part) {
+    LoraGradArgs la{t.dwt, ldw, o0, n_cols, in, out, mode, D.hd, part,
+                    static_cast<const bf16_t*>(lora->a[l * 7 + p]), static_cast<const bf16_t*>(lora->b[l * 7 + p]),
+                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p]};
+    return launch_lora_grad(la, s);
+  };
+  if (adapted(VLA_PROJ_Q) || adapted(VLA_PROJ_K) || adapted(VLA_PROJ_V)) {
+    VLA_CK(launch_transpose_frag(t.u1, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(t.dqkv, false, 3 * d, M, 3 * d, Mk, t.dyt, s));
+    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, 3 * d, Mk, t.dwt, 3 * d, s));
+    for (int p = VLA_PROJ_Q; p <= VLA_PROJ_V; ++p)
+      if (adapted(p)) VLA_CK(grad(p, 3 * d, p * d, d, d, d, p == VLA_PROJ_V ? kPackRows : kPackQk, 0));
+  }
+  if (adapted(VLA_PROJ_O)) {
+    VLA_CK(launch_transpose_frag(t.ob, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(t.dxm, true, d, M, d, Mk, t.dyt, s));
+    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, d, Mk, t.dwt, d, s));
+    VLA_CK(grad(VLA_PROJ_O, d, 0, d, d, d, kPackRows, 0));
+  }
+  if (adapted(VLA_PROJ_GATE) || adapted(VLA_PROJ_UP)) {
+    VLA_CK(launch_transpose_frag(t.u2, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(t.dgu, false, 2 * Fp, M, Fg, Mk, t.dyt, s));
+    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, Fg, Mk, t.dwt, 2 * Fp, s));
+    if (adapted(VLA_PROJ_GATE)) VLA_CK(grad(VLA_PROJ_GATE, 2 * Fp, 0, Fg, d, D.F, kPackGateUp, 0));
+    if (adapted(VLA_PROJ_UP)) VLA_CK(grad(VLA_PROJ_UP, 2 * Fp, 0, Fg, d, D.F, kPackGateUp, 1));
+  }
+  if (adapted(VLA_PROJ_DOWN)) {
+    VLA_CK(launch_transpose_frag(t.hb, false, Fp, M, D.F, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(t.dxf, false, d, M, d, Mk, t.dyt, s));
+    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, D.F, d, Mk, t.dwt, d, s));
+    VLA_CK(grad(VLA_PROJ_DOWN, d, 0, d, D.F, d, kPackRows, 0));
+  }
+  // dL/d(layer input) = dxm + RMSNorm backward of du1
+  VLA_CK(launch_rmsnorm_bwd(t.xs[l], w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
   return VLA_OK;
 }
 
@@ -703,6 +841,81 @@ int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* 
   }
   if (a.src_cols % 8 != 0) return fail(VLA_EUNSUPPORTED, "input features must be a multiple of 8");
   VLA_CK(launch_lora_merge(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_train_workspace_size(const vla_config* cfg, size_t* bytes) {
+  Dims D;
+  int rc = check_config(cfg, &D);
+  if (rc) return rc;
+  if (!bytes) return fail(VLA_EINVAL, "bytes_host is NULL");
+  Layout L;
+  TrainBufs t;
+  plan_train(L, D, t);
+  *bytes = L.off;
+  return VLA_OK;
+}
+
+int vla_ppo_lora_grads(vla_model* m, int32_t B, const void* vis, const int32_t* ids, const int32_t* lens_host,
+                       const int32_t* actions, const float* logp_old, const float* advantages, float eps, float T,
+                       const vla_lora* lora, void* train_ws, size_t train_bytes, float* stats, float* logp_new,
+                       void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  const Dims& D = m->D;
+  if (B < 1) return fail(VLA_EINVAL, "batch must be >= 1");
+  if (B > D.Bmax) return fail(VLA_ESHAPE, "batch > max_batch");
+  if (!lens_host || !actions || !logp_old || !advantages || !lora || !stats || !train_ws || (D.nvis > 0 && !vis))
+    return fail(VLA_EINVAL, "NULL argument");
+  if (!lora->a || !lora->b || !lora->grad_a || !lora->grad_b) return fail(VLA_EINVAL, "NULL adapter array");
+  if (lora->rank < 1 || lora->rank > 64) return fail(VLA_EUNSUPPORTED, "rank must be in [1, 64]");
+  if (!std::isfinite(lora->scale)) return fail(VLA_EINVAL, "scale must be finite");
+  for (int i = 0; i < D.L * 7; ++i)
+    if (lora->a[i] && (!lora->b[i] || !lora->grad_a[i] || !lora->grad_b[i]))
+      return fail(VLA_EINVAL, "an adapted projection needs B and both gradient buffers");
+  if (!(T > 0.f) || !std::isfinite(T)) return fail(VLA_EINVAL, "temperature must be finite and > 0");
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(VLA_EINVAL, "eps must be finite and >= 0");
+  if (m->layer_limit != 0) return fail(VLA_ESTATE, "a debug layer limit is set");
+  if (reinterpret_cast<uintptr_t>(train_ws) % 256 != 0) return fail(VLA_EWORKSPACE, "training workspace misaligned");
+  Layout L;
+  L.base = static_cast<char*>(train_ws);
+  TrainBufs t;
+  plan_train(L, D, t);
+  if (train_bytes < L.off) return fail(VLA_EWORKSPACE, "training workspace smaller than vla_train_workspace_size()");
+  long long np = 0;
+  for (int b = 0; b < B; ++b) np += lens_host[b];
+  if (np > 0 && !ids) return fail(VLA_EINVAL, "prompt_ids is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  m->state_valid = false;
+  // teacher-forced forward, every layer's input saved
+  int R = 0, M = 0;
+  int rc = forward(m, B, vis, ids, lens_host, actions, s, &R, t.xs.data(), &M);
+  if (rc) return rc;
+  rc = head_logits(m, m->u_head, R, m->logits_tf, s);
+  if (rc) return rc;
+  SamplerArgs sa{};
+  sa.z = m->logits_tf; sa.A = D.A; sa.temperature = T; sa.gumbel = nullptr; sa.given = actions;
+  sa.action_begin = m->cfg.action_begin; sa.logp = t.logp; sa.rows = R; sa.flags = m->flags;
+  VLA_CK(launch_sampler(sa, s));
+  if (logp_new) VLA_CK(hipMemcpyAsync(logp_new, t.logp, (size_t)R * sizeof(float), hipMemcpyDeviceToDevice, s));
+  // loss and its gradient down to the action logits
+  PpoArgs pp{t.logp, logp_old, advantages, B, D.nact, eps, stats, t.dlogp};
+  VLA_CK(launch_ppo_clip(pp, s));
+  LogprobBwdArgs lb{m->logits_tf, actions, t.dlogp, R, D.A, m->cfg.action_begin, T, t.dz};
+  VLA_CK(launch_logprob_backward(lb, s));
+  // head (the action rows of the LM head) and final RMSNorm of the scoring rows
+  const int A32 = round_up(D.A, 32);
+  VLA_CK(launch_to_frag(t.dz, D.A, R, D.A, A32, t.dzf, s));
+  VLA_CK(launch_transpose_frag(m->lm_act, false, D.d, D.A, D.d, A32, t.wact_t, s));
+  VLA_CK(gemm_f32(t.dzf, 0, t.wact_t, 0, R, D.d, A32, t.du_h, D.d, s));
+  VLA_CK(launch_move_rows(m->x, m->head_rows, R, D.d, t.xc, false, s));
+  VLA_CK(launch_rmsnorm_bwd(t.xc, m->final_norm, m->cfg.rms_eps, t.du_h, nullptr, t.dxc, nullptr, R, D.d, s));
+  VLA_CK(launch_fill_zero(t.dx, (size_t)M * D.d * sizeof(float), s));
+  VLA_CK(launch_move_rows(t.dxc, m->head_rows, R, D.d, t.dx, true, s));
+  for (int l = D.L - 1; l >= 0; --l) {
+    rc = layer_backward(m, t, l, B, M, lora, s);
+    if (rc) return rc;
+  }
   g_err.clear();
   return VLA_OK;
 }

@@ -24,7 +24,8 @@ FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
            "vla_value", "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
-           "vla_last_error", "vla_extract_actions", "vla_gae", "vla_ppo_clip", "vla_logprob_backward")
+           "vla_last_error", "vla_extract_actions", "vla_gae", "vla_ppo_clip", "vla_logprob_backward",
+           "vla_train_workspace_size", "vla_ppo_lora_grads")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
@@ -53,6 +54,11 @@ class _Weights(ctypes.Structure):
                [(n, _PP) for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wgate", "wup", "wdown")]
 
 
+class _Lora(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("scale", ctypes.c_float), ("a", _PP), ("b", _PP), ("grad_a", _PP),
+                ("grad_b", _PP)]
+
+
 _lib = None
 
 
@@ -75,6 +81,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.vla_extract_actions.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, vp]
+    lib.vla_train_workspace_size.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(ctypes.c_size_t)]
+    lib.vla_ppo_lora_grads.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, ctypes.POINTER(_Lora), vp,
+                                       ctypes.c_size_t, vp, vp, vp]
     lib.vla_gae.argtypes = [i32, i32, vp, vp, vp, f32, f32, vp, vp, vp]
     lib.vla_ppo_clip.argtypes = [i32, i32, vp, vp, vp, f32, vp, vp, vp]
     lib.vla_logprob_backward.argtypes = [i32, i32, i32, vp, vp, f32, vp, vp, vp]
@@ -219,6 +228,49 @@ class VlaModel:
             assert t.dtype == torch.bfloat16 and t.is_contiguous() and t.is_cuda
         _check(self.lib.vla_lora_merge(self.handle, layer, PROJECTIONS.index(projection), _ptr(w0), _ptr(lora_a),
                                        _ptr(lora_b), rank, float(scale), _stream(self.device)))
+
+    def ppo_lora_grads(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
+                       actions: torch.Tensor, logp_old: torch.Tensor, advantages: torch.Tensor, eps: float,
+                       temperature: float, adapters, scale: float):
+        """Gradients of the PPO-clip loss w.r.t. the LoRA factors (vla_ppo_lora_grads).
+        adapters: per layer {projection key: (A [r, in], B [out, r])} bf16 device tensors
+        (layers or keys absent: not adapted).  Returns (stats [loss, clipped fraction],
+        logp_new [batch, n_actions], grads: per layer {key: (dA, dB)})."""
+        lens = np.ascontiguousarray(prompt_lens, dtype=np.int32)
+        B = int(lens.shape[0])
+        L = self.cfg.n_layers
+        if getattr(self, "_train_ws", None) is None:
+            n = ctypes.c_size_t()
+            _check(self.lib.vla_train_workspace_size(ctypes.byref(self.c_cfg), ctypes.byref(n)))
+            self._train_ws = torch.empty(n.value, dtype=torch.uint8, device=self.device)
+        ranks = {int(a.shape[0]) for ad in adapters for a, _ in ad.values()}
+        assert len(ranks) == 1, "one rank for every adapter"
+        rank = ranks.pop()
+        arr = [[None] * (L * 7) for _ in range(4)]
+        grads = [dict() for _ in range(L)]
+        for li, ad in enumerate(adapters):
+            for key, (a, b) in ad.items():
+                p = PROJECTIONS.index(key)
+                for t in (a, b):
+                    assert t.dtype == torch.bfloat16 and t.is_contiguous() and t.is_cuda
+                ga = torch.empty(a.shape, dtype=torch.float32, device=self.device)
+                gb = torch.empty(b.shape, dtype=torch.float32, device=self.device)
+                grads[li][key] = (ga, gb)
+                for j, t in enumerate((a, b, ga, gb)):
+                    arr[j][li * 7 + p] = t.data_ptr()
+        ptrs = [(ctypes.c_void_p * (L * 7))(*arr[j]) for j in range(4)]
+        lora = _Lora(rank, float(scale), *[ctypes.cast(p, _PP) for p in ptrs])
+        stats = torch.empty(2, dtype=torch.float32, device=self.device)
+        logp_new = torch.empty(B, self.cfg.n_actions, dtype=torch.float32, device=self.device)
+        for t, name in ((logp_old, "logp_old"), (advantages, "advantages")):
+            if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous fp32 device tensor")
+        _check(self.lib.vla_ppo_lora_grads(self.handle, B, _ptr(vis), _ptr(prompt_ids),
+                                           lens.ctypes.data_as(ctypes.c_void_p), _ptr(actions), _ptr(logp_old),
+                                           _ptr(advantages), float(eps), float(temperature), ctypes.byref(lora),
+                                           _ptr(self._train_ws), self._train_ws.numel(), _ptr(stats), _ptr(logp_new),
+                                           _stream(self.device)))
+        return stats, logp_new, grads
 
     def read_flags(self) -> int:
         v = ctypes.c_uint32()

@@ -1,0 +1,134 @@
+"""Parity of the backward of the teacher-forced pass (the PPO update's
+gradient, Eq. 2 and Sec. 3.3 Learning Phase) with the CPU oracle: the loss,
+the teacher-forced log-probs and the gradients of every LoRA factor of every
+adapted projection, through the head, the final RMSNorm and every decoder
+block (SwiGLU, RMSNorm, causal attention with rotary embedding)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import Setup, log
+from oracle import learn_oracle as lo
+from paper_2505_18719_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+PROJ = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
+
+
+def _case(cfg, seed, rank=8, std=0.05, scale=0.5, layers_adapted=None, keys=PROJ):
+    S = Setup(cfg, seed=seed)
+    L = cfg.n_layers
+    full = inputs.make_lora(cfg, rank, seed=seed, device="cuda", std=std)
+    layers_adapted = range(L) if layers_adapted is None else layers_adapted
+    ad = [{k: full[li][k] for k in keys} if li in layers_adapted else {} for li in range(L)]
+    for li, layer in enumerate(ad):
+        for k, (a, b) in layer.items():
+            rp = (rank + 7) // 8 * 8  # the merge takes ranks in multiples of 8: zero rows of A, columns of B
+            ap = torch.zeros(rp, a.shape[1], dtype=a.dtype, device=a.device)
+            bp = torch.zeros(b.shape[0], rp, dtype=b.dtype, device=b.device)
+            ap[:rank], bp[:, :rank] = a, b
+            S.model.lora_merge(li, k, S.w["layers"][li][k], ap, bp.contiguous(), scale)
+    inp, dev = S.inputs(seed=seed)
+    B, T, eps = inp.batch, 1.5, 0.2
+    acts = torch.from_numpy(inputs.stored_actions(cfg, B, seed=seed)).cuda()
+    tf = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, T)
+    rng = np.random.default_rng(seed)
+    old = tf["logp"].cpu().numpy() + rng.normal(scale=0.03, size=(B, cfg.n_actions))
+    adv = inputs.ppo_minibatch(B, seed=seed)[2]
+    old[0] += -0.3 if adv[0] > 0 else 0.3  # action 0 clipped
+    logp_old = torch.from_numpy(old.astype(np.float32)).cuda()
+    advt = torch.from_numpy(adv).cuda()
+    stats, lp_new, grads = S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, logp_old, advt,
+                                                  eps, T, ad, scale)
+    torch.cuda.synchronize()
+    adc = [{k: (a.cpu(), b.cpu()) for k, (a, b) in layer.items()} for layer in ad]
+    args = (cfg, S.wc, adc, scale, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, acts.cpu().numpy(),
+            logp_old.cpu().numpy(), adv, eps, T)
+    ref = lo.ppo_lora_grads(*args, mode="bf16")
+    ideal = lo.ppo_lora_grads(*args, mode="ideal")
+    # how far the bf16 contract alone moves the oracle: the scale of any bf16 implementation's error
+    ref["gap_logp"] = float(np.abs(ref["logp"] - ideal["logp"]).max())
+    ref["gap_grad"] = max(np.linalg.norm(ref["grads"][li][k][f] - ideal["grads"][li][k][f])
+                          / np.linalg.norm(ideal["grads"][li][k][f])
+                          for li in range(cfg.n_layers) for k in ref["grads"][li] for f in (0, 1))
+    S.model.close()
+    return stats.cpu().numpy(), lp_new.cpu().numpy(), grads, ref
+
+
+def _errors(grads, ref):
+    out = {}
+    for li, layer in enumerate(grads):
+        for k, (ga, gb) in layer.items():
+            for f, g in enumerate((ga, gb)):
+                r = ref["grads"][li][k][f]
+                g = g.cpu().double().numpy()
+                out[(li, k, "AB"[f])] = (np.linalg.norm(g - r) / np.linalg.norm(r), np.abs(g - r).max() / np.abs(r).max())
+    return out
+
+
+# Gradient tolerance: the backward rounds its GEMM operands (activations and
+# gradients) to bf16 and accumulates in fp32, against the oracle's exact chain
+# rule through the same bf16-rounded forward; each layer the gradient crosses
+# adds about one bf16 unit (2^-8) of relative error, so the bar on a tensor's
+# relative error is (n_layers + 1) 2^-8 of its norm (1.5 times that for its
+# largest entry), or twice the distance between the oracle's own bf16 and fp64
+# gradients where that is larger (the wide 7B-width sums).  The log-probs use
+# the stated 1e-2, or twice the oracle's bf16-vs-fp64 gap where larger, as the
+# forward tests at full width do.
+def _grad_tol(n_layers, gap):
+    unit = (n_layers + 1) * 2.0 ** -8
+    return max(unit, 2 * gap), 1.5 * max(unit, 2 * gap)
+
+
+def _check(label, stats, lp, grads, ref, adv, n_layers):
+    dlp = np.abs(lp - ref["logp"]).max()
+    # the loss moves with the teacher-forced log-probs: rho changes by at most
+    # n_actions * max|dlogp| in its exponent
+    na = lp.shape[1]
+    bound = np.mean(np.abs(adv)) * 1.3 * (np.expm1(na * dlp) + 1e-6) + 1e-6
+    log(f"[{label}] loss gpu {stats[0]:.6f} oracle {ref['loss']:.6f} (bound {bound:.1e}); clipped {stats[1]:.3f} "
+        f"vs {ref['clip_frac']:.3f}; max|dlogp| {dlp:.2e}")
+    errs = _errors(grads, ref)
+    worst_n = max(v[0] for v in errs.values())
+    worst_m = max(v[1] for v in errs.values())
+    log(f"[{label}] {len(errs)} gradient tensors: worst relative-norm error {worst_n:.3e}, relative-max {worst_m:.3e}")
+    log(f"[{label}] oracle bf16-vs-fp64 gap: log-probs {ref['gap_logp']:.2e}, gradients {ref['gap_grad']:.2e}")
+    assert dlp <= max(1e-2, 2 * ref["gap_logp"])
+    n = len(adv)
+    assert round(float(stats[1]) * n) == round(ref["clip_frac"] * n)  # the same actions clipped
+    assert abs(stats[0] - ref["loss"]) <= bound
+    tol_n, tol_m = _grad_tol(n_layers, ref["gap_grad"])
+    assert worst_n <= tol_n and worst_m <= tol_m
+
+
+def test_tiny_lora_gradients_match_oracle():
+    """Both layers, all seven projections, rank 8, ragged prompts (empty ones included)."""
+    cfg = inputs.TINY.replace(name="tiny_bwd", batch=4, prompt_min=0, prompt_max=16)
+    stats, lp, grads, ref = _case(cfg, seed=41)
+    _check("tiny bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=41)[2], cfg.n_layers)
+
+
+def test_partial_adapters_and_odd_rank():
+    """Adapters on the last layer's q, v and down projections only, rank 5: the
+    other projections get no gradient buffers and the backward still runs
+    through every layer."""
+    cfg = inputs.TINY.replace(name="tiny_bwd_partial", batch=3, prompt_min=4, prompt_max=12)
+    stats, lp, grads, ref = _case(cfg, seed=43, rank=5, layers_adapted=[cfg.n_layers - 1], keys=("wq", "wv", "wdown"))
+    assert all(not g for g in grads[:-1]) and set(grads[-1]) == {"wq", "wv", "wdown"}
+    _check("tiny bwd partial", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=43)[2], cfg.n_layers)
+
+
+def test_mid_lora_gradients_match_oracle():
+    """Mid decoder (8 layers, d 1024, 16 heads): the gradient through eight layers."""
+    cfg = inputs.MID.replace(batch=2)
+    stats, lp, grads, ref = _case(cfg, seed=44, std=0.02)
+    _check("mid bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=44)[2], cfg.n_layers)
+
+
+def test_7b_width_two_layers_lora_gradients_match_oracle():
+    """OpenVLA-7B width (d 4096, 32 heads of 128, FFN 11008), two layers, two
+    environments: the head_dim-128 attention backward and the full-size GEMMs."""
+    cfg = inputs.L7B_B8.replace(n_layers=2, batch=2)
+    stats, lp, grads, ref = _case(cfg, seed=45, std=0.01)
+    _check("7b-width 2L bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=45)[2], cfg.n_layers)

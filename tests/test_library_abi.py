@@ -113,3 +113,17 @@ def test_extract_actions_validates_on_the_host(vla):
     assert lib.vla_extract_actions(4, 7, p, 0, 300, p, p, p, None) == -7
     assert lib.vla_extract_actions(4, 7, p, 0, 256, None, p, p, None) == -1
     assert lib.vla_extract_actions(0, 7, None, 0, 256, None, None, None, None) == 0
+
+
+def test_lora_gradient_entry_validates_on_the_host(vla):
+    """vla_ppo_lora_grads rejects a NULL model, bad batch, rank, parameters and a
+    missing workspace before any device work."""
+    lib = vla.load_library()
+    p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    lora = vla._Lora(8, 0.5, None, None, None, None)
+    assert lib.vla_ppo_lora_grads(None, 1, p, p, p, p, p, p, 0.2, 1.5, ctypes.byref(lora), p, 1, p, None, None) == -1
+    assert b"model is NULL" in lib.vla_last_error()
+    n = ctypes.c_size_t()
+    c = vla.make_config(inputs.TINY)
+    assert lib.vla_train_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0
+    assert lib.vla_train_workspace_size(None, ctypes.byref(n)) == -1
