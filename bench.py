@@ -185,6 +185,7 @@ def main():
     ap.add_argument("--no-value", action="store_true")
     ap.add_argument("--no-learning", action="store_true")
     ap.add_argument("--no-lora-merge", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain streaming kernel of known size before timing (HBM counter calibration)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -448,6 +449,28 @@ def main():
                                 "unit": "GB/s", "frac": merge_bytes / (merge_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
                                 "bytes": merge_bytes}
         log(f"[bench] LoRA merge of all {7 * L} projections: {merge_ms:.2f} ms")
+
+    if not args.no_lora_merge and not args.no_backward:
+        # PPO update gradient (Eq. 2 through the teacher-forced pass) w.r.t. the
+        # rank-32 adapters just merged, over the same batch with stored actions
+        inp, ids, _ = sets[0]
+        acts = torch.from_numpy(I.stored_actions(cfg, B, seed=0)).to(dev)
+        old = model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)["logp"].contiguous()
+        adv_b = torch.from_numpy(I.ppo_minibatch(B, seed=0)[2]).to(dev)
+        model.ppo_lora_grads(inp.vis, ids, inp.prompt_lens, acts, old, adv_b, 0.2, T, adapters, 0.5)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st_b, _, _ = model.ppo_lora_grads(inp.vis, ids, inp.prompt_lens, acts, old, adv_b, 0.2, T, adapters, 0.5)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        bwd_ms = e0.elapsed_time(e1)
+        Lt = inp.prefix_lens.astype(np.float64) + cfg.n_actions
+        fwd = 2 * layer_params * L * Lt.sum() + 2 * d * L * (Lt * (Lt + 1)).sum()
+        result["lora_backward"] = {"ms": bwd_ms, "rows": int(Lt.sum()), "projections": 7 * L, "rank": 32,
+                                   "mfma_frac": 3 * fwd / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                   "loss": float(st_b[0])}
+        log(f"[bench] PPO LoRA gradient (teacher-forced pass + backward): {bwd_ms:.1f} ms")
 
     if not args.no_cpu_baseline:
         log(f"[bench] oracle CPU baseline ({args.cpu_layers} layers of one environment)")

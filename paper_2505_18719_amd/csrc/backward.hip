@@ -297,6 +297,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_q_kernel(AttnBwdArgs a) {
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
       const int jend = min(t + 1, 64 * (i + 1));
+#pragma unroll 8
       for (int j = 64 * i; j < jend; ++j) {
         const float ds = __builtin_amdgcn_readlane(__float_as_int(dpv[i]), j - 64 * i);
 #pragma unroll
@@ -368,6 +369,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_kernel(AttnBwdArgs a) {
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
       const int tend = min(L, j + 64 * (i + 1));
+#pragma unroll 8
       for (int t = j + 64 * i; t < tend; ++t) {
         const float ds = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsv[i]), t - j - 64 * i));
         const float p = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pv[i]), t - j - 64 * i));
@@ -402,17 +404,21 @@ __device__ __forceinline__ int grad_row(const LoraGradArgs& a, int o) {
   return (j >= 0 && (a.mode != kPackGateUp || part == a.part)) ? j : -1;
 }
 
+constexpr int kLoraChunk = 512;  // reduction chunk of one workgroup (partials summed in chunk order)
+
+// partial dA over output columns [chunk * 512, +512): part[chunk][c][i]
 __global__ __launch_bounds__(256) void lora_da_kernel(LoraGradArgs a) {
   __shared__ float ws[64][33];  // dwt[i0 + ii, o]
   __shared__ float bs[32][65];  // B[grad_row(o), c]
   const int i0 = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  const int o_beg = blockIdx.y * kLoraChunk, o_end = min(a.n_cols, o_beg + kLoraChunk);
   float acc[4][4] = {};
-  for (int ob = 0; ob < a.n_cols; ob += 32) {
+  for (int ob = o_beg; ob < o_end; ob += 32) {
     for (int e = tid; e < 64 * 32; e += 256) {
       const int ii = e / 32, oo = e % 32;
-      ws[ii][oo] = (i0 + ii < a.in && ob + oo < a.n_cols) ? a.dwt[(size_t)(i0 + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
+      ws[ii][oo] = (i0 + ii < a.in && ob + oo < o_end) ? a.dwt[(size_t)(i0 + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
       const int c = e % 64, o2 = e / 64;
-      const int nr = ob + o2 < a.n_cols ? grad_row(a, ob + o2) : -1;
+      const int nr = ob + o2 < o_end ? grad_row(a, ob + o2) : -1;
       bs[o2][c] = (nr >= 0 && c < a.r) ? bf2f(a.b[(size_t)nr * a.r + c]) : 0.f;
     }
     __syncthreads();
@@ -424,26 +430,29 @@ __global__ __launch_bounds__(256) void lora_da_kernel(LoraGradArgs a) {
         for (int v = 0; v < 4; ++v) acc[u][v] += ws[ty * 4 + u][oo] * bs[oo][tx * 4 + v];
     __syncthreads();
   }
+  float* part = a.scratch + (size_t)blockIdx.y * 64 * a.in;
 #pragma unroll
   for (int u = 0; u < 4; ++u)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int i = i0 + ty * 4 + u, c = tx * 4 + v;
-      if (i < a.in && c < a.r) a.da[(size_t)c * a.in + i] = a.scale * acc[u][v];
+      if (i < a.in) part[(size_t)c * a.in + i] = acc[u][v];
     }
 }
 
+// partial dB^T over input features [chunk * 512, +512): part[chunk][c][o]
 __global__ __launch_bounds__(256) void lora_db_kernel(LoraGradArgs a) {
   __shared__ float ws[32][65];  // dwt[i, o0 + ob + oo]
   __shared__ float as[32][65];  // A[c, i]
   const int ob = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  const int i_beg = blockIdx.y * kLoraChunk, i_end = min(a.in, i_beg + kLoraChunk);
   float acc[4][4] = {};
-  for (int ib = 0; ib < a.in; ib += 32) {
+  for (int ib = i_beg; ib < i_end; ib += 32) {
     for (int e = tid; e < 32 * 64; e += 256) {
       const int ii = e / 64, oo = e % 64;
-      ws[ii][oo] = (ib + ii < a.in && ob + oo < a.n_cols) ? a.dwt[(size_t)(ib + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
+      ws[ii][oo] = (ib + ii < i_end && ob + oo < a.n_cols) ? a.dwt[(size_t)(ib + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
       const int c = e % 64, i2 = e / 64;
-      as[i2][c] = (c < a.r && ib + i2 < a.in) ? bf2f(a.a[(size_t)c * a.in + ib + i2]) : 0.f;
+      as[i2][c] = (c < a.r && ib + i2 < i_end) ? bf2f(a.a[(size_t)c * a.in + ib + i2]) : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
@@ -454,17 +463,35 @@ __global__ __launch_bounds__(256) void lora_db_kernel(LoraGradArgs a) {
         for (int v = 0; v < 4; ++v) acc[u][v] += ws[ii][ty * 4 + u] * as[ii][tx * 4 + v];
     __syncthreads();
   }
+  float* part = a.scratch + (size_t)blockIdx.y * 64 * a.n_cols;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int o = ob + ty * 4 + u;
-    const int nr = o < a.n_cols ? grad_row(a, o) : -1;
-    if (nr < 0) continue;
+  for (int u = 0; u < 4; ++u)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int c = tx * 4 + v;
-      if (c < a.r) a.db[(size_t)nr * a.r + c] = a.scale * acc[u][v];
+      const int o = ob + ty * 4 + u, c = tx * 4 + v;
+      if (o < a.n_cols) part[(size_t)c * a.n_cols + o] = acc[u][v];
     }
-  }
+}
+
+// dA[c, i] = s sum_chunks part[chunk][c][i]
+__global__ void lora_da_reduce_kernel(LoraGradArgs a, int chunks) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= a.r * a.in) return;
+  float v = 0.f;
+  for (int k = 0; k < chunks; ++k) v += a.scratch[(size_t)k * 64 * a.in + e];
+  a.da[e] = a.scale * v;
+}
+
+// dB[grad_row(o), c] = s sum_chunks part[chunk][c][o]
+__global__ void lora_db_reduce_kernel(LoraGradArgs a, int chunks) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= a.r * a.n_cols) return;
+  const int c = e / a.n_cols, o = e % a.n_cols;
+  const int nr = grad_row(a, o);
+  if (nr < 0) return;
+  float v = 0.f;
+  for (int k = 0; k < chunks; ++k) v += a.scratch[(size_t)k * 64 * a.n_cols + (size_t)c * a.n_cols + o];
+  a.db[(size_t)nr * a.r + c] = a.scale * v;
 }
 
 // dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), fp32 rows of d
@@ -480,10 +507,19 @@ __global__ void move_rows_kernel(const float* __restrict__ src, const int32_t* _
 
 }  // namespace
 
+size_t lora_grad_part_floats(int in, int n_cols) {
+  const size_t ca = (size_t)((n_cols + kLoraChunk - 1) / kLoraChunk) * 64 * in;
+  const size_t cb = (size_t)((in + kLoraChunk - 1) / kLoraChunk) * 64 * n_cols;
+  return ca > cb ? ca : cb;
+}
+
 hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s) {
   if (a.r < 1 || a.r > 64 || a.in <= 0 || a.n_cols <= 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(lora_da_kernel, dim3((a.in + 63) / 64), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(lora_db_kernel, dim3((a.n_cols + 63) / 64), dim3(256), 0, s, a);
+  const int ca = (a.n_cols + kLoraChunk - 1) / kLoraChunk, cb = (a.in + kLoraChunk - 1) / kLoraChunk;
+  hipLaunchKernelGGL(lora_da_kernel, dim3((a.in + 63) / 64, ca), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(lora_da_reduce_kernel, dim3((a.r * a.in + 255) / 256), dim3(256), 0, s, a, ca);
+  hipLaunchKernelGGL(lora_db_kernel, dim3((a.n_cols + 63) / 64, cb), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(lora_db_reduce_kernel, dim3((a.r * a.n_cols + 255) / 256), dim3(256), 0, s, a, cb);
   return hipGetLastError();
 }
 

@@ -327,7 +327,9 @@ struct LoraGradArgs {
   float scale;
   float* da;
   float* db;
+  float* scratch;    // lora_grad_part_floats(in, n_cols) floats of partial sums
 };
+size_t lora_grad_part_floats(int in, int n_cols);
 hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s);
 // fp32 rows of d: dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), i < R
 hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d, float* dst, bool scatter,

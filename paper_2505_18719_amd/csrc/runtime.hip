@@ -405,7 +405,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
 // Buffers of the caller's training workspace.
 struct TrainBufs {
   std::vector<float*> xs;  // per-layer input residual [Mmax, d]
-  float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *dwt, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp;
+  float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *dwt, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp, *lpart;
   bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t;
 };
 
@@ -424,6 +424,8 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   t.dh = L.take<float>(Mx * D.Fp);
   t.dwt = L.take<float>(std::max(d * 3 * d, std::max(d * 2 * D.Fp, (size_t)D.Fp * d)));
   t.stats = L.take<float>(Mx * D.H * 2);
+  const int Fg = 64 * ((D.F + 31) / 32);
+  t.lpart = L.take<float>(std::max(lora_grad_part_floats(D.d, std::max(D.d, Fg)), lora_grad_part_floats(D.F, D.d)));
   t.dz = L.take<float>(Rh * D.A);
   t.du_h = L.take<float>(Rh * d);
   t.xc = L.take<float>(Rh * d);
@@ -500,7 +502,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   auto grad = [&](int p, int ldw, int o0, int n_cols, int in, int out, int mode, int part) {
     LoraGradArgs la{t.dwt, ldw, o0, n_cols, in, out, mode, D.hd, part,
                     static_cast<const bf16_t*>(lora->a[l * 7 + p]), static_cast<const bf16_t*>(lora->b[l * 7 + p]),
-                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p]};
+                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p], t.lpart};
     return launch_lora_grad(la, s);
   };
   if (adapted(VLA_PROJ_Q) || adapted(VLA_PROJ_K) || adapted(VLA_PROJ_V)) {
