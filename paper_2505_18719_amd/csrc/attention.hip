@@ -108,6 +108,7 @@ __device__ __forceinline__ void attn_tile(const PrefillAttnArgs& a, const char* 
     }
   sum += __shfl_xor(sum, 16, kWave);
   sum += __shfl_xor(sum, 32, kWave);
+  if (a.lse && g == 0 && qpos < L) a.lse[((size_t)(row0 + qpos) * a.n_heads + head) * 2] = mx + logf(sum);
 
   // O^T = V^T P^T: A operand = V^T rows (feature nb*16 + r16), keys 32c + 8g .. +8,
   // i.e. page 2c + g/2, half g%2; (f >> 3) & 1 of feature 16nb + r16 is r16 >> 3

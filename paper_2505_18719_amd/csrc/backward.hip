@@ -156,24 +156,22 @@ __global__ void swiglu_bwd_kernel(const float* __restrict__ cgu, int ldc, const 
 }
 
 // ---- causal attention backward ------------------------------------------------
-// Per (environment, head) workgroup of 4 waves.  With P = softmax(scale q k^T)
-// (causal), dP = dO V^T, D_t = sum_j P_tj dP_tj and dS = P (dP - D):
-//   pass 1 (queries): dq_t = scale sum_j dS_tj k_j, and the row statistics
-//                     lse_t = log sum_j exp(scale q_t.k_j), D_t;
+// Per (environment, head) workgroup of 16 waves.  With P = softmax(scale q k^T)
+// (causal) given by the forward's log-sum-exp per query row (P = exp(scale
+// q.k - lse)), dP = dO V^T, D_t = dO_t . O_t and dS = P (dP - D):
+//   pass 1 (queries): D_t, and dq_t = scale sum_j dS_tj k_j;
 //   pass 2 (keys):    dk_j = scale sum_t dS_tj q_t, dv_j = sum_t P_tj dO_t.
-// q and k are the rotated values the forward attended with; the gradients are
-// taken back through the rotary embedding (the inverse rotation at each row's
-// position) and written as bf16 into the [q; k; v] gradient matrix in the
-// packed weight's column order (frag layout, K = 3 d).
+// A wave takes one row (query or key) at a time; its lanes hold 8 features
+// each, HD / 8 lanes per row of the other side, 512 / HD of those rows per step,
+// and reduce their partial dot products with shuffles.  q and k are the
+// rotated values the forward attended with; the gradients go back through the
+// inverse rotation at each row's position and are written as bf16 into the
+// [q; k; v] gradient in the packed weight's column order (frag layout, K = 3 d).
 constexpr int kBwdKeys = 320;  // longest sequence (one environment)
+constexpr int kBwdWaves = 16;
 
 template <int HD>
 __device__ __forceinline__ int bwd_swz(int row) { return row & (HD / 8 - 1); }
-// LDS element (row, f) of a [kBwdKeys, HD] bf16 tile whose 16-byte chunks are swizzled per row
-template <int HD>
-__device__ __forceinline__ int bwd_lds(int row, int f) {
-  return (row * (HD / 8) + ((f >> 3) ^ bwd_swz<HD>(row))) * 8 + (f & 7);
-}
 // packed column of natural feature f of a rotated head (q, k): pairs (i, i + HD/2) of each
 // 32-feature block sit 32 columns apart in 64-column groups
 template <int HD>
@@ -181,214 +179,177 @@ __device__ __forceinline__ int qk_packed_col(int f) {
   constexpr int half = HD / 2;
   return f < half ? 64 * (f >> 5) + (f & 31) : 64 * ((f - half) >> 5) + 32 + ((f - half) & 31);
 }
-
+// 16-byte chunk c of row `row` of a [kBwdKeys, HD] bf16 LDS tile (chunks swizzled per row)
 template <int HD>
-__device__ __forceinline__ void bwd_load_q_do(const AttnBwdArgs& a, int row, int head, float* q, float* dov) {
-  const bf16_t* qp = a.q + (size_t)row * a.d + head * HD;
-  const float* dp = a.dout + (size_t)row * a.d + head * HD;
+__device__ __forceinline__ void lds_chunk(const bf16_t* t, int row, int c, float* f8) {
+  unpack8(*reinterpret_cast<const uint4*>(t + (row * (HD / 8) + (c ^ bwd_swz<HD>(row))) * 8), f8);
+}
+template <int LPK>
+__device__ __forceinline__ float group_sum(float v) {
 #pragma unroll
-  for (int c = 0; c < HD / 8; ++c) {
-    float f8[8];
-    unpack8(*reinterpret_cast<const uint4*>(qp + 8 * c), f8);
+  for (int o = LPK / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+// sum over the 64 / LPK row groups of a wave (lanes with the same feature chunk)
+template <int LPK>
+__device__ __forceinline__ float across_groups(float v) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) q[8 * c + e] = f8[e];
-    const float4 x0 = *reinterpret_cast<const float4*>(dp + 8 * c);
-    const float4 x1 = *reinterpret_cast<const float4*>(dp + 8 * c + 4);
-    dov[8 * c + 0] = x0.x; dov[8 * c + 1] = x0.y; dov[8 * c + 2] = x0.z; dov[8 * c + 3] = x0.w;
-    dov[8 * c + 4] = x1.x; dov[8 * c + 5] = x1.y; dov[8 * c + 6] = x1.z; dov[8 * c + 7] = x1.w;
+  for (int o = LPK; o < 64; o <<= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+// write features 8c .. 8c + 7 of a q or k gradient back through the rotation; the
+// pair partner of chunk c is chunk c ^ (HD / 16), held by lane ^ (HD / 16)
+template <int HD>
+__device__ __forceinline__ void bwd_store_rot8(const AttnBwdArgs& a, int row, int pos, int head, int region, int c,
+                                               const float* g) {
+  constexpr int half = HD / 2, hc = HD / 16;
+  float out[8];
+  const bool first = c < hc;  // features below half
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float other = __shfl_xor(g[e], hc, kWave);
+    const int i = (first ? 8 * c : 8 * c - half) + e;  // rotary pair index
+    const float2 cs = a.rope[pos * half + i];
+    // (g1, g2) of pair i: g1 belongs to feature i, g2 to i + half
+    const float g1 = first ? g[e] : other, g2 = first ? other : g[e];
+    out[e] = first ? g1 * cs.x + g2 * cs.y : -g1 * cs.y + g2 * cs.x;
   }
-}
-
-// dot of a register row with LDS row `row` of tile t (bf16, swizzled chunks)
-template <int HD>
-__device__ __forceinline__ float bwd_dot(const bf16_t* t, int row, const float* v) {
-  float acc = 0.f;
+  const int base = region * a.d + head * HD, K3 = 3 * a.d;
 #pragma unroll
-  for (int c = 0; c < HD / 8; ++c) {
-    float f8[8];
-    unpack8(*reinterpret_cast<const uint4*>(t + (row * (HD / 8) + (c ^ bwd_swz<HD>(row))) * 8), f8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc += v[8 * c + e] * f8[e];
-  }
-  return acc;
-}
-
-// write the gradient of feature pair (f, f + HD/2) of row `row` (position pos) back
-// through the rotation, into region `region` (0 q, 1 k) of the [q; k; v] gradient
-template <int HD>
-__device__ __forceinline__ void bwd_store_rot(const AttnBwdArgs& a, int row, int pos, int head, int region, int f,
-                                              float g1, float g2) {
-  const float2 cs = a.rope[pos * (HD / 2) + f];
-  const float p1 = g1 * cs.x + g2 * cs.y, p2 = -g1 * cs.y + g2 * cs.x;
-  const int base = region * a.d + head * HD;
-  const int K3 = 3 * a.d;
-  a.dqkv[frag_index(row, base + qk_packed_col<HD>(f), K3)] = f2bf(p1);
-  a.dqkv[frag_index(row, base + qk_packed_col<HD>(f + HD / 2), K3)] = f2bf(p2);
+  for (int e = 0; e < 8; ++e) a.dqkv[frag_index(row, base + qk_packed_col<HD>(8 * c + e), K3)] = f2bf(out[e]);
 }
 
 template <int HD>
-__global__ __launch_bounds__(256, 1) void attn_bwd_q_kernel(AttnBwdArgs a) {
+__global__ __launch_bounds__(64 * kBwdWaves, 1) void attn_bwd_q_kernel(AttnBwdArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t ks[kBwdKeys * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs[kBwdKeys * HD];
-  constexpr int NS = kBwdKeys / 64;  // key slots per lane
+  constexpr int LPK = HD / 8, RPS = 64 / LPK;  // lanes per key row, key rows per step
   const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
   const int L = a.env_len[env], row0 = a.env_row0[env];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane % LPK, grp = lane / LPK;  // feature chunk, key slot of the step
   const int32_t* pt = a.page_table + env * a.max_pages;
   // K rows (key-major in the cache) and V (feature-major pages) into key-major LDS
-  for (int i = tid; i < L * (HD / 8); i += 256) {
-    const int j = i / (HD / 8), c = i % (HD / 8);
+  for (int i = tid; i < L * (HD / 8); i += 64 * kBwdWaves) {
+    const int j = i / (HD / 8), cc = i % (HD / 8);
     const int page = pt[j / kPage], slot = j % kPage;
-    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * c;
-    *reinterpret_cast<uint4*>(ks + (j * (HD / 8) + (c ^ bwd_swz<HD>(j))) * 8) = *reinterpret_cast<const uint4*>(kp);
-    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * c) * kPage + slot;
+    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * cc;
+    *reinterpret_cast<uint4*>(ks + (j * (HD / 8) + (cc ^ bwd_swz<HD>(j))) * 8) = *reinterpret_cast<const uint4*>(kp);
+    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * cc) * kPage + slot;
     bf16_t v8[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v8[e] = vp[e * kPage];
     uint4 o;
     o.x = v8[0] | (uint32_t(v8[1]) << 16); o.y = v8[2] | (uint32_t(v8[3]) << 16);
     o.z = v8[4] | (uint32_t(v8[5]) << 16); o.w = v8[6] | (uint32_t(v8[7]) << 16);
-    *reinterpret_cast<uint4*>(vs + (j * (HD / 8) + (c ^ bwd_swz<HD>(j))) * 8) = o;
+    *reinterpret_cast<uint4*>(vs + (j * (HD / 8) + (cc ^ bwd_swz<HD>(j))) * 8) = o;
   }
   __syncthreads();
-  for (int t = wave; t < L; t += 4) {
-    float q[HD], dov[HD];
-    bwd_load_q_do<HD>(a, row0 + t, head, q, dov);
-    float sv[NS], dpv[NS];
-    float m = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int j = lane + 64 * i;
-      sv[i] = -INFINITY;
-      dpv[i] = 0.f;
-      if (j <= t) {
-        sv[i] = a.scale * bwd_dot<HD>(ks, j, q);
-        dpv[i] = bwd_dot<HD>(vs, j, dov);
-      }
-      m = fmaxf(m, sv[i]);
-    }
-    m = wave_max(m);
-    float l = 0.f;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      sv[i] = lane + 64 * i <= t ? expf(sv[i] - m) : 0.f;
-      l += sv[i];
-    }
-    l = wave_sum(l);
-    const float inv = 1.f / l;
+  for (int t = wave; t < L; t += kBwdWaves) {
+    const int row = row0 + t;
+    float q8[8], do8[8], o8[8];
+    unpack8(*reinterpret_cast<const uint4*>(a.q + (size_t)row * a.d + head * HD + 8 * c), q8);
+    unpack8(*reinterpret_cast<const uint4*>(a.o + frag_index(row, head * HD + 8 * c, a.d)), o8);
+    const float* dp = a.dout + (size_t)row * a.d + head * HD + 8 * c;
     float dd = 0.f;
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      sv[i] *= inv;  // P
-      dd += sv[i] * dpv[i];
+    for (int e = 0; e < 8; ++e) {
+      do8[e] = bf2f(f2bf(dp[e]));  // dO as the bf16 operand it is in pass 2
+      dd += do8[e] * o8[e];
     }
-    dd = wave_sum(dd);
+    dd = group_sum<LPK>(dd);  // D_t = dO_t . O_t
+    float* st = a.stats + ((size_t)row * H + head) * 2;
+    const float lse = st[0];
+    if (lane == 0) st[1] = dd;
+    float dq[8] = {};
+    for (int j0 = 0; j0 <= t; j0 += RPS) {
+      const int j = j0 + grp;
+      const int jj = min(j, t);  // rows past t read a valid row and contribute 0
+      float k8[8], v8[8];
+      lds_chunk<HD>(ks, jj, c, k8);
+      lds_chunk<HD>(vs, jj, c, v8);
+      float sp = 0.f, dpv = 0.f;
 #pragma unroll
-    for (int i = 0; i < NS; ++i) dpv[i] = sv[i] * (dpv[i] - dd);  // dS
-    if (lane == 0) {
-      a.stats[((size_t)(row0 + t) * H + head) * 2] = m + logf(l);
-      a.stats[((size_t)(row0 + t) * H + head) * 2 + 1] = dd;
-    }
-    // dq over features f = lane (+ 64): dS_j is read from the lane holding key j
-    constexpr int FPL = HD / 64;  // features per lane
-    float dq[FPL];
-#pragma unroll
-    for (int u = 0; u < FPL; ++u) dq[u] = 0.f;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int jend = min(t + 1, 64 * (i + 1));
-#pragma unroll 8
-      for (int j = 64 * i; j < jend; ++j) {
-        const float ds = __builtin_amdgcn_readlane(__float_as_int(dpv[i]), j - 64 * i);
-#pragma unroll
-        for (int u = 0; u < FPL; ++u) dq[u] += __int_as_float(ds) * bf2f(ks[bwd_lds<HD>(j, lane + 64 * u)]);
+      for (int e = 0; e < 8; ++e) {
+        sp += q8[e] * k8[e];
+        dpv += do8[e] * v8[e];
       }
+      sp = group_sum<LPK>(sp);
+      dpv = group_sum<LPK>(dpv);
+      const float p = j <= t ? expf(a.scale * sp - lse) : 0.f;
+      const float ds = p * (dpv - dd);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dq[e] += ds * k8[e];
     }
-    // back through the rotation: pair (f, f + HD/2) is (lane, lane + 64) at HD 128, lanes f and f + 32 at HD 64
-    if (HD == 128) {
-      bwd_store_rot<HD>(a, row0 + t, t, head, 0, lane, a.scale * dq[0], a.scale * dq[FPL - 1]);
-    } else {
-      const float partner = __shfl_xor(dq[0], 32, kWave);
-      if (lane < 32) bwd_store_rot<HD>(a, row0 + t, t, head, 0, lane, a.scale * dq[0], a.scale * partner);
-    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dq[e] = a.scale * across_groups<LPK>(dq[e]);
+    if (grp == 0) bwd_store_rot8<HD>(a, row, t, head, 0, c, dq);
   }
 }
 
 template <int HD>
-__global__ __launch_bounds__(256, 1) void attn_bwd_kv_kernel(AttnBwdArgs a) {
+__global__ __launch_bounds__(64 * kBwdWaves, 1) void attn_bwd_kv_kernel(AttnBwdArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t qs[kBwdKeys * HD];
   __shared__ __attribute__((aligned(16))) bf16_t os[kBwdKeys * HD];  // dO rounded to bf16
-  constexpr int NS = kBwdKeys / 64;
+  constexpr int LPK = HD / 8, RPS = 64 / LPK;
   const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
   const int L = a.env_len[env], row0 = a.env_row0[env];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane % LPK, grp = lane / LPK;
   const int32_t* pt = a.page_table + env * a.max_pages;
-  for (int i = tid; i < L * (HD / 8); i += 256) {
-    const int t = i / (HD / 8), c = i % (HD / 8);
-    const int at = (t * (HD / 8) + (c ^ bwd_swz<HD>(t))) * 8;
+  for (int i = tid; i < L * (HD / 8); i += 64 * kBwdWaves) {
+    const int t = i / (HD / 8), cc = i % (HD / 8);
+    const int at = (t * (HD / 8) + (cc ^ bwd_swz<HD>(t))) * 8;
     *reinterpret_cast<uint4*>(qs + at) =
-        *reinterpret_cast<const uint4*>(a.q + (size_t)(row0 + t) * a.d + head * HD + 8 * c);
-    const float* dp = a.dout + (size_t)(row0 + t) * a.d + head * HD + 8 * c;
+        *reinterpret_cast<const uint4*>(a.q + (size_t)(row0 + t) * a.d + head * HD + 8 * cc);
+    const float* dp = a.dout + (size_t)(row0 + t) * a.d + head * HD + 8 * cc;
     const float4 x0 = *reinterpret_cast<const float4*>(dp), x1 = *reinterpret_cast<const float4*>(dp + 4);
     uint4 o;
     o.x = pack2bf(x0.x, x0.y); o.y = pack2bf(x0.z, x0.w); o.z = pack2bf(x1.x, x1.y); o.w = pack2bf(x1.z, x1.w);
     *reinterpret_cast<uint4*>(os + at) = o;
   }
   __syncthreads();
-  for (int j = wave; j < L; j += 4) {
-    // this key's k and v (the cache's bf16 values)
+  for (int j = wave; j < L; j += kBwdWaves) {
     const int page = pt[j / kPage], slot = j % kPage;
-    float kf[HD], vf[HD];
-    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD;
-    const bf16_t* vp = a.kv.v + ((size_t)page * H + head) * HD * kPage + slot;
+    float k8[8], v8[8];
+    unpack8(*reinterpret_cast<const uint4*>(a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * c), k8);
+    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * c) * kPage + slot;
 #pragma unroll
-    for (int c = 0; c < HD / 8; ++c) {
-      float f8[8];
-      unpack8(*reinterpret_cast<const uint4*>(kp + 8 * c), f8);
+    for (int e = 0; e < 8; ++e) v8[e] = bf2f(vp[e * kPage]);
+    float dk[8] = {}, dv[8] = {};
+    for (int t0 = j; t0 < L; t0 += RPS) {
+      const int t = t0 + grp;
+      const int tt = min(t, L - 1);
+      float q8[8], o8[8];
+      lds_chunk<HD>(qs, tt, c, q8);
+      lds_chunk<HD>(os, tt, c, o8);
+      float sp = 0.f, dpv = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kf[8 * c + e] = f8[e];
-    }
+      for (int e = 0; e < 8; ++e) {
+        sp += q8[e] * k8[e];
+        dpv += o8[e] * v8[e];
+      }
+      sp = group_sum<LPK>(sp);
+      dpv = group_sum<LPK>(dpv);
+      const float* st = a.stats + ((size_t)(row0 + tt) * H + head) * 2;
+      const float p = t < L ? expf(a.scale * sp - st[0]) : 0.f;
+      const float ds = p * (dpv - st[1]);
 #pragma unroll
-    for (int f = 0; f < HD; ++f) vf[f] = bf2f(vp[f * kPage]);
-    float pv[NS], dsv[NS];
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int t = j + lane + 64 * i;
-      pv[i] = dsv[i] = 0.f;
-      if (t < L) {
-        const float* st = a.stats + ((size_t)(row0 + t) * H + head) * 2;
-        const float p = expf(a.scale * bwd_dot<HD>(qs, t, kf) - st[0]);
-        pv[i] = p;
-        dsv[i] = p * (bwd_dot<HD>(os, t, vf) - st[1]);
+      for (int e = 0; e < 8; ++e) {
+        dk[e] += ds * q8[e];
+        dv[e] += p * o8[e];
       }
     }
-    constexpr int FPL = HD / 64;
-    float dk[FPL], dv[FPL];
 #pragma unroll
-    for (int u = 0; u < FPL; ++u) dk[u] = dv[u] = 0.f;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int tend = min(L, j + 64 * (i + 1));
-#pragma unroll 8
-      for (int t = j + 64 * i; t < tend; ++t) {
-        const float ds = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsv[i]), t - j - 64 * i));
-        const float p = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pv[i]), t - j - 64 * i));
-#pragma unroll
-        for (int u = 0; u < FPL; ++u) {
-          dk[u] += ds * bf2f(qs[bwd_lds<HD>(t, lane + 64 * u)]);
-          dv[u] += p * bf2f(os[bwd_lds<HD>(t, lane + 64 * u)]);
-        }
-      }
+    for (int e = 0; e < 8; ++e) {
+      dk[e] = a.scale * across_groups<LPK>(dk[e]);
+      dv[e] = across_groups<LPK>(dv[e]);
     }
-    const int row = row0 + j, K3 = 3 * a.d;
+    if (grp == 0) {
+      const int row = row0 + j, K3 = 3 * a.d;
 #pragma unroll
-    for (int u = 0; u < FPL; ++u)
-      a.dqkv[frag_index(row, 2 * a.d + head * HD + lane + 64 * u, K3)] = f2bf(dv[u]);
-    if (HD == 128) {
-      bwd_store_rot<HD>(a, row, j, head, 1, lane, a.scale * dk[0], a.scale * dk[FPL - 1]);
-    } else {
-      const float partner = __shfl_xor(dk[0], 32, kWave);
-      if (lane < 32) bwd_store_rot<HD>(a, row, j, head, 1, lane, a.scale * dk[0], a.scale * partner);
+      for (int e = 0; e < 8; ++e) a.dqkv[frag_index(row, 2 * a.d + head * HD + 8 * c + e, K3)] = f2bf(dv[e]);
+      bwd_store_rot8<HD>(a, row, j, head, 1, c, dk);
     }
   }
 }
@@ -533,7 +494,7 @@ hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d,
 
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s) {
   if (a.n_env <= 0) return hipSuccess;
-  const dim3 grid(a.n_env, a.n_heads), block(256);
+  const dim3 grid(a.n_env, a.n_heads), block(64 * kBwdWaves);
   if (a.head_dim == 128) {
     hipLaunchKernelGGL(attn_bwd_q_kernel<128>, grid, block, 0, s, a);
     hipLaunchKernelGGL(attn_bwd_kv_kernel<128>, grid, block, 0, s, a);

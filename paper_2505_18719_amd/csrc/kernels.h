@@ -150,6 +150,7 @@ struct PrefillAttnArgs {
   float scale;
   const int32_t* env_q0;      // [B] first query row of env b whose output is needed, or null for all;
                               // the 16-row query tiles below its tile are skipped
+  float* lse;                 // [M, n_heads, 2] or null: [row, head, 0] receives log sum_j exp(scale q.k_j)
 };
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
 
@@ -301,6 +302,7 @@ hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh
                              bf16_t* h, hipStream_t s);
 struct AttnBwdArgs {
   const bf16_t* q;        // [M, d] rotated queries of the forward
+  const bf16_t* o;        // [M, d] attention output of the forward (bf16 frag, K = d)
   const float* dout;      // [M, d] gradient of the attention output
   KvCache kv;             // rotated keys and values of the forward
   const int32_t* page_table;
@@ -310,7 +312,8 @@ struct AttnBwdArgs {
   int n_env, d, n_heads, head_dim;
   float scale;
   const float2* rope;     // [pos][head_dim / 2] (cos, sin)
-  float* stats;           // [M, n_heads, 2] scratch: log-sum-exp and D of each query row
+  float* stats;           // [M, n_heads, 2]: log-sum-exp of each query row (from the forward's
+                          // PrefillAttnArgs::lse) in, D_t = dO_t . O_t written by the first pass
   bf16_t* dqkv;           // [M, 3 d] bf16 frag (K = 3 d): gradients of q, k (before rotation, packed order), v
 };
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s);

@@ -473,7 +473,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   g.d_model = d; g.n_heads = D.H; g.head_dim = D.hd;
   VLA_CK(launch_gemm(g, kEpiQkvRope, s));
   PrefillAttnArgs pa{m->q, t.ob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
-                     B, d, D.H, D.hd, m->scale, nullptr};
+                     B, d, D.H, D.hd, m->scale, nullptr, t.stats};
   VLA_CK(launch_attn_prefill(pa, s));
   VLA_CK(hipMemcpyAsync(t.xm, t.xs[l], (size_t)M * d * sizeof(float), hipMemcpyDeviceToDevice, s));
   GemmArgs go{};
@@ -492,7 +492,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   // attention: do = dxm Wo, attention backward, du1 = d[q; k; v] Wqkv
   VLA_CK(launch_transpose_frag(w.wo, false, d, d, d, d, t.wt, s));
   VLA_CK(gemm_f32(t.dxmf, 0, t.wt, 0, M, d, d, t.dob, d, s));
-  AttnBwdArgs ab{m->q, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
+  AttnBwdArgs ab{m->q, t.ob, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
                  m->scale, m->rope, t.stats, t.dqkv};
   VLA_CK(launch_attn_bwd(ab, s));
   VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
