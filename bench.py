@@ -466,9 +466,16 @@ def main():
         torch.cuda.synchronize()
         bwd_ms = e0.elapsed_time(e1)
         Lt = inp.prefix_lens.astype(np.float64) + cfg.n_actions
-        fwd = 2 * layer_params * L * Lt.sum() + 2 * d * L * (Lt * (Lt + 1)).sum()
+        # algorithmic work: the forward, the input gradients (the GEMMs' flops again;
+        # dV, dP, dQ and dK of attention, twice its forward), and the four rank-32
+        # products of each adapted projection (X A^T, dY B, dY^T T1, T2^T X); no
+        # weight gradient is formed and the per-layer recompute is not counted
+        fwd_gemm = 2 * layer_params * L * Lt.sum()
+        fwd_attn = 2 * d * L * (Lt * (Lt + 1)).sum()
+        lora_flops = 4 * Lt.sum() * 32 * (11 * d + 3 * F) * L
+        work = 2 * fwd_gemm + 3 * fwd_attn + lora_flops
         result["lora_backward"] = {"ms": bwd_ms, "rows": int(Lt.sum()), "projections": 7 * L, "rank": 32,
-                                   "mfma_frac": 3 * fwd / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                   "mfma_frac": work / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                    "loss": float(st_b[0])}
         log(f"[bench] PPO LoRA gradient (teacher-forced pass + backward): {bwd_ms:.1f} ms")
 

@@ -102,8 +102,10 @@ int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
  * the head and final RMSNorm of the scoring rows, and for each layer from the
  * top a recompute of its forward from its saved input, the gradient GEMMs
  * against its transposed weights, RMSNorm, SwiGLU and causal-attention (with
- * rotary) backward, and dL/dA = scale B^T G, dL/dB = scale G A^T from the
- * projection's weight gradient G = dY^T X.
+ * rotary) backward, and the LoRA gradients dL/dB = scale dY^T (X A^T),
+ * dL/dA = scale (dY B)^T X of each adapted projection (X its input rows, dY
+ * the gradient of its output rows: the rank-r reductions of its weight
+ * gradient dY^T X, taken without forming it).
  *   batch, vis_emb, prompt_ids, prompt_lens_host, action_tokens  as in
  *                vla_token_logprobs
  *   logp_old     fp32 [batch, n_actions] token log-probs of the rollout policy
@@ -113,8 +115,9 @@ int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
  *   train_ws     device memory of >= vla_train_workspace_size bytes, 256-byte aligned
  *   stats        fp32 [2] out: loss -J and clipped fraction
  *   logp_new     fp32 [batch, n_actions] out, or NULL: the teacher-forced log-probs
- * Gradient operands of the GEMMs are rounded to bf16 as the forward's
- * activations are (fp32 accumulation).  Overwrites the handle's prefill state. */
+ * Gradient operands of the GEMMs, and the rank-r products X A^T and
+ * dY B, are rounded to bf16 as the forward's activations are (fp32
+ * accumulation).  Overwrites the handle's prefill state. */
 int vla_ppo_lora_grads(struct vla_model* m, int32_t batch, const void* vis_emb, const int32_t* prompt_ids,
                        const int32_t* prompt_lens_host, const int32_t* action_tokens, const float* logp_old,
                        const float* advantages, float eps, float temperature, const vla_lora* lora,

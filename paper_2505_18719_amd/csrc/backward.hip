@@ -355,104 +355,49 @@ __global__ __launch_bounds__(64 * kBwdWaves, 1) void attn_bwd_kv_kernel(AttnBwdA
 }
 
 // ---- LoRA gradients from a weight gradient ---------------------------------------
-// With W = W0 + s B A and G = dL/dW [out, in]: dL/dA = s B^T G, dL/dB = s G A^T.
-// G is given transposed, column o0 + o of dwt holding output o in the packed row
-// order of `mode` (grad_row maps it to the natural row, or -1 for a padding row
-// or the other half of [gate; up]).  64 x 64 output tiles of fp32 FMAs through LDS.
+// LoRA gradients (W = W0 + s B A): with T1 = X A^T and T2 = dY B over the M rows,
+// dL/dB = s dY^T T1 and dL/dA = s T2^T X, the rank-r reductions of dL/dW = dY^T X
+// taken without forming it.  Output o of a projection sits at column o0 + o of the
+// packed output order of `mode`; grad_row maps it to the natural row, or -1 for a
+// padding row or the other half of [gate; up].
 __device__ __forceinline__ int grad_row(const LoraGradArgs& a, int o) {
   int part;
   const int j = pack_src_row(a.mode, o, a.head_dim, a.out, part);
   return (j >= 0 && (a.mode != kPackGateUp || part == a.part)) ? j : -1;
 }
 
-constexpr int kLoraChunk = 512;  // reduction chunk of one workgroup (partials summed in chunk order)
-
-// partial dA over output columns [chunk * 512, +512): part[chunk][c][i]
-__global__ __launch_bounds__(256) void lora_da_kernel(LoraGradArgs a) {
-  __shared__ float ws[64][33];  // dwt[i0 + ii, o]
-  __shared__ float bs[32][65];  // B[grad_row(o), c]
-  const int i0 = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
-  const int o_beg = blockIdx.y * kLoraChunk, o_end = min(a.n_cols, o_beg + kLoraChunk);
-  float acc[4][4] = {};
-  for (int ob = o_beg; ob < o_end; ob += 32) {
-    for (int e = tid; e < 64 * 32; e += 256) {
-      const int ii = e / 32, oo = e % 32;
-      ws[ii][oo] = (i0 + ii < a.in && ob + oo < o_end) ? a.dwt[(size_t)(i0 + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
-      const int c = e % 64, o2 = e / 64;
-      const int nr = ob + o2 < o_end ? grad_row(a, ob + o2) : -1;
-      bs[o2][c] = (nr >= 0 && c < a.r) ? bf2f(a.b[(size_t)nr * a.r + c]) : 0.f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int oo = 0; oo < 32; ++oo)
+// B^T of one projection as a skinny-GEMM operand: dst (bf16 frag [64 rows, K]) row c,
+// column o0 + o = B[grad_row(o), c] for o < n_cols and c < r, zero elsewhere.
+__global__ void pack_bt_kernel(LoraGradArgs a, int K, bf16_t* __restrict__ dst) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= 64 * (K / 8)) return;
+  const int c = i / (K / 8), k0 = (i % (K / 8)) * 8;
+  float v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] += ws[ty * 4 + u][oo] * bs[oo][tx * 4 + v];
-    __syncthreads();
+  for (int e = 0; e < 8; ++e) {
+    const int o = k0 + e - a.o0;
+    const int nr = (c < a.r && o >= 0 && o < a.n_cols) ? grad_row(a, o) : -1;
+    v[e] = nr >= 0 ? bf2f(a.b[(size_t)nr * a.r + c]) : 0.f;
   }
-  float* part = a.scratch + (size_t)blockIdx.y * 64 * a.in;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int i = i0 + ty * 4 + u, c = tx * 4 + v;
-      if (i < a.in) part[(size_t)c * a.in + i] = acc[u][v];
-    }
+  uint4 q;
+  q.x = pack2bf(v[0], v[1]); q.y = pack2bf(v[2], v[3]); q.z = pack2bf(v[4], v[5]); q.w = pack2bf(v[6], v[7]);
+  *reinterpret_cast<uint4*>(dst + frag_index(c, k0, K)) = q;
 }
 
-// partial dB^T over input features [chunk * 512, +512): part[chunk][c][o]
-__global__ __launch_bounds__(256) void lora_db_kernel(LoraGradArgs a) {
-  __shared__ float ws[32][65];  // dwt[i, o0 + ob + oo]
-  __shared__ float as[32][65];  // A[c, i]
-  const int ob = blockIdx.x * 64, tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
-  const int i_beg = blockIdx.y * kLoraChunk, i_end = min(a.in, i_beg + kLoraChunk);
-  float acc[4][4] = {};
-  for (int ib = i_beg; ib < i_end; ib += 32) {
-    for (int e = tid; e < 32 * 64; e += 256) {
-      const int ii = e / 64, oo = e % 64;
-      ws[ii][oo] = (ib + ii < i_end && ob + oo < a.n_cols) ? a.dwt[(size_t)(ib + ii) * a.ldw + a.o0 + ob + oo] : 0.f;
-      const int c = e % 64, i2 = e / 64;
-      as[i2][c] = (c < a.r && ib + i2 < i_end) ? bf2f(a.a[(size_t)c * a.in + ib + i2]) : 0.f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int ii = 0; ii < 32; ++ii)
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] += ws[ii][ty * 4 + u] * as[ii][tx * 4 + v];
-    __syncthreads();
+// scale and place a [64, ldc] product: dB[grad_row(o), c] = s C[c, o] (o < n_cols), or
+// dA[c, i] = s C[c, i] (i < in)
+__global__ void lora_finalize_kernel(LoraGradArgs a, const float* __restrict__ C, int ldc, bool to_b) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int n = to_b ? a.n_cols : a.in;
+  if (e >= a.r * n) return;
+  const int c = e / n, o = e % n;
+  const float v = a.scale * C[(size_t)c * ldc + o];
+  if (to_b) {
+    const int nr = grad_row(a, o);
+    if (nr >= 0) a.db[(size_t)nr * a.r + c] = v;
+  } else {
+    a.da[(size_t)c * a.in + o] = v;
   }
-  float* part = a.scratch + (size_t)blockIdx.y * 64 * a.n_cols;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int o = ob + ty * 4 + u, c = tx * 4 + v;
-      if (o < a.n_cols) part[(size_t)c * a.n_cols + o] = acc[u][v];
-    }
-}
-
-// dA[c, i] = s sum_chunks part[chunk][c][i]
-__global__ void lora_da_reduce_kernel(LoraGradArgs a, int chunks) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= a.r * a.in) return;
-  float v = 0.f;
-  for (int k = 0; k < chunks; ++k) v += a.scratch[(size_t)k * 64 * a.in + e];
-  a.da[e] = a.scale * v;
-}
-
-// dB[grad_row(o), c] = s sum_chunks part[chunk][c][o]
-__global__ void lora_db_reduce_kernel(LoraGradArgs a, int chunks) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= a.r * a.n_cols) return;
-  const int c = e / a.n_cols, o = e % a.n_cols;
-  const int nr = grad_row(a, o);
-  if (nr < 0) return;
-  float v = 0.f;
-  for (int k = 0; k < chunks; ++k) v += a.scratch[(size_t)k * 64 * a.n_cols + (size_t)c * a.n_cols + o];
-  a.db[(size_t)nr * a.r + c] = a.scale * v;
 }
 
 // dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), fp32 rows of d
@@ -468,19 +413,16 @@ __global__ void move_rows_kernel(const float* __restrict__ src, const int32_t* _
 
 }  // namespace
 
-size_t lora_grad_part_floats(int in, int n_cols) {
-  const size_t ca = (size_t)((n_cols + kLoraChunk - 1) / kLoraChunk) * 64 * in;
-  const size_t cb = (size_t)((in + kLoraChunk - 1) / kLoraChunk) * 64 * n_cols;
-  return ca > cb ? ca : cb;
+hipError_t launch_pack_bt(const LoraGradArgs& a, int K, bf16_t* dst, hipStream_t s) {
+  if (K % 32 != 0 || a.r < 1 || a.r > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_bt_kernel, dim3((64 * (K / 8) + 255) / 256), dim3(256), 0, s, a, K, dst);
+  return hipGetLastError();
 }
 
-hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s) {
-  if (a.r < 1 || a.r > 64 || a.in <= 0 || a.n_cols <= 0) return hipErrorInvalidValue;
-  const int ca = (a.n_cols + kLoraChunk - 1) / kLoraChunk, cb = (a.in + kLoraChunk - 1) / kLoraChunk;
-  hipLaunchKernelGGL(lora_da_kernel, dim3((a.in + 63) / 64, ca), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(lora_da_reduce_kernel, dim3((a.r * a.in + 255) / 256), dim3(256), 0, s, a, ca);
-  hipLaunchKernelGGL(lora_db_kernel, dim3((a.n_cols + 63) / 64, cb), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(lora_db_reduce_kernel, dim3((a.r * a.n_cols + 255) / 256), dim3(256), 0, s, a, cb);
+hipError_t launch_lora_finalize(const LoraGradArgs& a, const float* C, int ldc, bool to_b, hipStream_t s) {
+  const int n = to_b ? a.n_cols : a.in;
+  if (a.r < 1 || a.r > 64 || n <= 0 || n > ldc) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lora_finalize_kernel, dim3((a.r * n + 255) / 256), dim3(256), 0, s, a, C, ldc, to_b);
   return hipGetLastError();
 }
 

@@ -317,23 +317,26 @@ struct AttnBwdArgs {
   bf16_t* dqkv;           // [M, 3 d] bf16 frag (K = 3 d): gradients of q, k (before rotation, packed order), v
 };
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s);
-// LoRA gradients of one projection from its weight gradient, given transposed:
-// dA = s B^T G [r, in] and dB = s G A^T [out, r] (fp32, row-major, overwritten)
+// LoRA gradients of one projection by the low-rank route: with X its input rows and
+// dY the gradient of its output rows, dB = s dY^T (X A^T) and dA = s (dY B)^T X on the
+// skinny GEMM (r <= 64 output rows), the four products chained through bf16 frag operands.
 struct LoraGradArgs {
-  const float* dwt;  // [in rows, ldw]: column o0 + o = output o in the packed order of `mode`
-  int ldw, o0, n_cols;
+  int o0, n_cols;    // this projection's columns o0 .. o0 + n_cols of the packed output order
   int in, out;       // natural sizes of the projection
   int mode, head_dim, part;  // PackMode of its packed rows; part 0 gate / 1 up for kPackGateUp
   const bf16_t* a;   // [r, in] row-major
   const bf16_t* b;   // [out, r] row-major
   int r;             // 1 .. 64
   float scale;
-  float* da;
-  float* db;
-  float* scratch;    // lora_grad_part_floats(in, n_cols) floats of partial sums
+  float* da;         // [r, in] fp32 out
+  float* db;         // [out, r] fp32 out
 };
-size_t lora_grad_part_floats(int in, int n_cols);
-hipError_t launch_lora_grad(const LoraGradArgs& a, hipStream_t s);
+// B^T as a bf16 frag [64, K] operand: row c, column o0 + o = B[natural row of packed
+// output o, c] for o < n_cols, c < r; zero elsewhere (K % 32 == 0)
+hipError_t launch_pack_bt(const LoraGradArgs& a, int K, bf16_t* dst, hipStream_t s);
+// dB[natural row of o, c] = s C[c, o] for o < n_cols (to_b), or dA[c, i] = s C[c, i] for i < in;
+// C fp32 [64, ldc] row-major
+hipError_t launch_lora_finalize(const LoraGradArgs& a, const float* C, int ldc, bool to_b, hipStream_t s);
 // fp32 rows of d: dst[rows[i]] = src[i] (scatter) or dst[i] = src[rows[i]] (gather), i < R
 hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d, float* dst, bool scatter,
                             hipStream_t s);

@@ -150,6 +150,7 @@ struct vla_model {
   float scale;
   // decode GEMM work splits (one persistent workgroup per CU)
   SkinnyPlan plan_qkv, plan_o, plan_gu, plan_d, plan_head;
+  int cus;  // compute units: the skinny GEMM's persistent grid
   // live profiling
   struct ProfSlot {
     hipEvent_t a, b;
@@ -405,13 +406,18 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
 // Buffers of the caller's training workspace.
 struct TrainBufs {
   std::vector<float*> xs;  // per-layer input residual [Mmax, d]
-  float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *dwt, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp, *lpart;
-  bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t;
+  float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp;
+  float *t1, *t2, *cres, *spart;  // low-rank products and skinny-GEMM partials
+  bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t, *apk, *bpt, *t1f, *t2f;
 };
 
 void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   const size_t Mx = D.Mmax, d = D.d;
-  const int A32 = round_up(D.A, 32), Mk = round_up((int)D.Mmax, 32);
+  // rows padded to 64 (the skinny GEMM's column tiles run over them), the
+  // row contraction padded to 256 (its K units)
+  const size_t Mx64 = round_up((int)D.Mmax, 64);
+  const int A32 = round_up(D.A, 32), Mk = round_up((int)D.Mmax, 256);
+  const int Fg = 64 * ((D.F + 31) / 32), F64 = round_up(D.F, 64);
   const size_t Rh = (size_t)D.Bmax * D.nact;
   t.xs.resize(D.L);
   for (int l = 0; l < D.L; ++l) t.xs[l] = L.take<float>(Mx * d);
@@ -422,30 +428,36 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   t.xm = L.take<float>(Mx * d);
   t.cgu = L.take<float>(Mx * 2 * D.Fp);
   t.dh = L.take<float>(Mx * D.Fp);
-  t.dwt = L.take<float>(std::max(d * 3 * d, std::max(d * 2 * D.Fp, (size_t)D.Fp * d)));
   t.stats = L.take<float>(Mx * D.H * 2);
-  const int Fg = 64 * ((D.F + 31) / 32);
-  t.lpart = L.take<float>(std::max(lora_grad_part_floats(D.d, std::max(D.d, Fg)), lora_grad_part_floats(D.F, D.d)));
   t.dz = L.take<float>(Rh * D.A);
   t.du_h = L.take<float>(Rh * d);
   t.xc = L.take<float>(Rh * d);
   t.dxc = L.take<float>(Rh * d);
   t.logp = L.take<float>(Rh);
   t.dlogp = L.take<float>(Rh);
-  t.dxf = L.take<bf16_t>(frag_elems(Mx, d));
-  t.dxmf = L.take<bf16_t>(frag_elems(Mx, d));
-  t.u1 = L.take<bf16_t>(frag_elems(Mx, d));
-  t.ob = L.take<bf16_t>(frag_elems(Mx, d));
-  t.u2 = L.take<bf16_t>(frag_elems(Mx, d));
-  t.hb = L.take<bf16_t>(frag_elems(Mx, D.Fp));
-  t.dgu = L.take<bf16_t>(frag_elems(Mx, 2 * D.Fp));
-  t.dqkv = L.take<bf16_t>(frag_elems(Mx, 3 * D.d));
+  const size_t ncol = std::max(std::max(Mx64, (size_t)Fg), std::max(d, (size_t)F64));
+  t.t1 = L.take<float>(64 * Mx64);
+  t.t2 = L.take<float>(64 * Mx64);
+  t.cres = L.take<float>(64 * ncol);
+  t.spart = L.take<float>((size_t)kMaxSplits * 64 * ncol);
+  t.dxf = L.take<bf16_t>(frag_elems(Mx64, d));
+  t.dxmf = L.take<bf16_t>(frag_elems(Mx64, d));
+  t.u1 = L.take<bf16_t>(frag_elems(Mx64, d));
+  t.ob = L.take<bf16_t>(frag_elems(Mx64, d));
+  t.u2 = L.take<bf16_t>(frag_elems(Mx64, d));
+  t.hb = L.take<bf16_t>(frag_elems(Mx64, D.Fp));
+  t.dgu = L.take<bf16_t>(frag_elems(Mx64, 2 * D.Fp));
+  t.dqkv = L.take<bf16_t>(frag_elems(Mx64, 3 * D.d));
   t.wt = L.take<bf16_t>(std::max(std::max(frag_elems(D.Fp, D.d), frag_elems(D.d, 2 * D.Fp)),
                                  std::max(frag_elems(D.d, D.d), frag_elems(D.d, 3 * D.d))));
   t.xt = L.take<bf16_t>(frag_elems(std::max(D.d, D.Fp), Mk));
   t.dyt = L.take<bf16_t>(frag_elems(std::max(3 * D.d, 2 * D.Fp), Mk));
   t.dzf = L.take<bf16_t>(frag_elems(Rh, A32));
   t.wact_t = L.take<bf16_t>(frag_elems(D.d, A32));
+  t.apk = L.take<bf16_t>(frag_elems(64, std::max(D.d, D.Fp)));
+  t.bpt = L.take<bf16_t>(frag_elems(64, std::max(3 * D.d, 2 * D.Fp)));
+  t.t1f = L.take<bf16_t>(frag_elems(64, Mk));
+  t.t2f = L.take<bf16_t>(frag_elems(64, Mk));
   L.off = align_up(L.off, 256);
 }
 
@@ -464,7 +476,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   const LayerW& w = m->lw[l];
   const float eps = m->cfg.rms_eps;
   const int d = D.d, Fp = D.Fp, F64 = round_up(D.F, 64), Fg = 64 * ((D.F + 31) / 32);
-  const int Mk = round_up(M, 32);
+  const int Mp = round_up(M, 64), Mk = round_up(M, 256);
   // recompute the layer's forward from its saved input
   VLA_CK(launch_rmsnorm(t.xs[l], d, nullptr, w.attn_norm, eps, t.u1, d, M, d, s, true));
   GemmArgs g{};
@@ -497,39 +509,63 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   VLA_CK(launch_attn_bwd(ab, s));
   VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
   VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
-  // LoRA gradients: dW^T = X^T dY on the GEMM, then dA = s B^T dW, dB = s dW A^T
+  // LoRA gradients by the low-rank route on the skinny GEMM (r <= 64 output rows; the
+  // contractions over the M rows run with K = Mk, rows past M zero):
+  //   T1^T = A X^T, T2^T = B^T dY^T (r x M);  dB^T = T1^T dY,  dA = T2^T X
   auto adapted = [&](int p) { return lora->a[l * 7 + p] != nullptr; };
-  auto grad = [&](int p, int ldw, int o0, int n_cols, int in, int out, int mode, int part) {
-    LoraGradArgs la{t.dwt, ldw, o0, n_cols, in, out, mode, D.hd, part,
+  auto skinny_to = [&](const bf16_t* a_op, const bf16_t* w_op, int N, int K, float* out) {
+    const SkinnyPlan sp = skinny_plan(N, K, m->cus, kMaxSplits);
+    SkinnyArgs sa{a_op, 64, w_op, N, K, t.spart};
+    hipError_t e = launch_skinny(sa, sp, s);
+    return e != hipSuccess ? e : launch_reduce_sum(t.spart, sp, out, 64, N, s);
+  };
+  // X frag [M, kx] (in real input features) with X^T rows in64; dY frag [M, ky] whose
+  // columns o0 .. o0 + n_cols are this projection's outputs in the packed order of
+  // `mode`, dYT its transpose (rows o0 .. o0 + n_cols)
+  auto lowrank = [&](int p, const bf16_t* X, int kx, int in, const bf16_t* XT, const bf16_t* dY, int ky,
+                     const bf16_t* dYT, int o0, int n_cols, int out, int mode, int part) -> hipError_t {
+    LoraGradArgs la{o0, n_cols, in, out, mode, D.hd, part,
                     static_cast<const bf16_t*>(lora->a[l * 7 + p]), static_cast<const bf16_t*>(lora->b[l * 7 + p]),
-                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p], t.lpart};
-    return launch_lora_grad(la, s);
+                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p]};
+    PackArgs pa{t.apk, 64, kx, la.a, nullptr, in, lora->rank, in, kPackRows, D.hd};
+    hipError_t e;
+    if ((e = launch_pack_frag(pa, s)) != hipSuccess) return e;
+    if ((e = skinny_to(t.apk, X, Mp, kx, t.t1)) != hipSuccess) return e;
+    if ((e = launch_to_frag(t.t1, Mp, 64, M, Mk, t.t1f, s)) != hipSuccess) return e;
+    if ((e = launch_pack_bt(la, ky, t.bpt, s)) != hipSuccess) return e;
+    if ((e = skinny_to(t.bpt, dY, Mp, ky, t.t2)) != hipSuccess) return e;
+    if ((e = launch_to_frag(t.t2, Mp, 64, M, Mk, t.t2f, s)) != hipSuccess) return e;
+    la.o0 = 0;  // dYT holds only this projection's rows
+    if ((e = skinny_to(t.t1f, dYT, n_cols, Mk, t.cres)) != hipSuccess) return e;
+    if ((e = launch_lora_finalize(la, t.cres, n_cols, true, s)) != hipSuccess) return e;
+    const int in64 = round_up(in, 64);
+    if ((e = skinny_to(t.t2f, XT, in64, Mk, t.cres)) != hipSuccess) return e;
+    return launch_lora_finalize(la, t.cres, in64, false, s);
   };
   if (adapted(VLA_PROJ_Q) || adapted(VLA_PROJ_K) || adapted(VLA_PROJ_V)) {
     VLA_CK(launch_transpose_frag(t.u1, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dqkv, false, 3 * d, M, 3 * d, Mk, t.dyt, s));
-    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, 3 * d, Mk, t.dwt, 3 * d, s));
     for (int p = VLA_PROJ_Q; p <= VLA_PROJ_V; ++p)
-      if (adapted(p)) VLA_CK(grad(p, 3 * d, p * d, d, d, d, p == VLA_PROJ_V ? kPackRows : kPackQk, 0));
+      if (adapted(p))
+        VLA_CK(lowrank(p, t.u1, d, d, t.xt, t.dqkv, 3 * d, t.dyt + frag_index(p * d, 0, Mk), p * d, d, d,
+                       p == VLA_PROJ_V ? kPackRows : kPackQk, 0));
   }
   if (adapted(VLA_PROJ_O)) {
     VLA_CK(launch_transpose_frag(t.ob, false, d, M, d, Mk, t.xt, s));
-    VLA_CK(launch_transpose_frag(t.dxm, true, d, M, d, Mk, t.dyt, s));
-    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, d, Mk, t.dwt, d, s));
-    VLA_CK(grad(VLA_PROJ_O, d, 0, d, d, d, kPackRows, 0));
+    VLA_CK(launch_transpose_frag(t.dxmf, false, d, M, d, Mk, t.dyt, s));
+    VLA_CK(lowrank(VLA_PROJ_O, t.ob, d, d, t.xt, t.dxmf, d, t.dyt, 0, d, d, kPackRows, 0));
   }
   if (adapted(VLA_PROJ_GATE) || adapted(VLA_PROJ_UP)) {
     VLA_CK(launch_transpose_frag(t.u2, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dgu, false, 2 * Fp, M, Fg, Mk, t.dyt, s));
-    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, d, Fg, Mk, t.dwt, 2 * Fp, s));
-    if (adapted(VLA_PROJ_GATE)) VLA_CK(grad(VLA_PROJ_GATE, 2 * Fp, 0, Fg, d, D.F, kPackGateUp, 0));
-    if (adapted(VLA_PROJ_UP)) VLA_CK(grad(VLA_PROJ_UP, 2 * Fp, 0, Fg, d, D.F, kPackGateUp, 1));
+    for (int p = VLA_PROJ_GATE; p <= VLA_PROJ_UP; ++p)
+      if (adapted(p))
+        VLA_CK(lowrank(p, t.u2, d, d, t.xt, t.dgu, 2 * Fp, t.dyt, 0, Fg, D.F, kPackGateUp, p - VLA_PROJ_GATE));
   }
   if (adapted(VLA_PROJ_DOWN)) {
     VLA_CK(launch_transpose_frag(t.hb, false, Fp, M, D.F, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dxf, false, d, M, d, Mk, t.dyt, s));
-    VLA_CK(gemm_f32(t.xt, 0, t.dyt, 0, D.F, d, Mk, t.dwt, d, s));
-    VLA_CK(grad(VLA_PROJ_DOWN, d, 0, d, D.F, d, kPackRows, 0));
+    VLA_CK(lowrank(VLA_PROJ_DOWN, t.hb, Fp, D.F, t.xt, t.dxf, d, t.dyt, 0, d, d, kPackRows, 0));
   }
   // dL/d(layer input) = dxm + RMSNorm backward of du1
   VLA_CK(launch_rmsnorm_bwd(t.xs[l], w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
@@ -581,6 +617,7 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
       cus = 256;
+    m->cus = cus;
     m->plan_qkv = skinny_plan(3 * D.d, D.d, cus, kMaxSplits);
     m->plan_o = skinny_plan(D.d, D.d, cus, kMaxSplits);
     m->plan_gu = skinny_plan(2 * D.Fp, D.d, cus, kMaxSplits);
