@@ -155,23 +155,32 @@ __global__ void swiglu_bwd_kernel(const float* __restrict__ cgu, int ldc, const 
   *reinterpret_cast<uint4*>(h + frag_index(m, j0, Fp)) = o;
 }
 
-// ---- causal attention backward ------------------------------------------------
-// Per (environment, head) workgroup of 16 waves.  With P = softmax(scale q k^T)
-// (causal) given by the forward's log-sum-exp per query row (P = exp(scale
-// q.k - lse)), dP = dO V^T, D_t = dO_t . O_t and dS = P (dP - D):
-//   pass 1 (queries): D_t, and dq_t = scale sum_j dS_tj k_j;
-//   pass 2 (keys):    dk_j = scale sum_t dS_tj q_t, dv_j = sum_t P_tj dO_t.
-// A wave takes one row (query or key) at a time; its lanes hold 8 features
-// each, HD / 8 lanes per row of the other side, 512 / HD of those rows per step,
-// and reduce their partial dot products with shuffles.  q and k are the
-// rotated values the forward attended with; the gradients go back through the
-// inverse rotation at each row's position and are written as bf16 into the
-// [q; k; v] gradient in the packed weight's column order (frag layout, K = 3 d).
-constexpr int kBwdKeys = 320;  // longest sequence (one environment)
-constexpr int kBwdWaves = 16;
+// ---- causal attention backward on the matrix cores -----------------------------
+// With P = softmax(scale q k^T) (causal) recovered from the forward's log-sum-exp
+// per query row (P = exp(scale q.k - lse)), dP = dO V^T, D_t = dO_t . O_t and
+// dS = P (dP - D):  dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO.
+// Two passes, each one 512-thread workgroup (8 waves) per (environment, head),
+// <= 320 rows, every product a 16x16x32 bf16 MFMA with fp32 accumulation:
+//   pass 1 (queries): a wave takes 16-query tiles; per 32-key chunk it forms
+//     S^T = K Q^T and dP^T = V dO^T, keys on the MFMA rows in the order that
+//     leaves lane group g holding keys 8g .. 8g+7 of the chunk, so dS^T is
+//     already the B operand of dQ^T += K^T dS^T.  V (key-major) and K^T (16-key
+//     pages) are transposed into LDS once; K rows stream from the cache.  Also
+//     writes D and dO rounded to bf16 (row-major) for pass 2.
+//   pass 2 (keys): a wave takes 16-key tiles; per 32-query chunk it forms
+//     S = Q K^T and dP = dO V^T with queries on the MFMA rows in the same
+//     order, so P and dS are the B operands of dV^T += dO^T P and
+//     dK^T += Q^T dS.  Q^T and dO^T (16-query pages) are transposed into LDS
+//     once; Q and dO rows stream from memory.
+// P and dS enter their products as hi + lo bf16 pairs (~16 significant bits);
+// q, k, v and dO are the bf16 operands of the forward.  q and k are the rotated
+// values the forward attended with: their gradients go back through the inverse
+// rotation and are written as bf16 into the [q; k; v] gradient in the packed
+// weight's column order (frag layout, K = 3 d).
+constexpr int kAbKeys = 320;  // longest sequence (one environment)
+constexpr int kAbPages = kAbKeys / kPage;
+constexpr int kAbWaves = 8;
 
-template <int HD>
-__device__ __forceinline__ int bwd_swz(int row) { return row & (HD / 8 - 1); }
 // packed column of natural feature f of a rotated head (q, k): pairs (i, i + HD/2) of each
 // 32-feature block sit 32 columns apart in 64-column groups
 template <int HD>
@@ -179,182 +188,317 @@ __device__ __forceinline__ int qk_packed_col(int f) {
   constexpr int half = HD / 2;
   return f < half ? 64 * (f >> 5) + (f & 31) : 64 * ((f - half) >> 5) + 32 + ((f - half) & 31);
 }
-// 16-byte chunk c of row `row` of a [kBwdKeys, HD] bf16 LDS tile (chunks swizzled per row)
+// Row order of a key- (query-) major MFMA operand: row i of 16-row tile t of 32-row chunk c
+// is sequence row 32 c + 8 (i / 4) + 4 t + i % 4, so C rows 4 g + r of tiles t = 0, 1 are
+// rows 8 g .. 8 g + 7 of the chunk in lane group g.  ab_slot inverts it.
+__device__ __forceinline__ int ab_row(int R) { return 32 * (R >> 5) + 8 * ((R & 15) >> 2) + 4 * ((R >> 4) & 1) + (R & 3); }
+__device__ __forceinline__ int ab_slot(int k) {
+  const int w = k & 31;
+  return 32 * (k >> 5) + 16 * ((w >> 2) & 1) + 4 * (w >> 3) + (w & 3);
+}
+// 16-byte feature chunk j of LDS row R of a row-major tile is stored at chunk j ^ ab_swz(R)
 template <int HD>
-__device__ __forceinline__ void lds_chunk(const bf16_t* t, int row, int c, float* f8) {
-  unpack8(*reinterpret_cast<const uint4*>(t + (row * (HD / 8) + (c ^ bwd_swz<HD>(row))) * 8), f8);
+__device__ __forceinline__ int ab_swz(int R) {
+  return HD == 128 ? (R & 15) : ((R >> 1) & 7);
 }
-template <int LPK>
-__device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int o = LPK / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-// sum over the 64 / LPK row groups of a wave (lanes with the same feature chunk)
-template <int LPK>
-__device__ __forceinline__ float across_groups(float v) {
-#pragma unroll
-  for (int o = LPK; o < 64; o <<= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-// write features 8c .. 8c + 7 of a q or k gradient back through the rotation; the
-// pair partner of chunk c is chunk c ^ (HD / 16), held by lane ^ (HD / 16)
+// byte offset of (feature f, rows 8h .. 8h + 7 of a 16-row page) in a paged transposed tile:
+// half h of feature f sits at 16-byte unit 2 f + (h ^ ((f >> 3) & 1)) of its page
 template <int HD>
-__device__ __forceinline__ void bwd_store_rot8(const AttnBwdArgs& a, int row, int pos, int head, int region, int c,
-                                               const float* g) {
-  constexpr int half = HD / 2, hc = HD / 16;
-  float out[8];
-  const bool first = c < hc;  // features below half
+__device__ __forceinline__ int ab_page_off(int page, int f, int h) {
+  return page * (HD * kPage * 2) + 16 * (2 * f + (h ^ ((f >> 3) & 1)));
+}
+// transpose of an 8 x 8 bf16 block: out[b] element a = in[a] element b
+__device__ __forceinline__ void transpose8(const uint4* in, uint4* out) {
+  uint32_t w[32], o[32];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float other = __shfl_xor(g[e], hc, kWave);
-    const int i = (first ? 8 * c : 8 * c - half) + e;  // rotary pair index
-    const float2 cs = a.rope[pos * half + i];
-    // (g1, g2) of pair i: g1 belongs to feature i, g2 to i + half
-    const float g1 = first ? g[e] : other, g2 = first ? other : g[e];
-    out[e] = first ? g1 * cs.x + g2 * cs.y : -g1 * cs.y + g2 * cs.x;
+  for (int a = 0; a < 8; ++a) {
+    w[4 * a] = in[a].x; w[4 * a + 1] = in[a].y; w[4 * a + 2] = in[a].z; w[4 * a + 3] = in[a].w;
   }
+#pragma unroll
+  for (int b = 0; b < 8; ++b)
+#pragma unroll
+    for (int ap = 0; ap < 4; ++ap) {
+      const uint32_t lo = w[8 * ap + b / 2], hi = w[8 * ap + 4 + b / 2];
+      o[4 * b + ap] = (b & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+#pragma unroll
+  for (int b = 0; b < 8; ++b) out[b] = make_uint4(o[4 * b], o[4 * b + 1], o[4 * b + 2], o[4 * b + 3]);
+}
+// element i of hi, lo = v as a hi + lo pair of bf16
+__device__ __forceinline__ void split_bf16(float v, bf16x8& hi, bf16x8& lo, int i) {
+  const __bf16 h = (__bf16)v;
+  hi[i] = h;
+  lo[i] = (__bf16)(v - (float)h);
+}
+// Store a q or k gradient held transposed (acc[nb][r] = gradient of feature 16 nb + 4 g + r,
+// times 1 / mul) for sequence position pos through the inverse rotation: pair i = (i, i + HD/2)
+// sits in blocks nb and nb + NB/2 of the same lane.
+template <int HD>
+__device__ __forceinline__ void ab_store_rot(const AttnBwdArgs& a, size_t row, int pos, int head, int region,
+                                             const f32x4* acc, float mul, int g) {
+  constexpr int NB = HD / 16, half = HD / 2;
+  const float2* cs = a.rope + (size_t)pos * half;
   const int base = region * a.d + head * HD, K3 = 3 * a.d;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) a.dqkv[frag_index(row, base + qk_packed_col<HD>(8 * c + e), K3)] = f2bf(out[e]);
+  for (int nb = 0; nb < NB / 2; ++nb) {
+    float lo[4], hi[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float2 c = cs[16 * nb + 4 * g + r];
+      const float g1 = mul * acc[nb][r], g2 = mul * acc[nb + NB / 2][r];
+      lo[r] = g1 * c.x + g2 * c.y;
+      hi[r] = -g1 * c.y + g2 * c.x;
+    }
+    *reinterpret_cast<uint2*>(a.dqkv + frag_index(row, base + qk_packed_col<HD>(16 * nb + 4 * g), K3)) =
+        make_uint2(pack2bf(lo[0], lo[1]), pack2bf(lo[2], lo[3]));
+    *reinterpret_cast<uint2*>(a.dqkv + frag_index(row, base + qk_packed_col<HD>(16 * nb + 4 * g + half), K3)) =
+        make_uint2(pack2bf(hi[0], hi[1]), pack2bf(hi[2], hi[3]));
+  }
+}
+
+// pass 1, one 16-query tile: queries 16 qt .. 16 qt + 15, keys in chunks 0 .. qt / 2
+template <int HD>
+__device__ __forceinline__ void ab_dq_tile(const AttnBwdArgs& a, const char* vlds, const char* ktlds, int ptv, int qt,
+                                           int L, int row0, int head, int lane) {
+  constexpr int KROW = HD * 2, KS = HD / 32, NB = HD / 16;
+  const int r16 = lane & 15, g = lane >> 4, H = a.n_heads;
+  const int q = qt * 16 + r16;
+  const size_t row = (size_t)(row0 + min(q, L - 1));
+  // B operands: query q, features 32 ks + 8 g .. + 8
+  uint4 qf[KS], df[KS];
+  float dd = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const size_t at = row * a.d + head * HD + 32 * ks + 8 * g;
+    qf[ks] = *reinterpret_cast<const uint4*>(a.q + at);
+    const float4 x0 = *reinterpret_cast<const float4*>(a.dout + at), x1 = *reinterpret_cast<const float4*>(a.dout + at + 4);
+    df[ks] = make_uint4(pack2bf(x0.x, x0.y), pack2bf(x0.z, x0.w), pack2bf(x1.x, x1.y), pack2bf(x1.z, x1.w));
+    float o8[8], d8[8];
+    unpack8(*reinterpret_cast<const uint4*>(a.o + frag_index(row, head * HD + 32 * ks + 8 * g, a.d)), o8);
+    unpack8(df[ks], d8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dd += d8[e] * o8[e];
+    if (q < L) *reinterpret_cast<uint4*>(a.do16 + at) = df[ks];
+  }
+  dd += __shfl_xor(dd, 16, kWave);
+  dd += __shfl_xor(dd, 32, kWave);  // D_q = dO_q . O_q (dO as its bf16 operand)
+  float* st = a.stats + (row * H + head) * 2;
+  const float lse = st[0];
+  if (q < L && g == 0) st[1] = dd;
+
+  f32x4 dq[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) dq[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int ncq = qt / 2 + 1;
+  for (int c = 0; c < ncq; ++c) {
+    f32x4 s[2], dp[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // A operand row r16 of tile t: key 32 c + 8 (r16 / 4) + 4 t + r16 % 4 (clamped into the sequence)
+      const int key = min(32 * c + 8 * (r16 >> 2) + 4 * t + (r16 & 3), L - 1);
+      const int page = __shfl(ptv, key / kPage, kWave);
+      const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + key % kPage) * HD + 8 * g;
+      const char* vr = vlds + (32 * c + 16 * t + r16) * KROW;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        s[t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(kp + 32 * ks)), as_bf16x8(qf[ks]), s[t]);
+        dp[t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(vr + 16 * ((4 * ks + g) ^ ab_swz<HD>(r16)))),
+                       as_bf16x8(df[ks]), dp[t]);
+      }
+    }
+    // lane: query q, keys 32 c + 8 g + 4 t + r -> dS^T as the B operand (hi + lo)
+    bf16x8 shi, slo;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = 32 * c + 8 * g + 4 * t + r;
+        const float p = expf(a.scale * s[t][r] - lse);
+        const float ds = key <= q ? p * (dp[t][r] - dd) : 0.f;
+        split_bf16(ds, shi, slo, 4 * t + r);
+      }
+    // dQ^T += K^T dS^T: A operand = K^T rows 16 nb + r16, keys 32 c + 8 g .. + 8
+    const char* kt0 = ktlds + ab_page_off<HD>(2 * c + (g >> 1), r16, g & 1);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 kv = as_bf16x8(*reinterpret_cast<const uint4*>(kt0 + nb * 512));
+      dq[nb] = mfma16(kv, shi, dq[nb]);
+      dq[nb] = mfma16(kv, slo, dq[nb]);
+    }
+  }
+  if (q < L) ab_store_rot<HD>(a, row, q, head, 0, dq, a.scale, g);
 }
 
 template <int HD>
-__global__ __launch_bounds__(64 * kBwdWaves, 1) void attn_bwd_q_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t ks[kBwdKeys * HD];
-  __shared__ __attribute__((aligned(16))) bf16_t vs[kBwdKeys * HD];
-  constexpr int LPK = HD / 8, RPS = 64 / LPK;  // lanes per key row, key rows per step
+__global__ __launch_bounds__(64 * kAbWaves, 1) void attn_bwd_dq_kernel(AttnBwdArgs a) {
+  constexpr int KROW = HD * 2, VPAGE = HD * kPage * 2, HC = HD / 8;
+  __shared__ __attribute__((aligned(1024))) char lds[kAbKeys * KROW + kAbPages * VPAGE];
+  char* const vlds = lds;                     // V, key-major rows in ab_row order
+  char* const ktlds = lds + kAbKeys * KROW;   // K^T, 16-key pages
   const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
   const int L = a.env_len[env], row0 = a.env_row0[env];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = lane % LPK, grp = lane / LPK;  // feature chunk, key slot of the step
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nch = (L + 31) / 32;
   const int32_t* pt = a.page_table + env * a.max_pages;
-  // K rows (key-major in the cache) and V (feature-major pages) into key-major LDS
-  for (int i = tid; i < L * (HD / 8); i += 64 * kBwdWaves) {
-    const int j = i / (HD / 8), cc = i % (HD / 8);
-    const int page = pt[j / kPage], slot = j % kPage;
-    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * cc;
-    *reinterpret_cast<uint4*>(ks + (j * (HD / 8) + (cc ^ bwd_swz<HD>(j))) * 8) = *reinterpret_cast<const uint4*>(kp);
-    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * cc) * kPage + slot;
-    bf16_t v8[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v8[e] = vp[e * kPage];
-    uint4 o;
-    o.x = v8[0] | (uint32_t(v8[1]) << 16); o.y = v8[2] | (uint32_t(v8[3]) << 16);
-    o.z = v8[4] | (uint32_t(v8[5]) << 16); o.w = v8[6] | (uint32_t(v8[7]) << 16);
-    *reinterpret_cast<uint4*>(vs + (j * (HD / 8) + (cc ^ bwd_swz<HD>(j))) * 8) = o;
-  }
-  __syncthreads();
-  for (int t = wave; t < L; t += kBwdWaves) {
-    const int row = row0 + t;
-    float q8[8], do8[8], o8[8];
-    unpack8(*reinterpret_cast<const uint4*>(a.q + (size_t)row * a.d + head * HD + 8 * c), q8);
-    unpack8(*reinterpret_cast<const uint4*>(a.o + frag_index(row, head * HD + 8 * c, a.d)), o8);
-    const float* dp = a.dout + (size_t)row * a.d + head * HD + 8 * c;
-    float dd = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      do8[e] = bf2f(f2bf(dp[e]));  // dO as the bf16 operand it is in pass 2
-      dd += do8[e] * o8[e];
-    }
-    dd = group_sum<LPK>(dd);  // D_t = dO_t . O_t
-    float* st = a.stats + ((size_t)row * H + head) * 2;
-    const float lse = st[0];
-    if (lane == 0) st[1] = dd;
-    float dq[8] = {};
-    for (int j0 = 0; j0 <= t; j0 += RPS) {
-      const int j = j0 + grp;
-      const int jj = min(j, t);  // rows past t read a valid row and contribute 0
-      float k8[8], v8[8];
-      lds_chunk<HD>(ks, jj, c, k8);
-      lds_chunk<HD>(vs, jj, c, v8);
-      float sp = 0.f, dpv = 0.f;
+  // fill: task (8-key group kg, feature chunk fc); keys >= L are zero
+  for (int i = threadIdx.x; i < nch * 4 * HC; i += 64 * kAbWaves) {
+    const int kg = i / HC, fc = i % HC, k0 = 8 * kg;
+    uint4 vin[8], kin[8], vout[8], kout[8];
+    if (k0 < L) {
+      const int page = pt[kg >> 1], h = kg & 1;
+      const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * fc) * kPage + 8 * h;
+      const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + 8 * h) * HD + 8 * fc;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        sp += q8[e] * k8[e];
-        dpv += do8[e] * v8[e];
+        vin[e] = *reinterpret_cast<const uint4*>(vp + e * kPage);            // feature 8 fc + e, keys k0 ..
+        kin[e] = k0 + e < L ? *reinterpret_cast<const uint4*>(kp + e * HD)  // key k0 + e, features 8 fc ..
+                            : make_uint4(0, 0, 0, 0);
       }
-      sp = group_sum<LPK>(sp);
-      dpv = group_sum<LPK>(dpv);
-      const float p = j <= t ? expf(a.scale * sp - lse) : 0.f;
-      const float ds = p * (dpv - dd);
+    } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) dq[e] += ds * k8[e];
+      for (int e = 0; e < 8; ++e) vin[e] = kin[e] = make_uint4(0, 0, 0, 0);
     }
+    transpose8(vin, vout);  // vout[b]: key k0 + b, features 8 fc ..
+    transpose8(kin, kout);  // kout[e]: feature 8 fc + e, keys k0 ..
 #pragma unroll
-    for (int e = 0; e < 8; ++e) dq[e] = a.scale * across_groups<LPK>(dq[e]);
-    if (grp == 0) bwd_store_rot8<HD>(a, row, t, head, 0, c, dq);
+    for (int b = 0; b < 8; ++b) {
+      const int R = ab_slot(k0 + b);
+      *reinterpret_cast<uint4*>(vlds + R * KROW + 16 * (fc ^ ab_swz<HD>(R))) =
+          k0 + b < L ? vout[b] : make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(ktlds + ab_page_off<HD>(kg >> 1, 8 * fc + b, kg & 1)) = kout[b];
+    }
+  }
+  // the environment's page table, one entry per lane (<= 20 pages)
+  const int ptv = pt[min(lane, a.max_pages - 1)];
+  __syncthreads();
+  const int nq = (L + 15) / 16;
+  for (int p0 = 0; p0 < nq; p0 += kAbWaves) {  // most expensive tiles first, snake order
+    const int p = p0 + (((p0 / kAbWaves) & 1) ? kAbWaves - 1 - wave : wave);
+    if (p < nq) ab_dq_tile<HD>(a, vlds, ktlds, ptv, nq - 1 - p, L, row0, head, lane);
+  }
+}
+
+// pass 2, one 16-key tile: keys 16 kt .. 16 kt + 15, queries in chunks kt / 2 .. nch - 1
+template <int HD>
+__device__ __forceinline__ void ab_dkv_tile(const AttnBwdArgs& a, const char* qtl, const char* otl, const int32_t* pt,
+                                            int kt, int L, int nch, int row0, int head, int lane) {
+  constexpr int KS = HD / 32, NB = HD / 16;
+  const int r16 = lane & 15, g = lane >> 4, H = a.n_heads;
+  const int key = kt * 16 + r16, kc = min(key, L - 1);
+  // B operands: key `key`, features 32 ks + 8 g .. + 8
+  uint4 kf[KS], vf[KS];
+  {
+    const int page = pt[kc / kPage], slot = kc % kPage;
+    const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * g;
+    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * g) * kPage + slot;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kf[ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
+      bf16_t v8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v8[e] = vp[(32 * ks + e) * kPage];
+      vf[ks] = make_uint4(v8[0] | (uint32_t(v8[1]) << 16), v8[2] | (uint32_t(v8[3]) << 16),
+                          v8[4] | (uint32_t(v8[5]) << 16), v8[6] | (uint32_t(v8[7]) << 16));
+    }
+  }
+  f32x4 dk[NB], dv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) dk[nb] = dv[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c = kt / 2; c < nch; ++c) {
+    f32x4 s[2], dp[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // A operand row r16 of tile t: query 32 c + 8 (r16 / 4) + 4 t + r16 % 4 (clamped)
+      const int qi = min(32 * c + 8 * (r16 >> 2) + 4 * t + (r16 & 3), L - 1);
+      const size_t at = (size_t)(row0 + qi) * a.d + head * HD + 8 * g;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        s[t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(a.q + at + 32 * ks)), as_bf16x8(kf[ks]), s[t]);
+        dp[t] = mfma16(as_bf16x8(*reinterpret_cast<const uint4*>(a.do16 + at + 32 * ks)), as_bf16x8(vf[ks]), dp[t]);
+      }
+    }
+    // lane: key `key`, queries 32 c + 8 g + 4 t + r -> P and dS as B operands (hi + lo)
+    bf16x8 phi, plo, shi, slo;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int qq = 32 * c + 8 * g + 4 * t + r;
+        const float2 ld = *reinterpret_cast<const float2*>(a.stats + ((size_t)(row0 + min(qq, L - 1)) * H + head) * 2);
+        const bool live = qq >= key && qq < L;
+        const float p = live ? expf(a.scale * s[t][r] - ld.x) : 0.f;
+        const float ds = live ? p * (dp[t][r] - ld.y) : 0.f;
+        split_bf16(p, phi, plo, 4 * t + r);
+        split_bf16(ds, shi, slo, 4 * t + r);
+      }
+    // dV^T += dO^T P, dK^T += Q^T dS: A operands = rows 16 nb + r16 of the transposed tiles,
+    // queries 32 c + 8 g .. + 8
+    const int off = ab_page_off<HD>(2 * c + (g >> 1), r16, g & 1);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 ov = as_bf16x8(*reinterpret_cast<const uint4*>(otl + off + nb * 512));
+      const bf16x8 qv = as_bf16x8(*reinterpret_cast<const uint4*>(qtl + off + nb * 512));
+      dv[nb] = mfma16(ov, phi, dv[nb]);
+      dv[nb] = mfma16(ov, plo, dv[nb]);
+      dk[nb] = mfma16(qv, shi, dk[nb]);
+      dk[nb] = mfma16(qv, slo, dk[nb]);
+    }
+  }
+  if (key < L) {
+    const size_t row = (size_t)(row0 + key);
+    const int K3 = 3 * a.d;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      *reinterpret_cast<uint2*>(a.dqkv + frag_index(row, 2 * a.d + head * HD + 16 * nb + 4 * g, K3)) =
+          make_uint2(pack2bf(dv[nb][0], dv[nb][1]), pack2bf(dv[nb][2], dv[nb][3]));
+    ab_store_rot<HD>(a, row, key, head, 1, dk, a.scale, g);
   }
 }
 
 template <int HD>
-__global__ __launch_bounds__(64 * kBwdWaves, 1) void attn_bwd_kv_kernel(AttnBwdArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t qs[kBwdKeys * HD];
-  __shared__ __attribute__((aligned(16))) bf16_t os[kBwdKeys * HD];  // dO rounded to bf16
-  constexpr int LPK = HD / 8, RPS = 64 / LPK;
-  const int env = blockIdx.x, head = blockIdx.y, H = a.n_heads;
+__global__ __launch_bounds__(64 * kAbWaves, 1) void attn_bwd_dkv_kernel(AttnBwdArgs a) {
+  constexpr int VPAGE = HD * kPage * 2, HC = HD / 8;
+  __shared__ __attribute__((aligned(1024))) char lds[2 * kAbPages * VPAGE];
+  char* const qtl = lds;                   // Q^T, 16-query pages
+  char* const otl = lds + kAbPages * VPAGE;  // dO^T (bf16), 16-query pages
+  const int env = blockIdx.x, head = blockIdx.y;
   const int L = a.env_len[env], row0 = a.env_row0[env];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = lane % LPK, grp = lane / LPK;
-  const int32_t* pt = a.page_table + env * a.max_pages;
-  for (int i = tid; i < L * (HD / 8); i += 64 * kBwdWaves) {
-    const int t = i / (HD / 8), cc = i % (HD / 8);
-    const int at = (t * (HD / 8) + (cc ^ bwd_swz<HD>(t))) * 8;
-    *reinterpret_cast<uint4*>(qs + at) =
-        *reinterpret_cast<const uint4*>(a.q + (size_t)(row0 + t) * a.d + head * HD + 8 * cc);
-    const float* dp = a.dout + (size_t)(row0 + t) * a.d + head * HD + 8 * cc;
-    const float4 x0 = *reinterpret_cast<const float4*>(dp), x1 = *reinterpret_cast<const float4*>(dp + 4);
-    uint4 o;
-    o.x = pack2bf(x0.x, x0.y); o.y = pack2bf(x0.z, x0.w); o.z = pack2bf(x1.x, x1.y); o.w = pack2bf(x1.z, x1.w);
-    *reinterpret_cast<uint4*>(os + at) = o;
-  }
-  __syncthreads();
-  for (int j = wave; j < L; j += kBwdWaves) {
-    const int page = pt[j / kPage], slot = j % kPage;
-    float k8[8], v8[8];
-    unpack8(*reinterpret_cast<const uint4*>(a.kv.k + (((size_t)page * H + head) * kPage + slot) * HD + 8 * c), k8);
-    const bf16_t* vp = a.kv.v + (((size_t)page * H + head) * HD + 8 * c) * kPage + slot;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v8[e] = bf2f(vp[e * kPage]);
-    float dk[8] = {}, dv[8] = {};
-    for (int t0 = j; t0 < L; t0 += RPS) {
-      const int t = t0 + grp;
-      const int tt = min(t, L - 1);
-      float q8[8], o8[8];
-      lds_chunk<HD>(qs, tt, c, q8);
-      lds_chunk<HD>(os, tt, c, o8);
-      float sp = 0.f, dpv = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sp += q8[e] * k8[e];
-        dpv += o8[e] * v8[e];
-      }
-      sp = group_sum<LPK>(sp);
-      dpv = group_sum<LPK>(dpv);
-      const float* st = a.stats + ((size_t)(row0 + tt) * H + head) * 2;
-      const float p = t < L ? expf(a.scale * sp - st[0]) : 0.f;
-      const float ds = p * (dpv - st[1]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        dk[e] += ds * q8[e];
-        dv[e] += p * o8[e];
-      }
-    }
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nch = (L + 31) / 32;
+  // fill: task (8-query group kg, feature chunk fc); queries >= L are zero
+  for (int i = threadIdx.x; i < nch * 4 * HC; i += 64 * kAbWaves) {
+    const int kg = i / HC, fc = i % HC, t0 = 8 * kg;
+    uint4 qin[8], oin[8], qout[8], oout[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      dk[e] = a.scale * across_groups<LPK>(dk[e]);
-      dv[e] = across_groups<LPK>(dv[e]);
+      const size_t at = (size_t)(row0 + t0 + e) * a.d + head * HD + 8 * fc;
+      const bool in = t0 + e < L;
+      qin[e] = in ? *reinterpret_cast<const uint4*>(a.q + at) : make_uint4(0, 0, 0, 0);
+      oin[e] = in ? *reinterpret_cast<const uint4*>(a.do16 + at) : make_uint4(0, 0, 0, 0);
     }
-    if (grp == 0) {
-      const int row = row0 + j, K3 = 3 * a.d;
+    transpose8(qin, qout);
+    transpose8(oin, oout);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) a.dqkv[frag_index(row, 2 * a.d + head * HD + 8 * c + e, K3)] = f2bf(dv[e]);
-      bwd_store_rot8<HD>(a, row, j, head, 1, c, dk);
+    for (int b = 0; b < 8; ++b) {
+      const int off = ab_page_off<HD>(kg >> 1, 8 * fc + b, kg & 1);
+      *reinterpret_cast<uint4*>(qtl + off) = qout[b];
+      *reinterpret_cast<uint4*>(otl + off) = oout[b];
     }
+  }
+  __syncthreads();
+  const int nq = (L + 15) / 16;
+  const int32_t* pt = a.page_table + env * a.max_pages;
+  for (int p0 = 0; p0 < nq; p0 += kAbWaves) {  // most expensive (earliest) key tiles first, snake order
+    const int p = p0 + (((p0 / kAbWaves) & 1) ? kAbWaves - 1 - wave : wave);
+    if (p < nq) ab_dkv_tile<HD>(a, qtl, otl, pt, p, L, nch, row0, head, lane);
   }
 }
 
-// ---- LoRA gradients from a weight gradient ---------------------------------------
+// ---- LoRA gradients ---------------------------------------
 // LoRA gradients (W = W0 + s B A): with T1 = X A^T and T2 = dY B over the M rows,
 // dL/dB = s dY^T T1 and dL/dA = s T2^T X, the rank-r reductions of dL/dW = dY^T X
 // taken without forming it.  Output o of a projection sits at column o0 + o of the
@@ -436,13 +580,14 @@ hipError_t launch_move_rows(const float* src, const int32_t* rows, int R, int d,
 
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s) {
   if (a.n_env <= 0) return hipSuccess;
-  const dim3 grid(a.n_env, a.n_heads), block(64 * kBwdWaves);
+  if (a.max_pages < 1 || a.max_pages > 64 || !a.do16) return hipErrorInvalidValue;
+  const dim3 grid(a.n_env, a.n_heads), block(64 * kAbWaves);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL(attn_bwd_q_kernel<128>, grid, block, 0, s, a);
-    hipLaunchKernelGGL(attn_bwd_kv_kernel<128>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<128>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_dkv_kernel<128>, grid, block, 0, s, a);
   } else if (a.head_dim == 64) {
-    hipLaunchKernelGGL(attn_bwd_q_kernel<64>, grid, block, 0, s, a);
-    hipLaunchKernelGGL(attn_bwd_kv_kernel<64>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<64>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, grid, block, 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

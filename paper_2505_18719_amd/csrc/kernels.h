@@ -308,13 +308,14 @@ struct AttnBwdArgs {
   const int32_t* page_table;
   int max_pages;
   const int32_t* env_row0;
-  const int32_t* env_len;  // <= 320
+  const int32_t* env_len;  // <= 320 rows (max_pages <= 64)
   int n_env, d, n_heads, head_dim;
   float scale;
   const float2* rope;     // [pos][head_dim / 2] (cos, sin)
   float* stats;           // [M, n_heads, 2]: log-sum-exp of each query row (from the forward's
                           // PrefillAttnArgs::lse) in, D_t = dO_t . O_t written by the first pass
   bf16_t* dqkv;           // [M, 3 d] bf16 frag (K = 3 d): gradients of q, k (before rotation, packed order), v
+  bf16_t* do16;           // [M, d] row-major scratch: dO rounded to bf16 (written by the first pass)
 };
 hipError_t launch_attn_bwd(const AttnBwdArgs& a, hipStream_t s);
 // LoRA gradients of one projection by the low-rank route: with X its input rows and

@@ -408,7 +408,7 @@ struct TrainBufs {
   std::vector<float*> xs;  // per-layer input residual [Mmax, d]
   float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp;
   float *t1, *t2, *cres, *spart;  // low-rank products and skinny-GEMM partials
-  bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t, *apk, *bpt, *t1f, *t2f;
+  bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t, *apk, *bpt, *t1f, *t2f, *do16;
 };
 
 void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
@@ -448,6 +448,7 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   t.hb = L.take<bf16_t>(frag_elems(Mx64, D.Fp));
   t.dgu = L.take<bf16_t>(frag_elems(Mx64, 2 * D.Fp));
   t.dqkv = L.take<bf16_t>(frag_elems(Mx64, 3 * D.d));
+  t.do16 = L.take<bf16_t>(Mx * d);
   t.wt = L.take<bf16_t>(std::max(std::max(frag_elems(D.Fp, D.d), frag_elems(D.d, 2 * D.Fp)),
                                  std::max(frag_elems(D.d, D.d), frag_elems(D.d, 3 * D.d))));
   t.xt = L.take<bf16_t>(frag_elems(std::max(D.d, D.Fp), Mk));
@@ -505,7 +506,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   VLA_CK(launch_transpose_frag(w.wo, false, d, d, d, d, t.wt, s));
   VLA_CK(gemm_f32(t.dxmf, 0, t.wt, 0, M, d, d, t.dob, d, s));
   AttnBwdArgs ab{m->q, t.ob, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
-                 m->scale, m->rope, t.stats, t.dqkv};
+                 m->scale, m->rope, t.stats, t.dqkv, t.do16};
   VLA_CK(launch_attn_bwd(ab, s));
   VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
   VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
