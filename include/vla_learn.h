@@ -87,10 +87,19 @@ typedef struct vla_lora {
   float* const* grad_b;    /* fp32 [out, rank] out: dL/dB */
 } vla_lora;
 
+/* Training modes, by what the forward of vla_ppo_lora_grads keeps per layer. */
+#define VLA_TRAIN_RECOMPUTE 0 /* the layer's input only; the backward recomputes the layer's
+                                 forward from it before its gradients */
+#define VLA_TRAIN_KEEP 1      /* also the normed inputs, rotated queries, attention output and
+                                 log-sum-exp, mid residual and fp32 gate/up pre-activations:
+                                 no recompute (about 2.9 GB per layer at d = 4096, d_ffn =
+                                 11008 and 64 x 320 rows) */
+
 /* Bytes of the training workspace vla_ppo_lora_grads needs for a handle of
- * this configuration (the inputs of every layer for max_batch * max_seq rows,
- * one layer's activations and gradients, transposed operands). */
-int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
+ * this configuration in `mode` (VLA_TRAIN_*), for max_batch * max_seq rows:
+ * what the forward keeps per layer, one layer's gradients, transposed
+ * operands.  Unknown mode: VLA_EINVAL. */
+int vla_train_workspace_size(const vla_config* cfg, int32_t mode, size_t* bytes_host);
 
 /* Gradient of one PPO update (Eq. 2, Sec. 3.3 Learning Phase) with respect to
  * the LoRA factors.  The handle's packed weights must be the policy being
@@ -100,9 +109,9 @@ int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
  * action log-probabilities (vla_ppo_clip) and its gradient down to the
  * action logits (vla_logprob_backward), then the backward of the whole pass:
  * the head and final RMSNorm of the scoring rows, and for each layer from the
- * top a recompute of its forward from its saved input, the gradient GEMMs
- * against its transposed weights, RMSNorm, SwiGLU and causal-attention (with
- * rotary) backward, and the LoRA gradients dL/dB = scale dY^T (X A^T),
+ * top (after recomputing its forward from its input in VLA_TRAIN_RECOMPUTE
+ * mode) the gradient GEMMs against its transposed weights, RMSNorm, SwiGLU
+ * and causal-attention (with rotary) backward, and the LoRA gradients dL/dB = scale dY^T (X A^T),
  * dL/dA = scale (dY B)^T X of each adapted projection (X its input rows, dY
  * the gradient of its output rows: the rank-r reductions of its weight
  * gradient dY^T X, taken without forming it).
@@ -112,7 +121,10 @@ int vla_train_workspace_size(const vla_config* cfg, size_t* bytes_host);
  *   advantages   fp32 [batch]
  *   eps, temperature  clipping parameter (>= 0) and sampling temperature (> 0)
  *   lora         adapters and gradient buffers (see vla_lora)
- *   train_ws     device memory of >= vla_train_workspace_size bytes, 256-byte aligned
+ *   train_ws     device memory, 256-byte aligned: with at least
+ *                vla_train_workspace_size(VLA_TRAIN_KEEP) bytes the call keeps every
+ *                layer's activations, else with at least the VLA_TRAIN_RECOMPUTE size
+ *                it recomputes them (same results, bit for bit), else VLA_EWORKSPACE
  *   stats        fp32 [2] out: loss -J and clipped fraction
  *   logp_new     fp32 [batch, n_actions] out, or NULL: the teacher-forced log-probs
  * Gradient operands of the GEMMs, and the rank-r products X A^T and

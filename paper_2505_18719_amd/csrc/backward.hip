@@ -41,17 +41,28 @@ __global__ __launch_bounds__(256) void transpose_frag_kernel(const void* __restr
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int rr = tid / 8 + 32 * h, kk = (tid % 8) * 8;
-    const int r = r0 + rr;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int k = k0 + kk + e;
-      float v = 0.f;
-      if (r < R && k < K) {
-        if (SRC_F32) v = static_cast<const float*>(src)[(size_t)r * ld + k];
-        else v = bf2f(static_cast<const bf16_t*>(src)[frag_index(r, k, ld)]);
+    const int r = r0 + rr, k = k0 + kk;
+    float v[8];
+    if (r < R && k + 8 <= K) {  // 8 consecutive k: one 16-byte frag chunk, or two float4
+      if (SRC_F32) {
+        const float* p = static_cast<const float*>(src) + (size_t)r * ld + k;
+        const float4 a0 = *reinterpret_cast<const float4*>(p), a1 = *reinterpret_cast<const float4*>(p + 4);
+        v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w; v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+      } else {
+        unpack8(*reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(src) + frag_index(r, k, ld)), v);
       }
-      t[rr][kk + e] = v;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] = 0.f;
+        if (r < R && k + e < K) {
+          if (SRC_F32) v[e] = static_cast<const float*>(src)[(size_t)r * ld + k + e];
+          else v[e] = bf2f(static_cast<const bf16_t*>(src)[frag_index(r, k + e, ld)]);
+        }
+      }
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[rr][kk + e] = v[e];
   }
   __syncthreads();
   // store: thread writes 8 consecutive destination columns (source rows) of one destination row
@@ -75,20 +86,39 @@ __global__ __launch_bounds__(256) void transpose_frag_kernel(const void* __restr
 
 // RMSNorm backward of y = x r g, r = (mean(x^2) + eps)^(-1/2), for one row per
 // workgroup: dx = dres + r (g dy) - x r^3 (sum x g dy) / d.  dres may be null;
-// dx_frag (bf16 frag, K = d) may be null.
+// dx_frag (bf16 frag, K = d) may be null.  The row stays in registers: thread t
+// takes features 8 (t + 256 j) .. + 8, j < kRmsBwdSteps (d <= 8192, d % 8 == 0).
+constexpr int kRmsBwdSteps = 4;
+__device__ __forceinline__ void load8(const float* p, float* v) {
+  const float4 a0 = *reinterpret_cast<const float4*>(p), a1 = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w; v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+}
+__device__ __forceinline__ void store8(float* p, const float* v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
 __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restrict__ x, const float* __restrict__ g,
                                                           float eps, const float* __restrict__ dy,
                                                           const float* __restrict__ dres, float* __restrict__ dx,
                                                           bf16_t* __restrict__ dx_frag, int d) {
   __shared__ float red[2][4];
   const int row = blockIdx.x, tid = threadIdx.x;
-  const float* xr = x + (size_t)row * d;
-  const float* dyr = dy + (size_t)row * d;
+  const size_t base = (size_t)row * d;
+  float xv[kRmsBwdSteps][8], gv[kRmsBwdSteps][8], dv[kRmsBwdSteps][8];
   float ss = 0.f, dot = 0.f;
-  for (int k = tid; k < d; k += 256) {
-    const float xv = xr[k];
-    ss += xv * xv;
-    dot += xv * g[k] * dyr[k];
+#pragma unroll
+  for (int j = 0; j < kRmsBwdSteps; ++j) {
+    const int k = 8 * (tid + 256 * j);
+    if (k < d) {
+      load8(x + base + k, xv[j]);
+      load8(g + k, gv[j]);
+      load8(dy + base + k, dv[j]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ss += xv[j][e] * xv[j][e];
+        dot += xv[j][e] * gv[j][e] * dv[j][e];
+      }
+    }
   }
   ss = wave_sum(ss);
   dot = wave_sum(dot);
@@ -101,56 +131,73 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restric
   dot = red[1][0] + red[1][1] + red[1][2] + red[1][3];
   const float r = 1.f / sqrtf(ss / d + eps);
   const float c = r * r * r * dot / d;
-  for (int k = 8 * tid; k < d; k += 8 * 256) {
-    float v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const size_t i = (size_t)row * d + k + e;
-      v[e] = (dres ? dres[i] : 0.f) + r * g[k + e] * dy[i] - xr[k + e] * c;
-      dx[i] = v[e];
-    }
-    if (dx_frag) {
-      uint4 o;
-      o.x = pack2bf(v[0], v[1]);
-      o.y = pack2bf(v[2], v[3]);
-      o.z = pack2bf(v[4], v[5]);
-      o.w = pack2bf(v[6], v[7]);
-      *reinterpret_cast<uint4*>(dx_frag + frag_index(row, k, d)) = o;
-    }
+  for (int j = 0; j < kRmsBwdSteps; ++j) {
+    const int k = 8 * (tid + 256 * j);
+    if (k >= d) continue;
+    float rv[8], v[8];
+    if (dres) load8(dres + base + k, rv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (dres ? rv[e] : 0.f) + r * gv[j][e] * dv[j][e] - xv[j][e] * c;
+    store8(dx + base + k, v);
+    if (dx_frag)
+      *reinterpret_cast<uint4*>(dx_frag + frag_index(row, k, d)) =
+          make_uint4(pack2bf(v[0], v[1]), pack2bf(v[2], v[3]), pack2bf(v[4], v[5]), pack2bf(v[6], v[7]));
   }
 }
 
 // SwiGLU backward for h = silu(g) up, with g, up the fp32 gate/up pre-activations
 // in the packed interleaved order (columns 64 (j / 32) + j % 32 and +32 of cgu) and
 // dh fp32 [M, F] (row stride ldh): writes d[g; up] as bf16 frag in that same order
-// (K = 2 Fp) and the forward h = bf16(silu(g) up) as bf16 frag (K = Fp).
-__global__ void swiglu_bwd_kernel(const float* __restrict__ cgu, int ldc, const float* __restrict__ dh, int ldh,
-                                  int M, int F, int Fp, bf16_t* __restrict__ dgu, bf16_t* __restrict__ h) {
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const int fc = Fp / 8;  // 8-feature chunks per row
-  if (i >= (size_t)M * fc) return;
-  const int m = (int)(i / fc), j0 = (int)(i % fc) * 8;  // features j0 .. j0 + 7 (one 32-block)
-  const int cg = 64 * (j0 / 32) + j0 % 32;
-  float dgv[8], duv[8], hv[8];
+// (K = 2 Fp) and the forward h = bf16(silu(g) up) as bf16 frag (K = Fp); with dh
+// null only h is written (the forward of a pass that keeps the pre-activations).  A wave
+// takes one 16-row x 32-feature block, lane (r, u) rows 16 mb + r and features
+// 32 jb + 8 u .. + 8, so each of its three stores is one contiguous 1 KB frag
+// block; rows >= M of the last block are written as zeros.
+__global__ __launch_bounds__(256) void swiglu_bwd_kernel(const float* __restrict__ cgu, int ldc,
+                                                         const float* __restrict__ dh, int ldh, int M, int F, int Fp,
+                                                         bf16_t* __restrict__ dgu, bf16_t* __restrict__ h) {
+  const int nj = Fp / 32;
+  const size_t w = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= (size_t)((M + 15) / 16) * nj) return;
+  const int mb = (int)(w / nj), jb = (int)(w % nj), lane = threadIdx.x & 63;
+  const int m = 16 * mb + (lane & 15), j0 = 32 * jb + 8 * (lane >> 4);
+  const int cg = 64 * jb + 8 * (lane >> 4);
+  float dgv[8], duv[8], hv[8], gv[8], uv[8], dv[8];
+  const float* cr = cgu + (size_t)m * ldc + cg;
+  if (m < M && j0 + 8 <= F) {
+    load8(cr, gv);
+    load8(cr + 32, uv);
+    if (dh) load8(dh + (size_t)m * ldh + j0, dv);
+  } else {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int j = j0 + e;
-    if (j < F) {
-      const float gg = cgu[(size_t)m * ldc + cg + e], up = cgu[(size_t)m * ldc + cg + 32 + e];
-      const float s = 1.f / (1.f + expf(-gg));
-      const float d = dh[(size_t)m * ldh + j];
-      dgv[e] = d * up * s * (1.f + gg * (1.f - s));
-      duv[e] = d * gg * s;
-      hv[e] = gg / (1.f + expf(-gg)) * up;  // the forward epilogue's expression
-    } else {
-      dgv[e] = duv[e] = hv[e] = 0.f;
+    for (int e = 0; e < 8; ++e) {
+      const bool in = m < M && j0 + e < F;
+      gv[e] = in ? cr[e] : 0.f;
+      uv[e] = in ? cr[32 + e] : 0.f;
+      if (dh) dv[e] = in ? dh[(size_t)m * ldh + j0 + e] : 0.f;
     }
   }
+  if (!dh) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dv[e] = 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float gg = gv[e], up = uv[e];
+    const float s = 1.f / (1.f + expf(-gg));
+    const float d = dv[e];
+    dgv[e] = d * up * s * (1.f + gg * (1.f - s));
+    duv[e] = d * gg * s;
+    hv[e] = gg / (1.f + expf(-gg)) * up;  // the forward epilogue's expression
+  }
   uint4 o;
-  o.x = pack2bf(dgv[0], dgv[1]); o.y = pack2bf(dgv[2], dgv[3]); o.z = pack2bf(dgv[4], dgv[5]); o.w = pack2bf(dgv[6], dgv[7]);
-  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg, 2 * Fp)) = o;
-  o.x = pack2bf(duv[0], duv[1]); o.y = pack2bf(duv[2], duv[3]); o.z = pack2bf(duv[4], duv[5]); o.w = pack2bf(duv[6], duv[7]);
-  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg + 32, 2 * Fp)) = o;
+  if (dh) {
+    o.x = pack2bf(dgv[0], dgv[1]); o.y = pack2bf(dgv[2], dgv[3]); o.z = pack2bf(dgv[4], dgv[5]); o.w = pack2bf(dgv[6], dgv[7]);
+    *reinterpret_cast<uint4*>(dgu + frag_index(m, cg, 2 * Fp)) = o;
+    o.x = pack2bf(duv[0], duv[1]); o.y = pack2bf(duv[2], duv[3]); o.z = pack2bf(duv[4], duv[5]); o.w = pack2bf(duv[6], duv[7]);
+    *reinterpret_cast<uint4*>(dgu + frag_index(m, cg + 32, 2 * Fp)) = o;
+  }
   o.x = pack2bf(hv[0], hv[1]); o.y = pack2bf(hv[2], hv[3]); o.z = pack2bf(hv[4], hv[5]); o.w = pack2bf(hv[6], hv[7]);
   *reinterpret_cast<uint4*>(h + frag_index(m, j0, Fp)) = o;
 }
@@ -616,7 +663,7 @@ hipError_t launch_transpose_frag(const void* src, bool src_f32, int ld, int R, i
 hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const float* dy, const float* dres,
                               float* dx, bf16_t* dx_frag, int M, int d, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (d % 8 != 0) return hipErrorInvalidValue;
+  if (d % 8 != 0 || d > 8 * 256 * kRmsBwdSteps) return hipErrorInvalidValue;
   hipLaunchKernelGGL(rmsnorm_bwd_kernel, dim3(M), dim3(256), 0, s, x, g, eps, dy, dres, dx, dx_frag, d);
   return hipGetLastError();
 }
@@ -624,10 +671,10 @@ hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const f
 hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
                              bf16_t* h, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (Fp % 32 != 0 || F > Fp) return hipErrorInvalidValue;
-  const size_t work = (size_t)M * (Fp / 8);
-  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, cgu, ldc, dh, ldh, M,
-                     F, Fp, dgu, h);
+  if (Fp % 32 != 0 || F > Fp || !cgu || !h || (dh && !dgu)) return hipErrorInvalidValue;
+  const size_t waves = (size_t)((M + 15) / 16) * (Fp / 32);
+  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, cgu, ldc, dh, ldh, M, F,
+                     Fp, dgu, h);
   return hipGetLastError();
 }
 

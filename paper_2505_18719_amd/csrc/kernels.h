@@ -297,7 +297,7 @@ hipError_t launch_transpose_frag(const void* src, bool src_f32, int ld, int R, i
 hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const float* dy, const float* dres,
                               float* dx, bf16_t* dx_frag, int M, int d, hipStream_t s);
 // SwiGLU backward from the fp32 interleaved gate/up pre-activations and dh: d[g; up] (bf16 frag,
-// K = 2 Fp, the packed interleaved order) and the forward h (bf16 frag, K = Fp)
+// K = 2 Fp, the packed interleaved order) and the forward h (bf16 frag, K = Fp); dh null: h only
 hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
                              bf16_t* h, hipStream_t s);
 struct AttnBwdArgs {

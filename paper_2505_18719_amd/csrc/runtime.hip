@@ -277,8 +277,19 @@ int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t
 // teacher-forced (each environment's rows extended by its action tokens).
 // save_x (training): per-layer device buffers that receive each layer's input
 // residual; a training pass computes every row of the last layer.
+// Activations a training forward keeps per layer: the layer input always; with
+// `full` also everything the backward would otherwise recompute from it.
+struct SavedActs {
+  std::vector<float*> xs;              // input residual [Mmax, d]
+  bool full = false;
+  std::vector<bf16_t*> u1, q, ob, u2;  // attention-norm output (frag), rotated queries (row-major),
+                                       // attention output (frag), MLP-norm output (frag)
+  std::vector<float*> xm, cgu, lse;    // mid residual [Mmax, d], gate/up pre-activations
+                                       // [Mmax, 2 Fp] (interleaved), log-sum-exp stats [Mmax, H, 2]
+};
+
 int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, const int32_t* lens_host,
-            const int32_t* actions, hipStream_t s, int* out_rows, float* const* save_x = nullptr,
+            const int32_t* actions, hipStream_t s, int* out_rows, const SavedActs* sv = nullptr,
             int* out_M = nullptr) {
   const Dims& D = m->D;
   const bool tf = actions != nullptr;
@@ -342,14 +353,15 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   VLA_CK(launch_embed(ea, s));
   const float eps = m->cfg.rms_eps;
   // the prefill GEMMs read their activations (u, attention output, h) in frag layout
-  VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
+  const bool full = sv && sv->full;
+  VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[0].attn_norm, eps, full ? sv->u1[0] : m->u, D.d, Mi, D.d, s, true));
   const int n_layers = m->layer_limit > 0 ? std::min(m->layer_limit, D.L) : D.L;
   // Only the rows read afterwards (head_rows: the last prefix row, or the n_actions
   // scoring rows, of each environment) need the last layer's output; its other rows
   // only feed the KV cache through the QKV projection.  Every row's computation is
   // independent of which other rows run with it, so results are the same bits.
   // (A layer limit set through the debug interface computes every row.)
-  const bool prune = m->layer_limit == 0 && save_x == nullptr;
+  const bool prune = m->layer_limit == 0 && sv == nullptr;
   const int R = tf ? B * D.nact : B;
   double attn_flops_last = 0.0;  // q.k and p.v of the needed query rows only
   for (int b = 0; b < B; ++b)
@@ -357,19 +369,20 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     const bool last = prune && l == D.L - 1;
-    if (save_x) VLA_CK(hipMemcpyAsync(save_x[l], m->x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
+    if (sv) VLA_CK(hipMemcpyAsync(sv->xs[l], m->x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
+    bf16_t* const qb = full ? sv->q[l] : m->q;
     GemmArgs g{};
-    g.A = m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
-    g.q = m->q; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
+    g.A = full ? sv->u1[l] : m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
+    g.q = qb; g.ldq = D.d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
     g.d_model = D.d; g.n_heads = D.H; g.head_dim = D.hd;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Mi, 3.0 * D.d, D.d), launch_gemm(g, kEpiQkvRope, s));
-    PrefillAttnArgs pa{m->q, m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
-                       B, D.d, D.H, D.hd, m->scale, last ? m->env_q0 : nullptr};
+    PrefillAttnArgs pa{qb, full ? sv->ob[l] : m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
+                       B, D.d, D.H, D.hd, m->scale, last ? m->env_q0 : nullptr, full ? sv->lse[l] : nullptr};
     PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, last ? attn_flops_last : attn_flops, launch_attn_prefill(pa, s));
     // the rest of the layer runs on all rows, or on the compacted needed rows of the last layer
     const int Ml = last ? R : Mi;
     float* x = m->x;
-    bf16_t* u = m->u;
+    bf16_t* u = full ? sv->ob[l] : m->u;
     bf16_t* hbuf = m->h;
     if (last) {
       VLA_CK(launch_gather_rows(m->x, m->u, m->head_rows, R, D.d, m->xc, m->uc, s));
@@ -380,18 +393,27 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     GemmArgs go{};
     go.A = u; go.W = w.wo; go.M = Ml; go.N = D.d; go.K = D.d; go.C = x; go.ldc = D.d;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.d), launch_gemm(go, kEpiResidual, s));
+    if (full) VLA_CK(hipMemcpyAsync(sv->xm[l], x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
+    if (full) u = sv->u2[l];
     VLA_CK(launch_rmsnorm(x, D.d, nullptr, w.mlp_norm, eps, u, D.d, Ml, D.d, s, true));
     GemmArgs gg{};
     // [gate; up] interleaved in 64-row blocks: only the blocks holding real rows are computed; the
     // down projection's contraction stops at the last real feature (h and Wdown stay Fp wide)
     gg.A = u; gg.W = w.wgu; gg.M = Ml; gg.N = 64 * ((D.F + 31) / 32); gg.K = D.d; gg.H = hbuf; gg.ldh = D.Fp;
-    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
+    if (full) {  // kept fp32 pre-activations, then h from them (the epilogue's expression: same bits)
+      gg.C = sv->cgu[l]; gg.ldc = 2 * D.Fp;
+      PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiStoreF32, s));
+      VLA_CK(launch_swiglu_bwd(sv->cgu[l], 2 * D.Fp, nullptr, 0, Ml, D.F, D.Fp, nullptr, hbuf, s));
+    } else {
+      PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
+    }
     GemmArgs gd{};
     gd.A = hbuf; gd.W = w.wd; gd.M = Ml; gd.N = D.d; gd.K = 32 * ((D.F + 31) / 32); gd.ka = D.Fp; gd.kw = D.Fp;
     gd.C = x; gd.ldc = D.d;
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
     if (l + 1 < D.L)
-      VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, m->u, D.d, Mi, D.d, s, true));
+      VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, full ? sv->u1[l + 1] : m->u, D.d, Mi,
+                            D.d, s, true));
   }
   if (prune)
     VLA_CK(launch_rmsnorm(m->xc, D.d, nullptr, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
@@ -405,13 +427,14 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
 // ---- training (backward of the teacher-forced pass) --------------------------
 // Buffers of the caller's training workspace.
 struct TrainBufs {
-  std::vector<float*> xs;  // per-layer input residual [Mmax, d]
+  SavedActs sv;  // what the forward keeps per layer
   float *dx, *dxm, *du, *dob, *xm, *cgu, *dh, *stats, *dz, *du_h, *xc, *dxc, *logp, *dlogp;
   float *t1, *t2, *cres, *spart;  // low-rank products and skinny-GEMM partials
   bf16_t *dxf, *dxmf, *u1, *ob, *u2, *hb, *dgu, *dqkv, *wt, *xt, *dyt, *dzf, *wact_t, *apk, *bpt, *t1f, *t2f, *do16;
 };
 
-void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
+// keep: every layer's activations are kept by the forward (no recompute in the backward)
+void plan_train(Layout& L, const Dims& D, TrainBufs& t, bool keep) {
   const size_t Mx = D.Mmax, d = D.d;
   // rows padded to 64 (the skinny GEMM's column tiles run over them), the
   // row contraction padded to 256 (its K units)
@@ -419,16 +442,35 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   const int A32 = round_up(D.A, 32), Mk = round_up((int)D.Mmax, 256);
   const int Fg = 64 * ((D.F + 31) / 32), F64 = round_up(D.F, 64);
   const size_t Rh = (size_t)D.Bmax * D.nact;
-  t.xs.resize(D.L);
-  for (int l = 0; l < D.L; ++l) t.xs[l] = L.take<float>(Mx * d);
+  SavedActs& sv = t.sv;
+  sv.full = keep;
+  sv.xs.resize(D.L);
+  for (int l = 0; l < D.L; ++l) sv.xs[l] = L.take<float>(Mx * d);
+  if (keep) {
+    for (int l = 0; l < D.L; ++l) {
+      sv.u1.push_back(L.take<bf16_t>(frag_elems(Mx64, d)));
+      sv.q.push_back(L.take<bf16_t>(Mx * d));
+      sv.ob.push_back(L.take<bf16_t>(frag_elems(Mx64, d)));
+      sv.u2.push_back(L.take<bf16_t>(frag_elems(Mx64, d)));
+      sv.xm.push_back(L.take<float>(Mx * d));
+      sv.cgu.push_back(L.take<float>(Mx * 2 * D.Fp));
+      sv.lse.push_back(L.take<float>(Mx * D.H * 2));
+    }
+    t.xm = t.cgu = t.stats = nullptr;
+    t.u1 = t.ob = t.u2 = nullptr;
+  } else {
+    t.xm = L.take<float>(Mx * d);
+    t.cgu = L.take<float>(Mx * 2 * D.Fp);
+    t.stats = L.take<float>(Mx * D.H * 2);
+    t.u1 = L.take<bf16_t>(frag_elems(Mx64, d));
+    t.ob = L.take<bf16_t>(frag_elems(Mx64, d));
+    t.u2 = L.take<bf16_t>(frag_elems(Mx64, d));
+  }
   t.dx = L.take<float>(Mx * d);
   t.dxm = L.take<float>(Mx * d);
   t.du = L.take<float>(Mx * d);
   t.dob = L.take<float>(Mx * d);
-  t.xm = L.take<float>(Mx * d);
-  t.cgu = L.take<float>(Mx * 2 * D.Fp);
   t.dh = L.take<float>(Mx * D.Fp);
-  t.stats = L.take<float>(Mx * D.H * 2);
   t.dz = L.take<float>(Rh * D.A);
   t.du_h = L.take<float>(Rh * d);
   t.xc = L.take<float>(Rh * d);
@@ -442,9 +484,6 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t) {
   t.spart = L.take<float>((size_t)kMaxSplits * 64 * ncol);
   t.dxf = L.take<bf16_t>(frag_elems(Mx64, d));
   t.dxmf = L.take<bf16_t>(frag_elems(Mx64, d));
-  t.u1 = L.take<bf16_t>(frag_elems(Mx64, d));
-  t.ob = L.take<bf16_t>(frag_elems(Mx64, d));
-  t.u2 = L.take<bf16_t>(frag_elems(Mx64, d));
   t.hb = L.take<bf16_t>(frag_elems(Mx64, D.Fp));
   t.dgu = L.take<bf16_t>(frag_elems(Mx64, 2 * D.Fp));
   t.dqkv = L.take<bf16_t>(frag_elems(Mx64, 3 * D.d));
@@ -478,35 +517,44 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   const float eps = m->cfg.rms_eps;
   const int d = D.d, Fp = D.Fp, F64 = round_up(D.F, 64), Fg = 64 * ((D.F + 31) / 32);
   const int Mp = round_up(M, 64), Mk = round_up(M, 256);
-  // recompute the layer's forward from its saved input
-  VLA_CK(launch_rmsnorm(t.xs[l], d, nullptr, w.attn_norm, eps, t.u1, d, M, d, s, true));
-  GemmArgs g{};
-  g.A = t.u1; g.W = w.wqkv; g.M = M; g.N = 3 * d; g.K = d;
-  g.q = m->q; g.ldq = d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
-  g.d_model = d; g.n_heads = D.H; g.head_dim = D.hd;
-  VLA_CK(launch_gemm(g, kEpiQkvRope, s));
-  PrefillAttnArgs pa{m->q, t.ob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
-                     B, d, D.H, D.hd, m->scale, nullptr, t.stats};
-  VLA_CK(launch_attn_prefill(pa, s));
-  VLA_CK(hipMemcpyAsync(t.xm, t.xs[l], (size_t)M * d * sizeof(float), hipMemcpyDeviceToDevice, s));
-  GemmArgs go{};
-  go.A = t.ob; go.W = w.wo; go.M = M; go.N = d; go.K = d; go.C = t.xm; go.ldc = d;
-  VLA_CK(launch_gemm(go, kEpiResidual, s));
-  VLA_CK(launch_rmsnorm(t.xm, d, nullptr, w.mlp_norm, eps, t.u2, d, M, d, s, true));
-  VLA_CK(gemm_f32(t.u2, 0, w.wgu, 0, M, Fg, d, t.cgu, 2 * Fp, s));
+  const SavedActs& sv = t.sv;
+  const float* const xs = sv.xs[l];
+  // the layer's forward activations: kept by the forward, or recomputed here from its input
+  bf16_t *u1 = t.u1, *ob = t.ob, *u2 = t.u2, *qb = m->q;
+  float *xm = t.xm, *cgu = t.cgu, *stats = t.stats;
+  if (sv.full) {
+    u1 = sv.u1[l]; ob = sv.ob[l]; u2 = sv.u2[l]; qb = sv.q[l];
+    xm = sv.xm[l]; cgu = sv.cgu[l]; stats = sv.lse[l];
+  } else {
+    VLA_CK(launch_rmsnorm(xs, d, nullptr, w.attn_norm, eps, u1, d, M, d, s, true));
+    GemmArgs g{};
+    g.A = u1; g.W = w.wqkv; g.M = M; g.N = 3 * d; g.K = d;
+    g.q = qb; g.ldq = d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
+    g.d_model = d; g.n_heads = D.H; g.head_dim = D.hd;
+    VLA_CK(launch_gemm(g, kEpiQkvRope, s));
+    PrefillAttnArgs pa{qb, ob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
+                       B, d, D.H, D.hd, m->scale, nullptr, stats};
+    VLA_CK(launch_attn_prefill(pa, s));
+    VLA_CK(hipMemcpyAsync(xm, xs, (size_t)M * d * sizeof(float), hipMemcpyDeviceToDevice, s));
+    GemmArgs go{};
+    go.A = ob; go.W = w.wo; go.M = M; go.N = d; go.K = d; go.C = xm; go.ldc = d;
+    VLA_CK(launch_gemm(go, kEpiResidual, s));
+    VLA_CK(launch_rmsnorm(xm, d, nullptr, w.mlp_norm, eps, u2, d, M, d, s, true));
+    VLA_CK(gemm_f32(u2, 0, w.wgu, 0, M, Fg, d, cgu, 2 * Fp, s));
+  }
   // MLP: dh = dy Wd, SwiGLU backward, du2 = d[g; up] Wgu, RMSNorm backward
   VLA_CK(launch_to_frag(t.dx, d, M, d, d, t.dxf, s));
   VLA_CK(launch_transpose_frag(w.wd, false, Fp, d, Fp, d, t.wt, s));
   VLA_CK(gemm_f32(t.dxf, 0, t.wt, 0, M, F64, d, t.dh, Fp, s));
-  VLA_CK(launch_swiglu_bwd(t.cgu, 2 * Fp, t.dh, Fp, M, D.F, Fp, t.dgu, t.hb, s));
+  VLA_CK(launch_swiglu_bwd(cgu, 2 * Fp, t.dh, Fp, M, D.F, Fp, t.dgu, t.hb, s));
   VLA_CK(launch_transpose_frag(w.wgu, false, d, 2 * Fp, d, 2 * Fp, t.wt, s));
   VLA_CK(gemm_f32(t.dgu, 2 * Fp, t.wt, 2 * Fp, M, d, Fg, t.du, d, s));
-  VLA_CK(launch_rmsnorm_bwd(t.xm, w.mlp_norm, eps, t.du, t.dx, t.dxm, t.dxmf, M, d, s));
+  VLA_CK(launch_rmsnorm_bwd(xm, w.mlp_norm, eps, t.du, t.dx, t.dxm, t.dxmf, M, d, s));
   // attention: do = dxm Wo, attention backward, du1 = d[q; k; v] Wqkv
   VLA_CK(launch_transpose_frag(w.wo, false, d, d, d, d, t.wt, s));
   VLA_CK(gemm_f32(t.dxmf, 0, t.wt, 0, M, d, d, t.dob, d, s));
-  AttnBwdArgs ab{m->q, t.ob, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
-                 m->scale, m->rope, t.stats, t.dqkv, t.do16};
+  AttnBwdArgs ab{qb, ob, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
+                 m->scale, m->rope, stats, t.dqkv, t.do16};
   VLA_CK(launch_attn_bwd(ab, s));
   VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
   VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
@@ -544,24 +592,24 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
     return launch_lora_finalize(la, t.cres, in64, false, s);
   };
   if (adapted(VLA_PROJ_Q) || adapted(VLA_PROJ_K) || adapted(VLA_PROJ_V)) {
-    VLA_CK(launch_transpose_frag(t.u1, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(u1, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dqkv, false, 3 * d, M, 3 * d, Mk, t.dyt, s));
     for (int p = VLA_PROJ_Q; p <= VLA_PROJ_V; ++p)
       if (adapted(p))
-        VLA_CK(lowrank(p, t.u1, d, d, t.xt, t.dqkv, 3 * d, t.dyt + frag_index(p * d, 0, Mk), p * d, d, d,
+        VLA_CK(lowrank(p, u1, d, d, t.xt, t.dqkv, 3 * d, t.dyt + frag_index(p * d, 0, Mk), p * d, d, d,
                        p == VLA_PROJ_V ? kPackRows : kPackQk, 0));
   }
   if (adapted(VLA_PROJ_O)) {
-    VLA_CK(launch_transpose_frag(t.ob, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(ob, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dxmf, false, d, M, d, Mk, t.dyt, s));
-    VLA_CK(lowrank(VLA_PROJ_O, t.ob, d, d, t.xt, t.dxmf, d, t.dyt, 0, d, d, kPackRows, 0));
+    VLA_CK(lowrank(VLA_PROJ_O, ob, d, d, t.xt, t.dxmf, d, t.dyt, 0, d, d, kPackRows, 0));
   }
   if (adapted(VLA_PROJ_GATE) || adapted(VLA_PROJ_UP)) {
-    VLA_CK(launch_transpose_frag(t.u2, false, d, M, d, Mk, t.xt, s));
+    VLA_CK(launch_transpose_frag(u2, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dgu, false, 2 * Fp, M, Fg, Mk, t.dyt, s));
     for (int p = VLA_PROJ_GATE; p <= VLA_PROJ_UP; ++p)
       if (adapted(p))
-        VLA_CK(lowrank(p, t.u2, d, d, t.xt, t.dgu, 2 * Fp, t.dyt, 0, Fg, D.F, kPackGateUp, p - VLA_PROJ_GATE));
+        VLA_CK(lowrank(p, u2, d, d, t.xt, t.dgu, 2 * Fp, t.dyt, 0, Fg, D.F, kPackGateUp, p - VLA_PROJ_GATE));
   }
   if (adapted(VLA_PROJ_DOWN)) {
     VLA_CK(launch_transpose_frag(t.hb, false, Fp, M, D.F, Mk, t.xt, s));
@@ -569,7 +617,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
     VLA_CK(lowrank(VLA_PROJ_DOWN, t.hb, Fp, D.F, t.xt, t.dxf, d, t.dyt, 0, d, d, kPackRows, 0));
   }
   // dL/d(layer input) = dxm + RMSNorm backward of du1
-  VLA_CK(launch_rmsnorm_bwd(t.xs[l], w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
+  VLA_CK(launch_rmsnorm_bwd(xs, w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
   return VLA_OK;
 }
 
@@ -885,14 +933,15 @@ int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* 
   return VLA_OK;
 }
 
-int vla_train_workspace_size(const vla_config* cfg, size_t* bytes) {
+int vla_train_workspace_size(const vla_config* cfg, int32_t mode, size_t* bytes) {
   Dims D;
   int rc = check_config(cfg, &D);
   if (rc) return rc;
   if (!bytes) return fail(VLA_EINVAL, "bytes_host is NULL");
+  if (mode != VLA_TRAIN_RECOMPUTE && mode != VLA_TRAIN_KEEP) return fail(VLA_EINVAL, "unknown training mode");
   Layout L;
   TrainBufs t;
-  plan_train(L, D, t);
+  plan_train(L, D, t, mode == VLA_TRAIN_KEEP);
   *bytes = L.off;
   return VLA_OK;
 }
@@ -917,11 +966,19 @@ int vla_ppo_lora_grads(vla_model* m, int32_t B, const void* vis, const int32_t* 
   if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(VLA_EINVAL, "eps must be finite and >= 0");
   if (m->layer_limit != 0) return fail(VLA_ESTATE, "a debug layer limit is set");
   if (reinterpret_cast<uintptr_t>(train_ws) % 256 != 0) return fail(VLA_EWORKSPACE, "training workspace misaligned");
+  // keep every layer's activations when the workspace holds them, else recompute
   Layout L;
   L.base = static_cast<char*>(train_ws);
   TrainBufs t;
-  plan_train(L, D, t);
-  if (train_bytes < L.off) return fail(VLA_EWORKSPACE, "training workspace smaller than vla_train_workspace_size()");
+  plan_train(L, D, t, true);
+  if (train_bytes < L.off) {
+    L = Layout{};
+    L.base = static_cast<char*>(train_ws);
+    t = TrainBufs{};
+    plan_train(L, D, t, false);
+    if (train_bytes < L.off)
+      return fail(VLA_EWORKSPACE, "training workspace smaller than vla_train_workspace_size(VLA_TRAIN_RECOMPUTE)");
+  }
   long long np = 0;
   for (int b = 0; b < B; ++b) np += lens_host[b];
   if (np > 0 && !ids) return fail(VLA_EINVAL, "prompt_ids is NULL");
@@ -929,7 +986,7 @@ int vla_ppo_lora_grads(vla_model* m, int32_t B, const void* vis, const int32_t* 
   m->state_valid = false;
   // teacher-forced forward, every layer's input saved
   int R = 0, M = 0;
-  int rc = forward(m, B, vis, ids, lens_host, actions, s, &R, t.xs.data(), &M);
+  int rc = forward(m, B, vis, ids, lens_host, actions, s, &R, &t.sv, &M);
   if (rc) return rc;
   rc = head_logits(m, m->u_head, R, m->logits_tf, s);
   if (rc) return rc;

@@ -29,6 +29,8 @@ EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_action
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
 PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
+# training modes of vla_ppo_lora_grads (VLA_TRAIN_*): recompute each layer's forward, or keep it
+TRAIN_RECOMPUTE, TRAIN_KEEP = 0, 1
 DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
                  "vla_debug_set_layer_limit")
 
@@ -81,7 +83,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.vla_extract_actions.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, vp]
-    lib.vla_train_workspace_size.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(ctypes.c_size_t)]
+    lib.vla_train_workspace_size.argtypes = [ctypes.POINTER(_Config), i32, ctypes.POINTER(ctypes.c_size_t)]
     lib.vla_ppo_lora_grads.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, ctypes.POINTER(_Lora), vp,
                                        ctypes.c_size_t, vp, vp, vp]
     lib.vla_gae.argtypes = [i32, i32, vp, vp, vp, f32, f32, vp, vp, vp]
@@ -231,18 +233,22 @@ class VlaModel:
 
     def ppo_lora_grads(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
                        actions: torch.Tensor, logp_old: torch.Tensor, advantages: torch.Tensor, eps: float,
-                       temperature: float, adapters, scale: float):
+                       temperature: float, adapters, scale: float, mode: int = TRAIN_KEEP):
         """Gradients of the PPO-clip loss w.r.t. the LoRA factors (vla_ppo_lora_grads).
         adapters: per layer {projection key: (A [r, in], B [out, r])} bf16 device tensors
-        (layers or keys absent: not adapted).  Returns (stats [loss, clipped fraction],
-        logp_new [batch, n_actions], grads: per layer {key: (dA, dB)})."""
+        (layers or keys absent: not adapted).  mode: TRAIN_KEEP (the forward keeps every
+        layer's activations) or TRAIN_RECOMPUTE (the workspace for it, the backward
+        recomputes them).  Returns (stats [loss, clipped fraction], logp_new [batch,
+        n_actions], grads: per layer {key: (dA, dB)})."""
         lens = np.ascontiguousarray(prompt_lens, dtype=np.int32)
         B = int(lens.shape[0])
         L = self.cfg.n_layers
-        if getattr(self, "_train_ws", None) is None:
+        if getattr(self, "_train_ws_mode", None) != mode:
+            self._train_ws = None
             n = ctypes.c_size_t()
-            _check(self.lib.vla_train_workspace_size(ctypes.byref(self.c_cfg), ctypes.byref(n)))
+            _check(self.lib.vla_train_workspace_size(ctypes.byref(self.c_cfg), int(mode), ctypes.byref(n)))
             self._train_ws = torch.empty(n.value, dtype=torch.uint8, device=self.device)
+            self._train_ws_mode = mode
         ranks = {int(a.shape[0]) for ad in adapters for a, _ in ad.values()}
         assert len(ranks) == 1, "one rank for every adapter"
         rank = ranks.pop()

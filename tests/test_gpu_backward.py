@@ -9,7 +9,7 @@ import torch
 
 from gpu_util import Setup, log
 from oracle import learn_oracle as lo
-from paper_2505_18719_amd import inputs
+from paper_2505_18719_amd import inputs, vla
 
 pytestmark = pytest.mark.gpu
 
@@ -132,3 +132,38 @@ def test_7b_width_two_layers_lora_gradients_match_oracle():
     cfg = inputs.L7B_B8.replace(n_layers=2, batch=2)
     stats, lp, grads, ref = _case(cfg, seed=45, std=0.01)
     _check("7b-width 2L bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=45)[2], cfg.n_layers)
+
+
+@pytest.mark.parametrize("cfg", [inputs.TINY.replace(name="tiny_modes", batch=3, prompt_min=0, prompt_max=16),
+                                 inputs.L7B_B8.replace(n_layers=2, batch=2)], ids=["tiny", "7b-width-2L"])
+def test_keep_and_recompute_modes_give_the_same_bits(cfg):
+    """The training forward that keeps every layer's activations and the one
+    that keeps only the layer inputs (the backward recomputing the rest) run
+    the same arithmetic: loss, log-probs and every gradient agree bit for bit."""
+    S = Setup(cfg, seed=5)
+    ad = inputs.make_lora(cfg, 8, seed=5, device="cuda", std=0.05)
+    for li, layer in enumerate(ad):
+        for k, (a, b) in layer.items():
+            S.model.lora_merge(li, k, S.w["layers"][li][k], a, b, 0.5)
+    inp, dev = S.inputs(seed=5)
+    B, T = inp.batch, 1.5
+    acts = torch.from_numpy(inputs.stored_actions(cfg, B, seed=5)).cuda()
+    old = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, T)["logp"].contiguous()
+    old = (old + 0.05).contiguous()
+    adv = torch.from_numpy(inputs.ppo_minibatch(B, seed=5)[2]).cuda()
+    out = {}
+    for mode in (vla.TRAIN_KEEP, vla.TRAIN_RECOMPUTE):
+        log(f"[modes {cfg.name}] training mode {mode}")
+        st, lp, gr = S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, old, adv, 0.2, T, ad, 0.5,
+                                           mode=mode)
+        torch.cuda.synchronize()
+        out[mode] = (st.cpu(), lp.cpu(), [{k: (ga.cpu(), gb.cpu()) for k, (ga, gb) in layer.items()} for layer in gr])
+    S.model.close()
+    (s0, l0, g0), (s1, l1, g1) = out[vla.TRAIN_KEEP], out[vla.TRAIN_RECOMPUTE]
+    assert torch.equal(s0, s1) and torch.equal(l0, l1)
+    n = 0
+    for a, b in zip(g0, g1):
+        for k in a:
+            assert torch.equal(a[k][0], b[k][0]) and torch.equal(a[k][1], b[k][1]), k
+            n += 2
+    assert n == 14 * cfg.n_layers

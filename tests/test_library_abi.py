@@ -125,5 +125,8 @@ def test_lora_gradient_entry_validates_on_the_host(vla):
     assert b"model is NULL" in lib.vla_last_error()
     n = ctypes.c_size_t()
     c = vla.make_config(inputs.TINY)
-    assert lib.vla_train_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0
-    assert lib.vla_train_workspace_size(None, ctypes.byref(n)) == -1
+    assert lib.vla_train_workspace_size(ctypes.byref(c), 0, ctypes.byref(n)) == 0 and n.value > 0
+    n_keep = ctypes.c_size_t()
+    assert lib.vla_train_workspace_size(ctypes.byref(c), 1, ctypes.byref(n_keep)) == 0 and n_keep.value > n.value
+    assert lib.vla_train_workspace_size(ctypes.byref(c), 2, ctypes.byref(n)) == -1
+    assert lib.vla_train_workspace_size(None, 0, ctypes.byref(n)) == -1
