@@ -557,11 +557,11 @@ __device__ __forceinline__ int grad_row(const LoraGradArgs& a, int o) {
   return (j >= 0 && (a.mode != kPackGateUp || part == a.part)) ? j : -1;
 }
 
-// B^T of one projection as a skinny-GEMM operand: dst (bf16 frag [64 rows, K]) row c,
+// B^T of one projection as a skinny-GEMM operand: dst (bf16 frag [rows, K]) row c,
 // column o0 + o = B[grad_row(o), c] for o < n_cols and c < r, zero elsewhere.
-__global__ void pack_bt_kernel(LoraGradArgs a, int K, bf16_t* __restrict__ dst) {
+__global__ void pack_bt_kernel(LoraGradArgs a, int K, int rows, bf16_t* __restrict__ dst) {
   const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= 64 * (K / 8)) return;
+  if (i >= rows * (K / 8)) return;
   const int c = i / (K / 8), k0 = (i % (K / 8)) * 8;
   float v[8];
 #pragma unroll
@@ -604,9 +604,9 @@ __global__ void move_rows_kernel(const float* __restrict__ src, const int32_t* _
 
 }  // namespace
 
-hipError_t launch_pack_bt(const LoraGradArgs& a, int K, bf16_t* dst, hipStream_t s) {
-  if (K % 32 != 0 || a.r < 1 || a.r > 64) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(pack_bt_kernel, dim3((64 * (K / 8) + 255) / 256), dim3(256), 0, s, a, K, dst);
+hipError_t launch_pack_bt(const LoraGradArgs& a, int K, int rows, bf16_t* dst, hipStream_t s) {
+  if (K % 32 != 0 || a.r < 1 || a.r > 64 || rows % 16 != 0 || rows < a.r || rows > 128) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_bt_kernel, dim3((rows * (K / 8) + 255) / 256), dim3(256), 0, s, a, K, rows, dst);
   return hipGetLastError();
 }
 

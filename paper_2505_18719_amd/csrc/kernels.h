@@ -332,9 +332,9 @@ struct LoraGradArgs {
   float* da;         // [r, in] fp32 out
   float* db;         // [out, r] fp32 out
 };
-// B^T as a bf16 frag [64, K] operand: row c, column o0 + o = B[natural row of packed
-// output o, c] for o < n_cols, c < r; zero elsewhere (K % 32 == 0)
-hipError_t launch_pack_bt(const LoraGradArgs& a, int K, bf16_t* dst, hipStream_t s);
+// B^T as a bf16 frag [rows, K] operand: row c, column o0 + o = B[natural row of packed
+// output o, c] for o < n_cols, c < r; zero elsewhere (K % 32 == 0, rows % 16 == 0, r <= rows <= 128)
+hipError_t launch_pack_bt(const LoraGradArgs& a, int K, int rows, bf16_t* dst, hipStream_t s);
 // dB[natural row of o, c] = s C[c, o] for o < n_cols (to_b), or dA[c, i] = s C[c, i] for i < in;
 // C fp32 [64, ldc] row-major
 hipError_t launch_lora_finalize(const LoraGradArgs& a, const float* C, int ldc, bool to_b, hipStream_t s);

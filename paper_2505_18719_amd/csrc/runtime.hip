@@ -478,10 +478,11 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t, bool keep) {
   t.logp = L.take<float>(Rh);
   t.dlogp = L.take<float>(Rh);
   const size_t ncol = std::max(std::max(Mx64, (size_t)Fg), std::max(d, (size_t)F64));
-  t.t1 = L.take<float>(64 * Mx64);
-  t.t2 = L.take<float>(64 * Mx64);
-  t.cres = L.take<float>(64 * ncol);
-  t.spart = L.take<float>((size_t)kMaxSplits * 64 * ncol);
+  // the low-rank products of up to 128 stacked factor rows (the skinny GEMM's A operand)
+  t.t1 = L.take<float>(128 * Mx64);
+  t.t2 = L.take<float>(128 * Mx64);
+  t.cres = L.take<float>(128 * ncol);
+  t.spart = L.take<float>((size_t)kMaxSplits * 128 * ncol);
   t.dxf = L.take<bf16_t>(frag_elems(Mx64, d));
   t.dxmf = L.take<bf16_t>(frag_elems(Mx64, d));
   t.hb = L.take<bf16_t>(frag_elems(Mx64, D.Fp));
@@ -494,10 +495,10 @@ void plan_train(Layout& L, const Dims& D, TrainBufs& t, bool keep) {
   t.dyt = L.take<bf16_t>(frag_elems(std::max(3 * D.d, 2 * D.Fp), Mk));
   t.dzf = L.take<bf16_t>(frag_elems(Rh, A32));
   t.wact_t = L.take<bf16_t>(frag_elems(D.d, A32));
-  t.apk = L.take<bf16_t>(frag_elems(64, std::max(D.d, D.Fp)));
-  t.bpt = L.take<bf16_t>(frag_elems(64, std::max(3 * D.d, 2 * D.Fp)));
-  t.t1f = L.take<bf16_t>(frag_elems(64, Mk));
-  t.t2f = L.take<bf16_t>(frag_elems(64, Mk));
+  t.apk = L.take<bf16_t>(frag_elems(128, std::max(D.d, D.Fp)));
+  t.bpt = L.take<bf16_t>(frag_elems(128, std::max(3 * D.d, 2 * D.Fp)));
+  t.t1f = L.take<bf16_t>(frag_elems(128, Mk));
+  t.t2f = L.take<bf16_t>(frag_elems(128, Mk));
   L.off = align_up(L.off, 256);
 }
 
@@ -558,63 +559,91 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   VLA_CK(launch_attn_bwd(ab, s));
   VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
   VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
-  // LoRA gradients by the low-rank route on the skinny GEMM (r <= 64 output rows; the
+  // LoRA gradients by the low-rank route on the skinny GEMM (<= 128 output rows; the
   // contractions over the M rows run with K = Mk, rows past M zero):
-  //   T1^T = A X^T, T2^T = B^T dY^T (r x M);  dB^T = T1^T dY,  dA = T2^T X
+  //   T1^T = A X^T, T2^T = B^T dY^T (r x M);  dB^T = T1^T dY,  dA = T2^T X.
+  // Projections that share X and dY (q, k, v; gate, up) stack their A and B^T
+  // factors, 16-row aligned, into one operand, so X, dY and X^T stream once per
+  // group for T1, T2 and dA.
   auto adapted = [&](int p) { return lora->a[l * 7 + p] != nullptr; };
-  auto skinny_to = [&](const bf16_t* a_op, const bf16_t* w_op, int N, int K, float* out) {
+  auto skinny_to = [&](const bf16_t* a_op, int rows, const bf16_t* w_op, int N, int K, float* out) {
     const SkinnyPlan sp = skinny_plan(N, K, m->cus, kMaxSplits);
-    SkinnyArgs sa{a_op, 64, w_op, N, K, t.spart};
+    SkinnyArgs sa{a_op, rows, w_op, N, K, t.spart};
     hipError_t e = launch_skinny(sa, sp, s);
-    return e != hipSuccess ? e : launch_reduce_sum(t.spart, sp, out, 64, N, s);
+    return e != hipSuccess ? e : launch_reduce_sum(t.spart, sp, out, rows, N, s);
   };
-  // X frag [M, kx] (in real input features) with X^T rows in64; dY frag [M, ky] whose
-  // columns o0 .. o0 + n_cols are this projection's outputs in the packed order of
-  // `mode`, dYT its transpose (rows o0 .. o0 + n_cols)
-  auto lowrank = [&](int p, const bf16_t* X, int kx, int in, const bf16_t* XT, const bf16_t* dY, int ky,
-                     const bf16_t* dYT, int o0, int n_cols, int out, int mode, int part) -> hipError_t {
-    LoraGradArgs la{o0, n_cols, in, out, mode, D.hd, part,
-                    static_cast<const bf16_t*>(lora->a[l * 7 + p]), static_cast<const bf16_t*>(lora->b[l * 7 + p]),
-                    lora->rank, lora->scale, lora->grad_a[l * 7 + p], lora->grad_b[l * 7 + p]};
-    PackArgs pa{t.apk, 64, kx, la.a, nullptr, in, lora->rank, in, kPackRows, D.hd};
+  const int r16 = round_up(lora->rank, 16), per = 128 / r16;
+  // one projection of a group: its packed output columns o0 .. o0 + n_cols of dY (the order
+  // of `mode`), and dYT, the transposed dY rows of those columns
+  struct Proj {
+    int p, o0, n_cols, out, mode, part;
+    const bf16_t* dYT;
+  };
+  // X frag [M, kx] (in real input features) with X^T rows in64 (XT); dY frag [M, ky]
+  auto group = [&](const Proj* ps, int n, const bf16_t* X, int kx, int in, const bf16_t* XT, const bf16_t* dY,
+                   int ky) -> hipError_t {
     hipError_t e;
-    if ((e = launch_pack_frag(pa, s)) != hipSuccess) return e;
-    if ((e = skinny_to(t.apk, X, Mp, kx, t.t1)) != hipSuccess) return e;
-    if ((e = launch_to_frag(t.t1, Mp, 64, M, Mk, t.t1f, s)) != hipSuccess) return e;
-    if ((e = launch_pack_bt(la, ky, t.bpt, s)) != hipSuccess) return e;
-    if ((e = skinny_to(t.bpt, dY, Mp, ky, t.t2)) != hipSuccess) return e;
-    if ((e = launch_to_frag(t.t2, Mp, 64, M, Mk, t.t2f, s)) != hipSuccess) return e;
-    la.o0 = 0;  // dYT holds only this projection's rows
-    if ((e = skinny_to(t.t1f, dYT, n_cols, Mk, t.cres)) != hipSuccess) return e;
-    if ((e = launch_lora_finalize(la, t.cres, n_cols, true, s)) != hipSuccess) return e;
     const int in64 = round_up(in, 64);
-    if ((e = skinny_to(t.t2f, XT, in64, Mk, t.cres)) != hipSuccess) return e;
-    return launch_lora_finalize(la, t.cres, in64, false, s);
+    for (int b0 = 0; b0 < n; b0 += per) {
+      const int nb = std::min(per, n - b0), rows = nb * r16;
+      LoraGradArgs la[3];
+      for (int i = 0; i < nb; ++i) {
+        const Proj& q = ps[b0 + i];
+        la[i] = LoraGradArgs{q.o0, q.n_cols, in, q.out, q.mode, D.hd, q.part,
+                             static_cast<const bf16_t*>(lora->a[l * 7 + q.p]),
+                             static_cast<const bf16_t*>(lora->b[l * 7 + q.p]), lora->rank, lora->scale,
+                             lora->grad_a[l * 7 + q.p], lora->grad_b[l * 7 + q.p]};
+        PackArgs pa{t.apk + frag_index(i * r16, 0, kx), r16, kx, la[i].a, nullptr, in, lora->rank, in, kPackRows, D.hd};
+        if ((e = launch_pack_frag(pa, s)) != hipSuccess) return e;
+        if ((e = launch_pack_bt(la[i], ky, r16, t.bpt + frag_index(i * r16, 0, ky), s)) != hipSuccess) return e;
+      }
+      if ((e = skinny_to(t.apk, rows, X, Mp, kx, t.t1)) != hipSuccess) return e;
+      if ((e = launch_to_frag(t.t1, Mp, rows, M, Mk, t.t1f, s)) != hipSuccess) return e;
+      if ((e = skinny_to(t.bpt, rows, dY, Mp, ky, t.t2)) != hipSuccess) return e;
+      if ((e = launch_to_frag(t.t2, Mp, rows, M, Mk, t.t2f, s)) != hipSuccess) return e;
+      for (int i = 0; i < nb; ++i) {
+        const Proj& q = ps[b0 + i];
+        LoraGradArgs lb = la[i];
+        lb.o0 = 0;  // q.dYT holds only this projection's rows
+        if ((e = skinny_to(t.t1f + frag_index(i * r16, 0, Mk), r16, q.dYT, q.n_cols, Mk, t.cres)) != hipSuccess)
+          return e;
+        if ((e = launch_lora_finalize(lb, t.cres, q.n_cols, true, s)) != hipSuccess) return e;
+      }
+      if ((e = skinny_to(t.t2f, rows, XT, in64, Mk, t.cres)) != hipSuccess) return e;
+      for (int i = 0; i < nb; ++i)
+        if ((e = launch_lora_finalize(la[i], t.cres + (size_t)i * r16 * in64, in64, false, s)) != hipSuccess) return e;
+    }
+    return hipSuccess;
   };
-  if (adapted(VLA_PROJ_Q) || adapted(VLA_PROJ_K) || adapted(VLA_PROJ_V)) {
+  Proj ps[3];
+  int n = 0;
+  for (int p = VLA_PROJ_Q; p <= VLA_PROJ_V; ++p)
+    if (adapted(p))
+      ps[n++] = Proj{p, p * d, d, d, p == VLA_PROJ_V ? kPackRows : kPackQk, 0, t.dyt + frag_index(p * d, 0, Mk)};
+  if (n) {
     VLA_CK(launch_transpose_frag(u1, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dqkv, false, 3 * d, M, 3 * d, Mk, t.dyt, s));
-    for (int p = VLA_PROJ_Q; p <= VLA_PROJ_V; ++p)
-      if (adapted(p))
-        VLA_CK(lowrank(p, u1, d, d, t.xt, t.dqkv, 3 * d, t.dyt + frag_index(p * d, 0, Mk), p * d, d, d,
-                       p == VLA_PROJ_V ? kPackRows : kPackQk, 0));
+    VLA_CK(group(ps, n, u1, d, d, t.xt, t.dqkv, 3 * d));
   }
   if (adapted(VLA_PROJ_O)) {
     VLA_CK(launch_transpose_frag(ob, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dxmf, false, d, M, d, Mk, t.dyt, s));
-    VLA_CK(lowrank(VLA_PROJ_O, ob, d, d, t.xt, t.dxmf, d, t.dyt, 0, d, d, kPackRows, 0));
+    ps[0] = Proj{VLA_PROJ_O, 0, d, d, kPackRows, 0, t.dyt};
+    VLA_CK(group(ps, 1, ob, d, d, t.xt, t.dxmf, d));
   }
-  if (adapted(VLA_PROJ_GATE) || adapted(VLA_PROJ_UP)) {
+  n = 0;
+  for (int p = VLA_PROJ_GATE; p <= VLA_PROJ_UP; ++p)
+    if (adapted(p)) ps[n++] = Proj{p, 0, Fg, D.F, kPackGateUp, p - VLA_PROJ_GATE, t.dyt};
+  if (n) {
     VLA_CK(launch_transpose_frag(u2, false, d, M, d, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dgu, false, 2 * Fp, M, Fg, Mk, t.dyt, s));
-    for (int p = VLA_PROJ_GATE; p <= VLA_PROJ_UP; ++p)
-      if (adapted(p))
-        VLA_CK(lowrank(p, u2, d, d, t.xt, t.dgu, 2 * Fp, t.dyt, 0, Fg, D.F, kPackGateUp, p - VLA_PROJ_GATE));
+    VLA_CK(group(ps, n, u2, d, d, t.xt, t.dgu, 2 * Fp));
   }
   if (adapted(VLA_PROJ_DOWN)) {
     VLA_CK(launch_transpose_frag(t.hb, false, Fp, M, D.F, Mk, t.xt, s));
     VLA_CK(launch_transpose_frag(t.dxf, false, d, M, d, Mk, t.dyt, s));
-    VLA_CK(lowrank(VLA_PROJ_DOWN, t.hb, Fp, D.F, t.xt, t.dxf, d, t.dyt, 0, d, d, kPackRows, 0));
+    ps[0] = Proj{VLA_PROJ_DOWN, 0, d, d, kPackRows, 0, t.dyt};
+    VLA_CK(group(ps, 1, t.hb, Fp, D.F, t.xt, t.dxf, d));
   }
   // dL/d(layer input) = dxm + RMSNorm backward of du1
   VLA_CK(launch_rmsnorm_bwd(xs, w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
