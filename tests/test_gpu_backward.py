@@ -134,6 +134,16 @@ def test_7b_width_two_layers_lora_gradients_match_oracle():
     _check("7b-width 2L bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=45)[2], cfg.n_layers)
 
 
+def test_7b_width_longest_sequences():
+    """Two environments of exactly 320 rows (256 visual + 57 prompt + 7 actions),
+    the longest sequence the attention kernels hold: all ten 32-row chunks of the
+    attention backward's LDS tiles in use, at head_dim 128, one layer."""
+    cfg = inputs.L7B_B8.replace(name="openvla7b_full_len", n_layers=1, batch=2, prompt_min=57, prompt_max=57)
+    assert cfg.max_seq == 320
+    stats, lp, grads, ref = _case(cfg, seed=46, std=0.01)
+    _check("7b-width 320-row bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=46)[2], cfg.n_layers)
+
+
 @pytest.mark.parametrize("cfg", [inputs.TINY.replace(name="tiny_modes", batch=3, prompt_min=0, prompt_max=16),
                                  inputs.L7B_B8.replace(n_layers=2, batch=2)], ids=["tiny", "7b-width-2L"])
 def test_keep_and_recompute_modes_give_the_same_bits(cfg):
