@@ -511,7 +511,8 @@ hipError_t gemm_f32(const bf16_t* A, int ka, const bf16_t* W, int kw, int M, int
 }
 
 // Backward of decoder layer l: t.dx holds dL/d(layer output) [M, d] and receives
-// dL/d(layer input); LoRA gradients of the adapted projections are written.
+// dL/d(layer input) (not for layer 0, whose input is the embeddings); LoRA gradients
+// of the adapted projections are written.
 int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lora* lora, hipStream_t s) {
   const Dims& D = m->D;
   const LayerW& w = m->lw[l];
@@ -557,8 +558,11 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
   AttnBwdArgs ab{qb, ob, t.dob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len, B, d, D.H, D.hd,
                  m->scale, m->rope, stats, t.dqkv, t.do16};
   VLA_CK(launch_attn_bwd(ab, s));
-  VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
-  VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
+  // the gradient of the first layer's input (the embeddings) feeds no trained parameter
+  if (l > 0) {
+    VLA_CK(launch_transpose_frag(w.wqkv, false, d, 3 * d, d, 3 * d, t.wt, s));
+    VLA_CK(gemm_f32(t.dqkv, 0, t.wt, 0, M, d, 3 * d, t.du, d, s));
+  }
   // LoRA gradients by the low-rank route on the skinny GEMM (<= 128 output rows; the
   // contractions over the M rows run with K = Mk, rows past M zero):
   //   T1^T = A X^T, T2^T = B^T dY^T (r x M);  dB^T = T1^T dY,  dA = T2^T X.
@@ -646,7 +650,7 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
     VLA_CK(group(ps, 1, t.hb, Fp, D.F, t.xt, t.dxf, d));
   }
   // dL/d(layer input) = dxm + RMSNorm backward of du1
-  VLA_CK(launch_rmsnorm_bwd(xs, w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
+  if (l > 0) VLA_CK(launch_rmsnorm_bwd(xs, w.attn_norm, eps, t.du, t.dxm, t.dx, nullptr, M, d, s));
   return VLA_OK;
 }
 
