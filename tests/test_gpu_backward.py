@@ -134,6 +134,17 @@ def test_7b_width_two_layers_lora_gradients_match_oracle():
     _check("7b-width 2L bwd", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=45)[2], cfg.n_layers)
 
 
+@pytest.mark.parametrize("rank", [48, 64])
+def test_large_ranks_split_the_stacked_groups(rank):
+    """Ranks 48 and 64 (16-row-aligned slots of 48 and 64 rows): at most two factors
+    fit the 128-row operand of the low-rank products, so q, k, v run as two
+    batches (q, k, then v) and gate, up fill all 128 rows."""
+    cfg = inputs.TINY.replace(name=f"tiny_bwd_r{rank}", batch=3, prompt_min=2, prompt_max=14)
+    stats, lp, grads, ref = _case(cfg, seed=47 + rank, rank=rank, std=0.03)
+    _check(f"tiny bwd rank {rank}", stats, lp, grads, ref, inputs.ppo_minibatch(cfg.batch, seed=47 + rank)[2],
+           cfg.n_layers)
+
+
 def test_7b_width_longest_sequences():
     """Two environments of exactly 320 rows (256 visual + 57 prompt + 7 actions),
     the longest sequence the attention kernels hold: all ten 32-row chunks of the
