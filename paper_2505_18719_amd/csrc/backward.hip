@@ -149,8 +149,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restric
 // SwiGLU backward for h = silu(g) up, with g, up the fp32 gate/up pre-activations
 // in the packed interleaved order (columns 64 (j / 32) + j % 32 and +32 of cgu) and
 // dh fp32 [M, F] (row stride ldh): writes d[g; up] as bf16 frag in that same order
-// (K = 2 Fp) and the forward h = bf16(silu(g) up) as bf16 frag (K = Fp); with dh
-// null only h is written (the forward of a pass that keeps the pre-activations).  A wave
+// (K = 2 Fp) and the forward h = bf16(silu(g) up) as bf16 frag (K = Fp).  A wave
 // takes one 16-row x 32-feature block, lane (r, u) rows 16 mb + r and features
 // 32 jb + 8 u .. + 8, so each of its three stores is one contiguous 1 KB frag
 // block; rows >= M of the last block are written as zeros.
@@ -168,19 +167,15 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const float* __restrict
   if (m < M && j0 + 8 <= F) {
     load8(cr, gv);
     load8(cr + 32, uv);
-    if (dh) load8(dh + (size_t)m * ldh + j0, dv);
+    load8(dh + (size_t)m * ldh + j0, dv);
   } else {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const bool in = m < M && j0 + e < F;
       gv[e] = in ? cr[e] : 0.f;
       uv[e] = in ? cr[32 + e] : 0.f;
-      if (dh) dv[e] = in ? dh[(size_t)m * ldh + j0 + e] : 0.f;
+      dv[e] = in ? dh[(size_t)m * ldh + j0 + e] : 0.f;
     }
-  }
-  if (!dh) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dv[e] = 0.f;
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -192,12 +187,10 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const float* __restrict
     hv[e] = gg / (1.f + expf(-gg)) * up;  // the forward epilogue's expression
   }
   uint4 o;
-  if (dh) {
-    o.x = pack2bf(dgv[0], dgv[1]); o.y = pack2bf(dgv[2], dgv[3]); o.z = pack2bf(dgv[4], dgv[5]); o.w = pack2bf(dgv[6], dgv[7]);
-    *reinterpret_cast<uint4*>(dgu + frag_index(m, cg, 2 * Fp)) = o;
-    o.x = pack2bf(duv[0], duv[1]); o.y = pack2bf(duv[2], duv[3]); o.z = pack2bf(duv[4], duv[5]); o.w = pack2bf(duv[6], duv[7]);
-    *reinterpret_cast<uint4*>(dgu + frag_index(m, cg + 32, 2 * Fp)) = o;
-  }
+  o.x = pack2bf(dgv[0], dgv[1]); o.y = pack2bf(dgv[2], dgv[3]); o.z = pack2bf(dgv[4], dgv[5]); o.w = pack2bf(dgv[6], dgv[7]);
+  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg, 2 * Fp)) = o;
+  o.x = pack2bf(duv[0], duv[1]); o.y = pack2bf(duv[2], duv[3]); o.z = pack2bf(duv[4], duv[5]); o.w = pack2bf(duv[6], duv[7]);
+  *reinterpret_cast<uint4*>(dgu + frag_index(m, cg + 32, 2 * Fp)) = o;
   o.x = pack2bf(hv[0], hv[1]); o.y = pack2bf(hv[2], hv[3]); o.z = pack2bf(hv[4], hv[5]); o.w = pack2bf(hv[6], hv[7]);
   *reinterpret_cast<uint4*>(h + frag_index(m, j0, Fp)) = o;
 }
@@ -671,7 +664,7 @@ hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const f
 hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
                              bf16_t* h, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (Fp % 32 != 0 || F > Fp || !cgu || !h || (dh && !dgu)) return hipErrorInvalidValue;
+  if (Fp % 32 != 0 || F > Fp || !cgu || !h || !dh || !dgu) return hipErrorInvalidValue;
   const size_t waves = (size_t)((M + 15) / 16) * (Fp / 32);
   hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, cgu, ldc, dh, ldh, M, F,
                      Fp, dgu, h);

@@ -69,13 +69,18 @@ template <int EPI>
 __device__ __forceinline__ void pair_epilogue(const GemmArgs& a, int row, int c0, int q, const float4& v1,
                                               const float4& v2) {
   const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
-  if constexpr (EPI == kEpiSwiGlu) {
+  if constexpr (EPI == kEpiSwiGlu || EPI == kEpiSwiGluKeep) {
     // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
     float o[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
     *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
         make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
+    if constexpr (EPI == kEpiSwiGluKeep) {
+      float* cr = a.C + (size_t)row * a.ldc + c0 + 4 * q;
+      *reinterpret_cast<float4*>(cr) = v1;
+      *reinterpret_cast<float4*>(cr + 32) = v2;
+    }
   } else {  // kEpiQkvRope
     const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
     const int region = c0 / d;
@@ -265,6 +270,10 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
     case kEpiResidual: hipLaunchKernelGGL(gemm_bf16_kernel<kEpiResidual>, grid, block, 0, s, a, tm, tn); break;
     case kEpiSwiGlu: hipLaunchKernelGGL(gemm_bf16_kernel<kEpiSwiGlu>, grid, block, 0, s, a, tm, tn); break;
     case kEpiQkvRope: hipLaunchKernelGGL(gemm_bf16_kernel<kEpiQkvRope>, grid, block, 0, s, a, tm, tn); break;
+    case kEpiSwiGluKeep:
+      if (!a.C || a.ldc % 4 != 0 || a.ldc < a.N) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(gemm_bf16_kernel<kEpiSwiGluKeep>, grid, block, 0, s, a, tm, tn);
+      break;
   }
   return hipGetLastError();
 }

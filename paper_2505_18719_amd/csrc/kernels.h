@@ -36,6 +36,7 @@ enum GemmEpilogue {
   kEpiSwiGlu = 2,    // H[m, j] = bf16(silu(gate) * up)  for W = interleaved [gate; up] blocks of 32 rows;
                      //   H in frag layout with K = ldh
   kEpiQkvRope = 3,   // rotate q, k by RoPE, store q bf16 [M, d] and K/V into the page pool
+  kEpiSwiGluKeep = 4,  // kEpiSwiGlu, and the fp32 pre-activations C[m, n] = acc kept (ldc) for a backward
 };
 
 struct GemmArgs {
@@ -297,7 +298,7 @@ hipError_t launch_transpose_frag(const void* src, bool src_f32, int ld, int R, i
 hipError_t launch_rmsnorm_bwd(const float* x, const float* g, float eps, const float* dy, const float* dres,
                               float* dx, bf16_t* dx_frag, int M, int d, hipStream_t s);
 // SwiGLU backward from the fp32 interleaved gate/up pre-activations and dh: d[g; up] (bf16 frag,
-// K = 2 Fp, the packed interleaved order) and the forward h (bf16 frag, K = Fp); dh null: h only
+// K = 2 Fp, the packed interleaved order) and the forward h (bf16 frag, K = Fp)
 hipError_t launch_swiglu_bwd(const float* cgu, int ldc, const float* dh, int ldh, int M, int F, int Fp, bf16_t* dgu,
                              bf16_t* h, hipStream_t s);
 struct AttnBwdArgs {

@@ -400,10 +400,9 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     // [gate; up] interleaved in 64-row blocks: only the blocks holding real rows are computed; the
     // down projection's contraction stops at the last real feature (h and Wdown stay Fp wide)
     gg.A = u; gg.W = w.wgu; gg.M = Ml; gg.N = 64 * ((D.F + 31) / 32); gg.K = D.d; gg.H = hbuf; gg.ldh = D.Fp;
-    if (full) {  // kept fp32 pre-activations, then h from them (the epilogue's expression: same bits)
+    if (full) {  // h, and the fp32 pre-activations kept for the backward
       gg.C = sv->cgu[l]; gg.ldc = 2 * D.Fp;
-      PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiStoreF32, s));
-      VLA_CK(launch_swiglu_bwd(sv->cgu[l], 2 * D.Fp, nullptr, 0, Ml, D.F, D.Fp, nullptr, hbuf, s));
+      PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGluKeep, s));
     } else {
       PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, 2.0 * D.F, D.d), launch_gemm(gg, kEpiSwiGlu, s));
     }
