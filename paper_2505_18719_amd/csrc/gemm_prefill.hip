@@ -232,7 +232,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
         if (row < M) {
           float4* p = reinterpret_cast<float4*>(a.C + (size_t)row * a.ldc + c0 + 4 * q);
           if constexpr (EPI == kEpiResidual) {
-            const float4 o = *p;
+            const float4 o = a.R ? *reinterpret_cast<const float4*>(a.R + (size_t)row * a.ldc + c0 + 4 * q) : *p;
             *p = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
           } else {
             *p = v;

@@ -32,7 +32,7 @@ struct RowMeta {
 // bf16, fp32 accumulation on MFMA, and one of these epilogues:
 enum GemmEpilogue {
   kEpiStoreF32 = 0,  // C[m, n] = acc                         (fp32, ldc)
-  kEpiResidual = 1,  // C[m, n] += acc                        (fp32 residual stream, ldc)
+  kEpiResidual = 1,  // C[m, n] = (R ? R : C)[m, n] + acc     (fp32 residual stream, ldc)
   kEpiSwiGlu = 2,    // H[m, j] = bf16(silu(gate) * up)  for W = interleaved [gate; up] blocks of 32 rows;
                      //   H in frag layout with K = ldh
   kEpiQkvRope = 3,   // rotate q, k by RoPE, store q bf16 [M, d] and K/V into the page pool
@@ -46,6 +46,7 @@ struct GemmArgs {
   int ka, kw;       // K of A's and W's frag allocations when wider than the contraction (0: K)
   float* C;
   int ldc;
+  const float* R;   // kEpiResidual: the residual read (row stride ldc), or null for C itself
   bf16_t* H;
   int ldh;
   // kEpiQkvRope

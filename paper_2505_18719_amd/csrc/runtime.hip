@@ -369,7 +369,10 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     const bool last = prune && l == D.L - 1;
-    if (sv) VLA_CK(hipMemcpyAsync(sv->xs[l], m->x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
+    // keep mode chains the residual stream through the kept buffers (x_l -> xm_l -> x_{l+1}, the
+    // residual epilogues reading one and writing the next); otherwise it is updated in place
+    if (sv && !(full && l > 0))
+      VLA_CK(hipMemcpyAsync(sv->xs[l], m->x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
     bf16_t* const qb = full ? sv->q[l] : m->q;
     GemmArgs g{};
     g.A = full ? sv->u1[l] : m->u; g.W = w.wqkv; g.M = Mi; g.N = 3 * D.d; g.K = D.d;
@@ -392,8 +395,11 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     }
     GemmArgs go{};
     go.A = u; go.W = w.wo; go.M = Ml; go.N = D.d; go.K = D.d; go.C = x; go.ldc = D.d;
+    if (full) {
+      go.R = sv->xs[l];
+      go.C = x = sv->xm[l];
+    }
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.d), launch_gemm(go, kEpiResidual, s));
-    if (full) VLA_CK(hipMemcpyAsync(sv->xm[l], x, (size_t)Mi * D.d * sizeof(float), hipMemcpyDeviceToDevice, s));
     if (full) u = sv->u2[l];
     VLA_CK(launch_rmsnorm(x, D.d, nullptr, w.mlp_norm, eps, u, D.d, Ml, D.d, s, true));
     GemmArgs gg{};
@@ -409,10 +415,14 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     GemmArgs gd{};
     gd.A = hbuf; gd.W = w.wd; gd.M = Ml; gd.N = D.d; gd.K = 32 * ((D.F + 31) / 32); gd.ka = D.Fp; gd.kw = D.Fp;
     gd.C = x; gd.ldc = D.d;
+    if (full) {
+      gd.R = sv->xm[l];
+      gd.C = x = l + 1 < D.L ? sv->xs[l + 1] : m->x;
+    }
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.F), launch_gemm(gd, kEpiResidual, s));
     if (l + 1 < D.L)
-      VLA_CK(launch_rmsnorm(m->x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, full ? sv->u1[l + 1] : m->u, D.d, Mi,
-                            D.d, s, true));
+      VLA_CK(launch_rmsnorm(x, D.d, nullptr, m->lw[l + 1].attn_norm, eps, full ? sv->u1[l + 1] : m->u, D.d, Mi, D.d,
+                            s, true));
   }
   if (prune)
     VLA_CK(launch_rmsnorm(m->xc, D.d, nullptr, m->final_norm, eps, m->u_head, D.d, R, D.d, s, true));
