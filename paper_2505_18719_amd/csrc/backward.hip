@@ -337,7 +337,7 @@ __device__ __forceinline__ void ab_dq_tile(const AttnBwdArgs& a, const char* vld
       s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       dp[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       // A operand row r16 of tile t: key 32 c + 8 (r16 / 4) + 4 t + r16 % 4 (clamped into the sequence)
-      const int key = min(32 * c + 8 * (r16 >> 2) + 4 * t + (r16 & 3), L - 1);
+      const int key = min(ab_row(32 * c + 16 * t + r16), L - 1);
       const int page = __shfl(ptv, key / kPage, kWave);
       const bf16_t* kp = a.kv.k + (((size_t)page * H + head) * kPage + key % kPage) * HD + 8 * g;
       const char* vr = vlds + (32 * c + 16 * t + r16) * KROW;
@@ -453,7 +453,7 @@ __device__ __forceinline__ void ab_dkv_tile(const AttnBwdArgs& a, const char* qt
       s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       dp[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       // A operand row r16 of tile t: query 32 c + 8 (r16 / 4) + 4 t + r16 % 4 (clamped)
-      const int qi = min(32 * c + 8 * (r16 >> 2) + 4 * t + (r16 & 3), L - 1);
+      const int qi = min(ab_row(32 * c + 16 * t + r16), L - 1);
       const size_t at = (size_t)(row0 + qi) * a.d + head * HD + 8 * g;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
