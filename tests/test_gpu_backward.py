@@ -188,3 +188,41 @@ def test_keep_and_recompute_modes_give_the_same_bits(cfg):
             assert torch.equal(a[k][0], b[k][0]) and torch.equal(a[k][1], b[k][1]), k
             n += 2
     assert n == 14 * cfg.n_layers
+
+
+def test_training_workspace_sizes_select_the_mode():
+    """A workspace of the keep size runs the keep mode, one of the recompute size
+    the recompute mode (same bits), and one byte less than that is refused with
+    VLA_EWORKSPACE before any device work."""
+    import ctypes
+    cfg = inputs.TINY.replace(name="tiny_ws", batch=2, prompt_min=4, prompt_max=8)
+    S = Setup(cfg, seed=9)
+    ad = inputs.make_lora(cfg, 8, seed=9, device="cuda")
+    for li, layer in enumerate(ad):
+        for k, (a, b) in layer.items():
+            S.model.lora_merge(li, k, S.w["layers"][li][k], a, b, 0.5)
+    inp, dev = S.inputs(seed=9)
+    acts = torch.from_numpy(inputs.stored_actions(cfg, inp.batch, seed=9)).cuda()
+    old = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, acts, 1.0)["logp"].contiguous()
+    adv = torch.from_numpy(inputs.ppo_minibatch(inp.batch, seed=9)[2]).cuda()
+    lib = vla.load_library()
+    sizes = {}
+    for mode in (vla.TRAIN_RECOMPUTE, vla.TRAIN_KEEP):
+        n = ctypes.c_size_t()
+        assert lib.vla_train_workspace_size(ctypes.byref(S.model.c_cfg), mode, ctypes.byref(n)) == 0
+        sizes[mode] = n.value
+    assert sizes[vla.TRAIN_KEEP] > sizes[vla.TRAIN_RECOMPUTE]
+    st, _, _ = S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, old, adv, 0.2, 1.0, ad, 0.5,
+                                      mode=vla.TRAIN_RECOMPUTE)
+    torch.cuda.synchronize()
+    assert np.isfinite(st.cpu().numpy()).all()
+    # one byte short of the recompute size: refused on the host
+    S.model._train_ws_mode = None
+    S.model._train_ws = None
+    small = torch.empty(sizes[vla.TRAIN_RECOMPUTE] - 1, dtype=torch.uint8, device="cuda")
+    S.model._train_ws, S.model._train_ws_mode = small, "short"
+    with pytest.raises(vla.VlaError) as err:
+        S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, old, adv, 0.2, 1.0, ad, 0.5,
+                               mode="short")
+    assert err.value.code == -3
+    S.model.close()
