@@ -49,7 +49,8 @@ int vla_debug_sample(const float* z, int32_t B, int32_t A, int32_t n_actions, in
  * [hd/2 + 32b, hd/2 + 32b + 32)), 6 Wo [d, d], 7 [Wgate; Wup] [2 Fp, d]
  * interleaved in blocks of 32 rows (gate rows 32 (r / 64) + r % 32 at r % 64 < 32,
  * the matching up rows after them; rows past d_ffn zero), 8 Wdown [d, Fp]
- * (columns past d_ffn zero); Fp = d_ffn rounded up to a multiple of 256. */
+ * (columns past d_ffn zero); Fp = d_ffn rounded up to a multiple of 256;
+ * 9 the SwiGLU output h, bf16 [rows, Fp] in frag layout. */
 struct vla_model;
 int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream);
 
@@ -60,6 +61,16 @@ int vla_debug_read(struct vla_model* m, int32_t which, int32_t layer, void* dst,
  * the last layer computes its attention output, O projection and MLP only
  * for the rows read afterwards (the same bits for those rows). */
 int vla_debug_set_layer_limit(struct vla_model* m, int32_t n_layers);
+
+/* With a layer limit set, end the last layer run at a stage, so that each
+ * rounding point of the layer (Sec. 3.5: the rollout runs in bf16) can be read
+ * on its own: 0 the layer's end (x: its output, buffer 9: its SwiGLU output h);
+ * 1 before the QKV projection (x: the layer input, buffer 4: the attention
+ * norm's output); 2 after attention (buffer 1: rotated q, buffers 2 / 3: the
+ * layer's K / V pages, buffer 4: the attention output); 3 after the MLP norm
+ * (x: the mid residual, buffer 4: the MLP norm's output).  Stages 1..3 leave
+ * the rest of the pass undone; the prefill logits are then not meaningful. */
+int vla_debug_set_stop(struct vla_model* m, int32_t stage);
 
 #ifdef __cplusplus
 }

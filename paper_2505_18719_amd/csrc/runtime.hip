@@ -147,6 +147,7 @@ struct vla_model {
   bool state_valid;
   std::vector<int> prefix_host;  // L_b of the last prefill
   int layer_limit;               // test hook: run only the first layer_limit layers (0 = all)
+  int debug_stop;                // test hook: with a layer limit, where the last layer run stops (0 = its end)
   float scale;
   // decode GEMM work splits (one persistent workgroup per CU)
   SkinnyPlan plan_qkv, plan_o, plan_gu, plan_d, plan_head;
@@ -369,6 +370,9 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
   for (int l = 0; l < n_layers; ++l) {
     const LayerW& w = m->lw[l];
     const bool last = prune && l == D.L - 1;
+    // debug stop points inside the last layer of a limited pass (every buffer read afterwards holds that stage)
+    const int stop = m->layer_limit > 0 && l == n_layers - 1 ? m->debug_stop : 0;
+    if (stop == 1) break;  // u: the attention norm's output, x: the layer input
     // keep mode chains the residual stream through the kept buffers (x_l -> xm_l -> x_{l+1}, the
     // residual epilogues reading one and writing the next); otherwise it is updated in place
     if (sv && !(full && l > 0))
@@ -382,6 +386,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     PrefillAttnArgs pa{qb, full ? sv->ob[l] : m->u, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
                        B, D.d, D.H, D.hd, m->scale, last ? m->env_q0 : nullptr, full ? sv->lse[l] : nullptr};
     PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, last ? attn_flops_last : attn_flops, launch_attn_prefill(pa, s));
+    if (stop == 2) break;  // u: the attention output; q and the layer's K/V pages written
     // the rest of the layer runs on all rows, or on the compacted needed rows of the last layer
     const int Ml = last ? R : Mi;
     float* x = m->x;
@@ -402,6 +407,7 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(Ml, D.d, D.d), launch_gemm(go, kEpiResidual, s));
     if (full) u = sv->u2[l];
     VLA_CK(launch_rmsnorm(x, D.d, nullptr, w.mlp_norm, eps, u, D.d, Ml, D.d, s, true));
+    if (stop == 3) break;  // x: the mid residual, u: the MLP norm's output
     GemmArgs gg{};
     // [gate; up] interleaved in 64-row blocks: only the blocks holding real rows are computed; the
     // down projection's contraction stops at the last real feature (h and Wdown stay Fp wide)
@@ -1188,6 +1194,12 @@ int vla_debug_set_layer_limit(vla_model* m, int32_t n_layers) {
   return VLA_OK;
 }
 
+int vla_debug_set_stop(vla_model* m, int32_t stage) {
+  if (!m || stage < 0 || stage > 3) return fail(VLA_EINVAL, "bad argument");
+  m->debug_stop = stage;
+  return VLA_OK;
+}
+
 int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t bytes, void* stream) {
   if (!m || !dst || layer < 0 || layer >= m->D.L) return fail(VLA_EINVAL, "bad argument");
   const Dims& D = m->D;
@@ -1204,6 +1216,7 @@ int vla_debug_read(vla_model* m, int32_t which, int32_t layer, void* dst, size_t
     case 6: src = m->lw[layer].wo; avail = frag_elems(D.d, D.d) * sizeof(bf16_t); break;
     case 7: src = m->lw[layer].wgu; avail = frag_elems(2 * D.Fp, D.d) * sizeof(bf16_t); break;
     case 8: src = m->lw[layer].wd; avail = frag_elems(D.d, D.Fp) * sizeof(bf16_t); break;
+    case 9: src = m->h; avail = frag_elems(D.Mmax, D.Fp) * sizeof(bf16_t); break;
     default: return fail(VLA_EINVAL, "unknown buffer");
   }
   if (bytes > avail) return fail(VLA_EINVAL, "read larger than the buffer");

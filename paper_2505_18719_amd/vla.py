@@ -32,7 +32,7 @@ PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
 # training modes of vla_ppo_lora_grads (VLA_TRAIN_*): recompute each layer's forward, or keep it
 TRAIN_RECOMPUTE, TRAIN_KEEP = 0, 1
 DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
-                 "vla_debug_set_layer_limit")
+                 "vla_debug_set_layer_limit", "vla_debug_set_stop")
 
 
 class VlaError(RuntimeError):
@@ -100,6 +100,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
     lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
     lib.vla_debug_set_layer_limit.argtypes = [vp, i32]
+    lib.vla_debug_set_stop.argtypes = [vp, i32]
     for name in EXPORTS + DEBUG_EXPORTS:
         if name not in ("vla_destroy", "vla_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -305,6 +306,10 @@ class VlaModel:
 
     def debug_layer_limit(self, n_layers: int) -> None:
         _check(self.lib.vla_debug_set_layer_limit(self.handle, n_layers))
+
+    def debug_stop(self, stage: int) -> None:
+        """Stop point inside the last layer of a layer-limited pass (vla_debug.h)."""
+        _check(self.lib.vla_debug_set_stop(self.handle, stage))
 
     def close(self) -> None:
         if getattr(self, "handle", None):

@@ -42,7 +42,7 @@ def test_tiny_rollout_matches_oracle(tiny, T):
     z0, out = _rollout(tiny, inp, dev, T)
     st = compare_rollout(tiny.cfg, tiny.W, inp, out, T, label=f"tiny T={T}")
     assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["dent"] <= LOGP_TOL
-    assert st["mismatches"] == 0
+    assert st["mismatches"] == 0 and st["strict"] == 0
     np.testing.assert_array_equal(z0.cpu().numpy(), out["logits"][:, 0].cpu().numpy())
     toks = out["tokens"].cpu().numpy()
     assert ((toks >= tiny.cfg.action_begin) & (toks < tiny.cfg.vocab)).all()
@@ -55,7 +55,7 @@ def test_ragged_prompts_with_gains_match_oracle(tiny_ragged):
     inp, dev = S.inputs(seed=3, prompt_lens=[0, 40, 7, 33, 16])
     z0, out = _rollout(S, inp, dev, 1.5)
     st = compare_rollout(S.cfg, S.W, inp, out, 1.5, label="tiny ragged")
-    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
+    assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0 and st["strict"] == 0
 
 
 def test_teacher_forced_matches_oracle_and_decode(tiny_ragged):
@@ -153,6 +153,10 @@ def test_mid_rollout_and_teacher_forced_match_oracle():
     inp, dev = S.inputs(seed=0)
     z0, out = _rollout(S, inp, dev, 1.5)
     st = compare_rollout(S.cfg, S.W, inp, out, 1.5, label="mid")
+    # At 8 layers the float32-accumulation distance from the contract oracle (~2.5e-2 in the
+    # logits, the size of the contract's own rounding effect: test_fp32_noise_floor.py) can
+    # bridge top-2 margins above the 1e-3 near-tie scale; tokens must agree wherever the margin
+    # exceeds what the measured logit difference can bridge.
     assert st["dlogit"] <= LOGIT_TOL and st["dlogp"] <= LOGP_TOL and st["mismatches"] == 0
     tf = S.model.token_logprobs(dev["vis"], dev["ids"], inp.prompt_lens, out["tokens"].clone(), 1.5)
     torch.cuda.synchronize()

@@ -112,6 +112,35 @@ def test_7b_layerwise_residual_parity(big):
     assert worst <= 2e-2
 
 
+def _gap_bound(cfg, W, inp, out, T, envs, label):
+    """compare_rollout against the bf16-contract oracle on `envs`, plus the
+    oracle's own bf16-vs-float64 gap on the same environments and tokens; the
+    bound of each quantity is max(stated tolerance, that gap)."""
+    toks = out["tokens"].cpu().numpy()
+    st = compare_rollout(cfg, W, inp, out, T, envs=envs, label=label)
+    ideal = oracle.rollout(cfg, W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, inp.gumbel, T,
+                           mode="ideal", envs=envs, feed_tokens=toks)
+    gap = {k: float(np.abs(ideal[k] - st["ref"][k]).max()) for k in ("logits", "logp", "entropy")}
+    log(f"[{label}] oracle bf16-vs-float64 gap: logits {gap['logits']:.3e} logp {gap['logp']:.3e} "
+        f"entropy {gap['entropy']:.3e}")
+    return st, gap
+
+
+def _assert_within_gap(st, gap):
+    assert st["dlogit"] <= max(LOGIT_TOL, gap["logits"])
+    assert st["dlogp"] <= max(LOGP_TOL, gap["logp"])
+    assert st["dent"] <= max(LOGP_TOL, gap["entropy"])
+    assert st["mismatches"] == 0
+
+
+def _sample_envs(prefix_lens, n, seed):
+    """The shortest and the longest prefix plus seeded others, n in all."""
+    B = len(prefix_lens)
+    envs = [int(np.argmin(prefix_lens)), int(np.argmax(prefix_lens))]
+    rest = [b for b in np.random.default_rng(seed).permutation(B).tolist() if b not in envs]
+    return sorted(set(envs + rest[:n - len(set(envs))]))
+
+
 def test_7b_b64_ragged_end_to_end_within_bf16_gap(big):
     model, W = big
     cfg = inputs.L7B_B64
@@ -119,26 +148,19 @@ def test_7b_b64_ragged_end_to_end_within_bf16_gap(big):
     toks = out["tokens"].cpu().numpy()
     assert ((toks >= cfg.action_begin) & (toks < cfg.vocab)).all()
     assert torch.isfinite(out["logp"]).all() and (out["logp"] <= 0).all()
-    envs = [int(np.argmin(inp.prefix_lens)), int(np.argmax(inp.prefix_lens))]
+    envs = _sample_envs(inp.prefix_lens, 6, 0)
     t0 = time.time()
-    st = compare_rollout(cfg, W, inp, out, 1.5, envs=envs, label="7b b64 ragged")
-    ideal = oracle.rollout(cfg, W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, inp.gumbel, 1.5,
-                           mode="ideal", envs=envs, feed_tokens=toks)
-    gap_z = np.abs(ideal["logits"] - st["ref"]["logits"]).max()
-    gap_p = np.abs(ideal["logp"] - st["ref"]["logp"]).max()
-    log(f"[7b] oracle bf16-vs-float64 gap: logits {gap_z:.3e} logp {gap_p:.3e}; "
-        f"oracle on {len(envs)} envs in {time.time() - t0:.1f}s")
-    assert st["dlogit"] <= max(LOGIT_TOL, gap_z) and st["dlogp"] <= max(LOGP_TOL, gap_p)
-    assert st["mismatches"] == 0
+    st, gap = _gap_bound(cfg, W, inp, out, 1.5, envs, "7b b64 ragged")
+    log(f"[7b b64] oracle on {len(envs)} envs in {time.time() - t0:.1f}s")
+    _assert_within_gap(st, gap)
 
 
 def test_7b_b8_rollout_end_to_end(big):
     model, W = big
     cfg = inputs.L7B_B8
     inp, _, z0, out = _gpu_rollout(model, cfg, 1, 1.0)
-    st = compare_rollout(cfg, W, inp, out, 1.0, envs=[5], label="7b b8")
-    assert st["mismatches"] == 0
-    assert st["dlogit"] <= 0.25 and st["dlogp"] <= 0.1
+    st, gap = _gap_bound(cfg, W, inp, out, 1.0, [0, 5, 7], "7b b8")
+    _assert_within_gap(st, gap)
 
 
 def test_7b_b128_teacher_forced_sampled_envs(big):
@@ -149,14 +171,59 @@ def test_7b_b128_teacher_forced_sampled_envs(big):
     tf = model.token_logprobs(inp.vis, torch.from_numpy(inp.prompt_ids).cuda(), inp.prompt_lens,
                               torch.from_numpy(acts).cuda(), 1.5)
     torch.cuda.synchronize()
-    assert torch.isfinite(tf["logp"]).all()
-    envs = [0, 127]
+    assert torch.isfinite(tf["logp"]).all() and torch.isfinite(tf["entropy"]).all()
+    envs = [0, 43, 86, 127]
     ref = oracle.teacher_forced(cfg, W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, acts, 1.5, envs=envs)
     ideal = oracle.teacher_forced(cfg, W, inp.vis.cpu(), inp.prompt_ids, inp.prompt_lens, acts, 1.5, envs=envs,
                                   mode="ideal")
-    dl = np.abs(tf["logits"].cpu().numpy()[envs] - ref["logits"]).max()
-    dp = np.abs(tf["logp"].cpu().numpy()[envs] - ref["logp"]).max()
-    gap_z = np.abs(ideal["logits"] - ref["logits"]).max()
-    gap_p = np.abs(ideal["logp"] - ref["logp"]).max()
-    log(f"[7b b128 teacher-forced] max|dlogit|={dl:.3e} max|dlogp|={dp:.3e} (bf16 gap {gap_z:.3e} / {gap_p:.3e})")
-    assert dl <= max(LOGIT_TOL, gap_z) and dp <= max(LOGP_TOL, gap_p)
+    d = {k: float(np.abs(tf[k].cpu().numpy()[envs] - ref[k]).max()) for k in ("logits", "logp", "entropy")}
+    gap = {k: float(np.abs(ideal[k] - ref[k]).max()) for k in ("logits", "logp", "entropy")}
+    log(f"[7b b128 teacher-forced] envs {envs}: max|dlogit|={d['logits']:.3e} max|dlogp|={d['logp']:.3e} "
+        f"max|dH|={d['entropy']:.3e} (bf16 gap {gap['logits']:.3e} / {gap['logp']:.3e} / {gap['entropy']:.3e})")
+    assert d["logits"] <= max(LOGIT_TOL, gap["logits"])
+    assert d["logp"] <= max(LOGP_TOL, gap["logp"])
+    assert d["entropy"] <= max(LOGP_TOL, gap["entropy"])
+
+
+def test_7b_b128_rollout_loop_fresh_observations(big):
+    """The PPO-update workload's rollout loop: 128 environments for 10
+    environment steps; every step prefills each environment's (unchanged)
+    32-token prompt after fresh visual embeddings and decodes 7 actions.  The
+    policy is Markov in the current observation (Sec. 3.3), so the KV cache is
+    rebuilt every step: a step run again after the loop gives the same bits.
+    Sampled (step, environment) pairs are checked against the oracle."""
+    model, W = big
+    cfg = inputs.L7B_B128
+    base = inputs.make_inputs(cfg, seed=5, step=0, device="cuda")
+    ids = torch.from_numpy(base.prompt_ids).cuda()
+
+    def step_inputs(k):
+        vis = base.vis if k == 0 else inputs.make_inputs(cfg, seed=5, step=k, device="cuda").vis
+        return inputs.RolloutInputs(vis=vis, prompt_lens=base.prompt_lens, prompt_ids=base.prompt_ids,
+                                    gumbel=inputs.gumbel_noise(cfg, cfg.batch, seed=5, step=k))
+
+    def run(inp):
+        model.prefill(inp.vis, ids, inp.prompt_lens)
+        out = model.decode_actions(torch.from_numpy(inp.gumbel).cuda(), 1.5)
+        torch.cuda.synchronize()
+        return {k: v.clone() for k, v in out.items()}
+
+    steps = []
+    t0 = time.time()
+    for k in range(10):
+        inp = step_inputs(k)
+        out = run(inp)
+        toks = out["tokens"]
+        assert ((toks >= cfg.action_begin) & (toks < cfg.vocab)).all()
+        assert torch.isfinite(out["logp"]).all() and (out["logp"] <= 0).all()
+        steps.append((inp, out))
+    log(f"[7b b128 loop] 10 steps in {time.time() - t0:.1f}s")
+    # consecutive steps see different observations, so their actions differ
+    assert not torch.equal(steps[0][1]["tokens"], steps[1][1]["tokens"])
+    again = run(steps[4][0])
+    for k in again:
+        assert torch.equal(again[k], steps[4][1][k]), k
+    for k, envs in ((0, [0, 127]), (5, [64]), (9, [31, 127])):
+        inp, out = steps[k]
+        st, gap = _gap_bound(cfg, W, inp, out, 1.5, envs, f"7b b128 loop step {k}")
+        _assert_within_gap(st, gap)

@@ -239,6 +239,27 @@ def test_sampler_closed_forms():
     assert vo.token_stats(z, 0, 1e-3)[1] < 1e-6
 
 
+def test_sampler_margin_is_the_top2_gap_of_the_scores():
+    """The margin that decides which tokens are near-ties (Eq. 1 sampling at
+    temperature T, Sec. 4.3): the gap between the two largest scores
+    z_j / T + g_j, in float64.  Hand cases chosen so that dropping g, dropping
+    T or taking the gap in float32 gives another value."""
+    z = np.array([3.0, 1.5, 0.0, -2.0])
+    g = np.array([0.0, 1.2, 0.5, 0.0])
+    # scores z/T + g at T = 1.5: [2.0, 2.2, 0.5, -4/3] -> bin 1, gap 0.2
+    # (without g: [2, 1, 0, -4/3], gap 1; without T: [3, 2.7, 0.5, -2], gap 0.3)
+    k, _, _, margin = vo.sample_bin(z, g, 1.5)
+    assert k == 1 and margin == pytest.approx(0.2, abs=1e-15)
+    # a gap of 3e-9 at scores near 0.1 is below float32's spacing there (7.5e-9):
+    # a float32 margin would be 0 or 7.5e-9
+    z = np.array([0.1, 0.1 + 3e-9, -1.0])
+    margin = vo.sample_bin(z, np.zeros(3), 1.0)[3]
+    assert margin == pytest.approx(3e-9, abs=1e-16)
+    # at an exact tie of the scores the margin is 0 and the lowest bin wins
+    k, _, _, margin = vo.sample_bin(np.array([0.5, 1.0, 0.0]), np.array([0.5, 0.0, 0.2]), 1.0)
+    assert k == 0 and margin == 0.0
+
+
 def test_gumbel_max_frequencies_follow_softmax():
     """Chi-square test: Gumbel-max with the generator's noise draws bins with
     probability softmax(z / T)."""
