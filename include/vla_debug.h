@@ -23,6 +23,22 @@ int vla_debug_gemm(const void* A, const void* W, int32_t M, int32_t N, int32_t K
 int vla_debug_skinny(const void* A, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
                      float* scratch, float* C, void* stream);
 
+/* vla_debug_skinny without a scratch argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops, hosts
+ * that forbid allocation): the split-K partials live in a fixed device array
+ * of 2^23 floats (32 MiB) that the library holds on each GPU it runs on until
+ * the process ends.  Same plan and kernels as vla_debug_skinny, so C gets the
+ * same bits.  Requires M <= 128, N % 64 == 0, K % 256 == 0 (else
+ * VLA_EUNSUPPORTED) and slots * M * N <= 2^23, where slots (<= 16) is the
+ * plan's largest number of partial slots of a column tile (else VLA_ESHAPE;
+ * e.g. M = 64 with N = 12288, K = 4096 fits).  Allocates nothing; every call
+ * on a GPU shares that GPU's array, so calls that overlap on one GPU (on
+ * different streams, or from different threads) race and give wrong results;
+ * calls on one stream run in order.  Every partial slot the reduction reads
+ * is written by the same call first, so nothing needs clearing. */
+int vla_debug_skinny_noalloc(const void* A, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
+                             float* C, void* stream);
+
 /* Repack a row-major bf16 matrix src [rows, K] (row stride ld) into the frag
  * layout the GEMMs read: 16 x 32 blocks of 1 KB; 16-row block r / 16 holds
  * K / 32 + 1 consecutive blocks (the last one spare), K block k / 32 at

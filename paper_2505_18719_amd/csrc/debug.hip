@@ -1,11 +1,45 @@
 // Test hooks: single kernels of the rollout path behind a C ABI.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <string>
+
 #include "kernels.h"
 #include "vla.h"
 #include "vla_debug.h"
 
 using namespace vla;
+
+namespace {
+
+// Split-K partials of vla_debug_skinny_noalloc: a file-scope device array that
+// every GPU the library runs on holds until the process ends.  Host code never
+// uses its name as an address: the device address is looked up once per device.
+constexpr size_t kNoAllocScratchFloats = size_t(1) << 23;  // 32 MiB
+__device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (looked up on the first call there).
+int scratch_on_current_device(float** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return set_error(VLA_EHIP, "hipGetDevice failed or device index out of range");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(VLA_EHIP, (std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e)).c_str());
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return VLA_OK;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -30,6 +64,27 @@ int vla_debug_skinny(const void* A, const void* W, int32_t M, int32_t N, int32_t
   SkinnyArgs a{static_cast<const bf16_t*>(A), M, static_cast<const bf16_t*>(W), N, K, scratch};
   if (launch_skinny(a, p, s) != hipSuccess) return VLA_EHIP;
   return launch_reduce_sum(scratch, p, C, M, N, s) == hipSuccess ? VLA_OK : VLA_EHIP;
+}
+
+int vla_debug_skinny_noalloc(const void* A, const void* W, int32_t M, int32_t N, int32_t K, int32_t workgroups,
+                             float* C, void* stream) {
+  if (!A || !W || !C || M < 0 || N <= 0 || K <= 0 || workgroups < 1)
+    return set_error(VLA_EINVAL, "NULL pointer or non-positive size");
+  if (M > 128 || N % 64 != 0 || K % 256 != 0)
+    return set_error(VLA_EUNSUPPORTED, "needs M <= 128, N % 64 == 0, K % 256 == 0");
+  // the plan of vla_debug_skinny, so that both give the same bits
+  const SkinnyPlan p = skinny_plan(N, K, workgroups, 16);
+  if ((size_t)p.slots * M * N > kNoAllocScratchFloats)
+    return set_error(VLA_ESHAPE, "partial sums exceed the fixed scratch: slots * M * N must be <= 2^23 floats");
+  float* part = nullptr;
+  const int rc = scratch_on_current_device(&part);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SkinnyArgs a{static_cast<const bf16_t*>(A), M, static_cast<const bf16_t*>(W), N, K, part};
+  hipError_t e = launch_skinny(a, p, s);
+  if (e == hipSuccess) e = launch_reduce_sum(part, p, C, M, N, s);
+  if (e != hipSuccess) return set_error(VLA_EHIP, hipGetErrorString(e));
+  return VLA_OK;
 }
 
 int vla_debug_pack_frag(const void* src, int32_t rows, int32_t K, int32_t ld, void* dst, void* stream) {

@@ -100,6 +100,9 @@ __device__ inline float skinny_sum(const float* __restrict__ part, const SkinnyP
 SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots);
 hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t s);
 
+// Set the calling thread's message for vla_last_error and return `code`.
+int set_error(int code, const char* msg);
+
 // Elementwise / reduction kernels
 struct EmbedArgs {
   float* x;                     // [M, d] out

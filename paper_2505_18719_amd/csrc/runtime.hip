@@ -28,6 +28,12 @@ int fail(int code, const std::string& msg) {
   return code;
 }
 
+}  // namespace
+
+int vla::set_error(int code, const char* msg) { return fail(code, msg); }
+
+namespace {
+
 #define VLA_CK(expr)                                                                        \
   do {                                                                                      \
     hipError_t e_ = (expr);                                                                 \

@@ -32,7 +32,7 @@ PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
 # training modes of vla_ppo_lora_grads (VLA_TRAIN_*): recompute each layer's forward, or keep it
 TRAIN_RECOMPUTE, TRAIN_KEEP = 0, 1
 DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
-                 "vla_debug_set_layer_limit", "vla_debug_set_stop")
+                 "vla_debug_set_layer_limit", "vla_debug_set_stop", "vla_debug_skinny_noalloc")
 
 
 class VlaError(RuntimeError):
@@ -96,6 +96,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_last_error.restype = ctypes.c_char_p
     lib.vla_debug_gemm.argtypes = [vp, vp, i32, i32, i32, vp, vp]
     lib.vla_debug_skinny.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp]
+    lib.vla_debug_skinny_noalloc.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp]
     lib.vla_debug_pack_frag.argtypes = [vp, i32, i32, i32, vp, vp]
     lib.vla_debug_sample.argtypes = [vp, i32, i32, i32, i32, i32, vp, f32, vp, vp, vp, vp, vp, vp]
     lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
