@@ -69,8 +69,10 @@ def check_line(result):
 # the kernel sources it was taken on; it is reported only while they match.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_openvla7b_b64.md")
 TRAFFIC_SOURCES = {"prefill_gemm": ["gemm_prefill.hip", "common.h"],
-                   "decode_gemm": ["gemm_decode.hip", "common.h"]}
-TRAFFIC_KERNELS = {"prefill_gemm": "gemm_bf16_kernel", "decode_gemm": "skinny_kernel"}
+                   "decode_gemm": ["gemm_decode.hip", "skinny_dev.h", "common.h"],
+                   "decode_layer": ["decode_layer.hip", "skinny_dev.h", "common.h"]}
+TRAFFIC_KERNELS = {"prefill_gemm": "gemm_bf16_kernel", "decode_gemm": "skinny_kernel",
+                   "decode_layer": "decode_layer_kernel"}
 CALIB_ELEMS = 1 << 28       # bf16 elements of the calibration kernel: reads and writes 512 MiB
 
 
@@ -167,9 +169,170 @@ def cpu_baseline(cfg, w, inp, layers, T):
                    inp.gumbel[b:b + 1], T, mode="bf16")
     dt = time.perf_counter() - t0
     t_env = dt * cfg.n_layers / layers
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": 1.0 / t_env, "unit": "actions/s", "cores": int(cores), "kind": "oracle",
+            "cpu": cpu, "extrapolated": True,
             "sample": f"1 environment (prefix {int(inp.prefix_lens[b])} tokens), prefill + 7-token decode + "
-                      f"log-probs over {layers} of {cfg.n_layers} layers in {dt:.1f} s, scaled x{cfg.n_layers / layers:g}"}
+                      f"log-probs over {layers} of {cfg.n_layers} layers in {dt:.1f} s; the rate is extrapolated "
+                      f"to all layers (x{cfg.n_layers / layers:g}: every layer does the same work)"}
+
+
+def step_work(cfg, inp):
+    """Algorithmic work of one rollout step on its own inputs: prefill flops
+    (the GEMMs and causal attention actually run, plus the action head) and
+    decode HBM bytes (every 7B weight once per decode pass, the action rows of
+    the LM head, the KV cache read and appended, the embedding rows)."""
+    d, F, L, B = cfg.d_model, cfg.d_ffn, cfg.n_layers, inp.batch
+    layer_params = 4 * d * d + 3 * d * F
+    Lb = inp.prefix_lens.astype(np.float64)
+    flops = pass_flops(d, F, L, Lb, 1) + 2 * d * cfg.action_bins * B
+    nbytes = 0.0
+    for t in range(1, cfg.n_actions):
+        nbytes += 2 * layer_params * L + 2 * cfg.action_bins * d + 4 * d * L * (Lb + t).sum() + 2 * d * B
+    return flops, nbytes
+
+
+def measure_rollout(model, cfg, sets, steps, warmup, T, dev):
+    """Rollout steps (vla_prefill + vla_decode_actions) over device-resident
+    input sets, step k on sets[k % len(sets)]: `warmup` untimed steps, then
+    `steps` timed ones between two synchronisations, with HIP events around
+    each step's prefill and decode and the library's per-launch events on the
+    prefill GEMM and attention; then one separately profiled decode (decode
+    GEMM and attention launches), since events between the ~10^3 decode
+    launches would perturb the timed region."""
+    import torch
+    B = sets[0][0].batch
+    logits = torch.empty(B, cfg.action_bins, dtype=torch.float32, device=dev)
+    out = {"tokens": torch.empty(B, cfg.n_actions, dtype=torch.int32, device=dev),
+           "logp": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev),
+           "entropy": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev)}
+    stream = torch.cuda.current_stream(dev)
+    n = len(sets)
+
+    def step(k, ev=None):
+        inp, ids, g = sets[k % n]
+        if ev:
+            ev[0].record(stream)
+        model.prefill(inp.vis, ids, inp.prompt_lens, out=logits)
+        if ev:
+            ev[1].record(stream)
+        model.decode_actions(g, T, batch=B, out=out)
+        if ev:
+            ev[2].record(stream)
+
+    for k in range(warmup):
+        step(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    model.profile_begin(("prefill_gemm", "prefill_attn"))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(warmup + k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    prof = model.profile_end()
+    inp0, ids0, g0 = sets[0]
+    model.prefill(inp0.vis, ids0, inp0.prompt_lens, out=logits)
+    model.profile_begin(("decode_gemm", "decode_attn", "decode_layer"))
+    model.decode_actions(g0, T, batch=B, out=out)
+    dprof = model.profile_end()
+    flops = nbytes = 0.0
+    for k in range(steps):
+        f, b = step_work(cfg, sets[(warmup + k) % n][0])
+        flops += f / steps
+        nbytes += b / steps
+    prefill_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    decode_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    pg = prof["prefill_gemm"]
+    # the decode's weight-streaming kernel: the persistent layer kernel where it runs, else the projections
+    layer = dprof["decode_layer"]["launches"] > 0
+    dg = dprof["decode_layer"] if layer else dprof["decode_gemm"]
+    g_tflops = pg["work"] / (pg["ms"] * 1e-3) / 1e12
+    dg_gbs = dg["work"] / (dg["ms"] * 1e-3) / 1e9
+    return {
+        "ms_per_step": wall * 1e3 / steps, "prefill_ms": prefill_ms, "decode_ms": decode_ms,
+        "prefill_mfma_frac": flops / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "decode_hbm_gbs": nbytes / (decode_ms * 1e-3) / 1e9,
+        "decode_hbm_frac": nbytes / (decode_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+        "roofline": {"kernel": "gemm_bf16_kernel (prefill QKV/O/gate-up/down)", "bound": "mfma",
+                     "achieved": g_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": g_tflops / PEAK_BF16_TFLOPS, "avg_launch_ms": pg["ms"] / max(pg["launches"], 1),
+                     "launches": pg["launches"]},
+        "roofline_decode": {"kernel": ("decode_layer_kernel (per layer and step: O, gate/up, down and the next QKV "
+                                       "projection with their norms, one persistent launch)") if layer else
+                                      "skinny_kernel (decode QKV/O/gate-up/down)", "bound": "hbm", "key": ("decode_layer" if layer else "decode_gemm"),
+                            "achieved": dg_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": dg_gbs / PEAK_HBM_GBS, "avg_launch_ms": dg["ms"] / max(dg["launches"], 1),
+                            "launches": dg["launches"]},
+        "prof": prof, "dprof": dprof,
+    }
+
+
+def teacher_forced_pass(model, cfg, inp, ids, acts, T, dev, reps=2):
+    """Mean time of `reps` teacher-forced passes (vla_token_logprobs) after an untimed one."""
+    import torch
+    stream = torch.cuda.current_stream(dev)
+    model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tf_ms = e0.elapsed_time(e1) / reps
+    d, F, L, B = cfg.d_model, cfg.d_ffn, cfg.n_layers, inp.batch
+    Lb = inp.prefix_lens.astype(np.float64) + cfg.n_actions
+    tf_flops = pass_flops(d, F, L, Lb, cfg.n_actions) + 2 * d * cfg.action_bins * B * cfg.n_actions
+    return {"ms": tf_ms, "rows": int(Lb.sum()),
+            "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
+
+
+def secondary_configs(model, w, T, dev, steps):
+    """The other 7B-shape workloads, on the same handle and weights:
+    batch 8 (prompt 32) rollout steps, and the PPO-update workload at batch
+    128: a 10-step rollout loop in which every environment keeps its 32-token
+    prompt and sees fresh visual embeddings each step (the KV cache is rebuilt
+    every step), then a teacher-forced pass over 128 x 295 rows."""
+    import torch
+    from paper_2505_18719_amd import inputs as I
+    res = {}
+    cfg = I.L7B_B8
+    sets = []
+    for k in range(4):
+        inp = I.make_inputs(cfg, seed=0, step=k, device=dev)
+        sets.append((inp, torch.from_numpy(inp.prompt_ids).to(dev), torch.from_numpy(inp.gumbel).to(dev)))
+    r = measure_rollout(model, cfg, sets, max(steps, 10), 3, T, dev)
+    res[cfg.name] = {"actions_per_s": cfg.batch / (r["ms_per_step"] * 1e-3),
+                     **{k: v for k, v in r.items() if k not in ("prof", "dprof")}}
+    log(f"[bench] {cfg.name}: {r['ms_per_step']:.2f} ms/step (prefill {r['prefill_ms']:.2f}, "
+        f"decode {r['decode_ms']:.2f})")
+    cfg = I.L7B_B128
+    base = I.make_inputs(cfg, seed=0, step=0, device=dev)
+    ids = torch.from_numpy(base.prompt_ids).to(dev)
+    sets = []
+    for k in range(10):
+        vis = base.vis if k == 0 else I.make_inputs(cfg, seed=0, step=k, device=dev).vis
+        inp = I.RolloutInputs(vis=vis, prompt_lens=base.prompt_lens, prompt_ids=base.prompt_ids,
+                              gumbel=I.gumbel_noise(cfg, cfg.batch, seed=0, step=k))
+        sets.append((inp, ids, torch.from_numpy(inp.gumbel).to(dev)))
+    r = measure_rollout(model, cfg, sets, 10, 1, T, dev)
+    acts = torch.from_numpy(I.stored_actions(cfg, cfg.batch, seed=0)).to(dev)
+    tf = teacher_forced_pass(model, cfg, base, ids, acts, T, dev)
+    res[cfg.name] = {"rollout_loop_steps": 10, "actions_per_s": cfg.batch / (r["ms_per_step"] * 1e-3),
+                     **{k: v for k, v in r.items() if k not in ("prof", "dprof")}, "teacher_forced": tf}
+    log(f"[bench] {cfg.name}: rollout loop {r['ms_per_step']:.2f} ms/step (prefill {r['prefill_ms']:.2f}, "
+        f"decode {r['decode_ms']:.2f}); teacher-forced pass over {tf['rows']} rows {tf['ms']:.2f} ms")
+    return res
 
 
 def main():
@@ -182,6 +345,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=8, help="decoder layers in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher-forced", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the batch-8 and batch-128 7B workloads")
     ap.add_argument("--no-value", action="store_true")
     ap.add_argument("--no-learning", action="store_true")
     ap.add_argument("--no-lora-merge", action="store_true")
@@ -209,84 +373,29 @@ def main():
     dev = torch.device("cuda:0")
     log(f"[bench] {cfg.name}: building weights and inputs")
     w = I.make_weights(cfg, seed=0, device=dev)
-    model = VlaModel(cfg, w, max_batch=B, device=dev)
+    # one handle serves every 7B-shape workload (batch 8, 64 and 128; sequences up to 311 rows)
+    model = VlaModel(cfg, w, max_batch=max(B, 128), max_seq=max(cfg.max_seq, I.L7B_B64.max_seq), device=dev)
     n_sets = max(1, min(args.steps + args.warmup, 4))
     sets = []
     for k in range(n_sets):
         inp = I.make_inputs(cfg, seed=0, step=k, device=dev)
         sets.append((inp, torch.from_numpy(inp.prompt_ids).to(dev), torch.from_numpy(inp.gumbel).to(dev)))
-    logits = torch.empty(B, cfg.action_bins, dtype=torch.float32, device=dev)
-    out = {"tokens": torch.empty(B, cfg.n_actions, dtype=torch.int32, device=dev),
-           "logp": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev),
-           "entropy": torch.empty(B, cfg.n_actions, dtype=torch.float32, device=dev)}
     stream = torch.cuda.current_stream(dev)
-
-    def step(k, ev=None):
-        inp, ids, g = sets[k % n_sets]
-        if ev:
-            ev[0].record(stream)
-        model.prefill(inp.vis, ids, inp.prompt_lens, out=logits)
-        if ev:
-            ev[1].record(stream)
-        model.decode_actions(g, T, batch=B, out=out)
-        if ev:
-            ev[2].record(stream)
-
-    for k in range(args.warmup):
-        step(k)
     if args.copy_calibration:
         src = torch.ones(CALIB_ELEMS, dtype=torch.bfloat16, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         torch.neg(src, out=dst)
         del src, dst
-    torch.cuda.synchronize()
-    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
-
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    model.profile_begin(("prefill_gemm", "prefill_attn"))
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(args.warmup + k, evs[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    prof = model.profile_end()
-    prefill_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    decode_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    ms_per_step = wall * 1e3 / args.steps
-    log(f"[bench] {ms_per_step:.2f} ms/step (prefill {prefill_ms:.2f} ms, decode {decode_ms:.2f} ms)")
-
-    # decode kernels profiled on a separate step (events between the ~10^3
-    # decode launches would perturb the timed region)
-    inp0, ids0, g0 = sets[0]
-    model.prefill(inp0.vis, ids0, inp0.prompt_lens, out=logits)
-    model.profile_begin(("decode_gemm", "decode_attn"))
-    model.decode_actions(g0, T, batch=B, out=out)
-    dprof = model.profile_end()
-
-    # algorithmic work per step (the step's own inputs)
+    log(f"[bench] timing {args.steps} steps after {args.warmup} warm-up steps")
+    r = measure_rollout(model, cfg, sets, args.steps, args.warmup, T, dev)
+    ms_per_step = r["ms_per_step"]
+    log(f"[bench] {ms_per_step:.2f} ms/step (prefill {r['prefill_ms']:.2f} ms, decode {r['decode_ms']:.2f} ms)")
     d, F, L = cfg.d_model, cfg.d_ffn, cfg.n_layers
     layer_params = 4 * d * d + 3 * d * F
-    prefill_flops = decode_bytes = 0.0
-    for k in range(args.steps):
-        inp = sets[(args.warmup + k) % n_sets][0]
-        Lb = inp.prefix_lens.astype(np.float64)
-        prefill_flops += pass_flops(d, F, L, Lb, 1) + 2 * d * cfg.action_bins * B
-        for t in range(1, cfg.n_actions):
-            decode_bytes += 2 * layer_params * L + 2 * cfg.action_bins * d \
-                + 4 * d * L * (Lb + t).sum() + 2 * d * B  # weights + head rows + KV + embeddings
-    prefill_flops /= args.steps
-    decode_bytes /= args.steps
-
     traffic = load_traffic()
-    pg = prof["prefill_gemm"]
-    g_ms = pg["ms"] / max(pg["launches"], 1)
-    g_tflops = pg["work"] / (pg["ms"] * 1e-3) / 1e12
-    dg = dprof["decode_gemm"]
-    dg_gbs = dg["work"] / (dg["ms"] * 1e-3) / 1e9
-    da = dprof["decode_attn"]
-    pa = prof["prefill_attn"]
+    prof, dprof = r["prof"], r["dprof"]
+    pg, da, pa, dg = prof["prefill_gemm"], dprof["decode_attn"], prof["prefill_attn"], dprof["decode_gemm"]
 
     result = {
         "metric": "VLA actions/sec at 7B shape, batch 64; decode HBM GB/s; prefill MFMA util",
@@ -308,43 +417,28 @@ def main():
                    "global_batch": B, "seq_len": int(cfg.n_visual + cfg.prompt_max + cfg.n_actions),
                    "parallelism": "single GPU"},
         "action_tokens_per_s": B * cfg.n_actions / (ms_per_step * 1e-3),
-        "prefill_ms": prefill_ms,
-        "decode_ms": decode_ms,
-        "prefill_mfma_frac": prefill_flops / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-        "decode_hbm_gbs": decode_bytes / (decode_ms * 1e-3) / 1e9,
-        "decode_hbm_frac": decode_bytes / (decode_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
-        "roofline": {"kernel": "gemm_bf16_kernel (prefill QKV/O/gate-up/down)", "bound": "mfma",
-                     "achieved": g_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": g_tflops / PEAK_BF16_TFLOPS, "traffic": traffic.get("prefill_gemm"),
-                     "avg_launch_ms": g_ms, "launches": pg["launches"]},
-        "roofline_decode": {"kernel": "skinny_kernel (decode QKV/O/gate-up/down)", "bound": "hbm",
-                            "achieved": dg_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                            "frac": dg_gbs / PEAK_HBM_GBS, "traffic": traffic.get("decode_gemm"),
-                            "avg_launch_ms": dg["ms"] / max(dg["launches"], 1), "launches": dg["launches"]},
+        "prefill_ms": r["prefill_ms"],
+        "decode_ms": r["decode_ms"],
+        "prefill_mfma_frac": r["prefill_mfma_frac"],
+        "decode_hbm_gbs": r["decode_hbm_gbs"],
+        "decode_hbm_frac": r["decode_hbm_frac"],
+        "roofline": {**r["roofline"], "traffic": traffic.get("prefill_gemm")},
+        "roofline_decode": {**r["roofline_decode"], "traffic": traffic.get(r["roofline_decode"]["key"])},
         "kernels": {"prefill_attn_tflops": pa["work"] / max(pa["ms"], 1e-9) / 1e9,
                     "prefill_attn_ms_per_step": pa["ms"] / args.steps,
                     "prefill_gemm_ms_per_step": pg["ms"] / args.steps,
                     "decode_attn_gbs": da["work"] / max(da["ms"], 1e-9) / 1e6,
-                    "decode_attn_ms": da["ms"], "decode_gemm_ms": dg["ms"]},
+                    "decode_attn_ms": da["ms"], "decode_gemm_ms": dg["ms"],
+                    "decode_layer_ms": dprof["decode_layer"]["ms"]},
     }
 
     if not args.no_teacher_forced:
         inp, ids, _ = sets[0]
         acts = torch.from_numpy(I.stored_actions(cfg, B, seed=0)).to(dev)
-        model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(2):
-            model.token_logprobs(inp.vis, ids, inp.prompt_lens, acts, T)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        tf_ms = e0.elapsed_time(e1) / 2
-        Lb = inp.prefix_lens.astype(np.float64) + cfg.n_actions
-        tf_flops = pass_flops(d, F, L, Lb, cfg.n_actions) + 2 * d * cfg.action_bins * B * cfg.n_actions
-        result["teacher_forced"] = {"ms": tf_ms, "rows": int(Lb.sum()),
-                                    "mfma_frac": tf_flops / (tf_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-                                    "log_probs_per_s": B * cfg.n_actions / (tf_ms * 1e-3)}
+        result["teacher_forced"] = teacher_forced_pass(model, cfg, inp, ids, acts, T, dev)
+
+    if not args.no_configs:
+        result["configs"] = secondary_configs(model, w, T, dev, args.steps)
 
     if not args.no_value:
         # value estimate of every environment's prefix (Alg. 1), a value model of

@@ -50,6 +50,8 @@ extern "C" {
 /* device-side flags (see vla_read_device_flags) */
 #define VLA_FLAG_BAD_PROMPT_ID 1u   /* a prompt id outside [0, vocab): a zero row was used */
 #define VLA_FLAG_BAD_ACTION 2u      /* a teacher-forced token outside the action range: scored as NaN */
+#define VLA_FLAG_SYNC_TIMEOUT 4u    /* a grid barrier of the persistent decode kernel timed out: that decode's
+                                       outputs are invalid */
 
 /* Decoder shape and capacity.
  *   d_model = n_heads * head_dim, head_dim in {64, 128}, d_model % 256 == 0,
@@ -235,7 +237,8 @@ int vla_read_device_flags(vla_model* m, void* stream, uint32_t* flags_host);
 #define VLA_PROF_PREFILL_ATTN 1
 #define VLA_PROF_DECODE_GEMM 2
 #define VLA_PROF_DECODE_ATTN 3
-#define VLA_PROF_CATEGORIES 4
+#define VLA_PROF_DECODE_LAYER 4  /* persistent decode layer kernel: HBM bytes of its four projections */
+#define VLA_PROF_CATEGORIES 5
 int vla_profile_begin(vla_model* m, uint32_t mask);
 int vla_profile_end(vla_model* m, double* ms_host, double* work_host, int64_t* launches_host);
 

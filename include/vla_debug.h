@@ -88,6 +88,23 @@ int vla_debug_set_layer_limit(struct vla_model* m, int32_t n_layers);
  * the rest of the pass undone; the prefill logits are then not meaningful. */
 int vla_debug_set_stop(struct vla_model* m, int32_t stage);
 
+/* Decode path of later vla_decode_actions calls: 0 (the default) runs one
+ * kernel per projection and per consumer; 1 (where the device supports
+ * cooperative launches) runs each decoder layer's work after attention, and
+ * the next projection, in one persistent launch with grid barriers between
+ * its phases.  Both give the same bits; the persistent path measured slower
+ * (grid barriers and the row phases cost more than the kernel boundaries they
+ * replace). */
+int vla_debug_set_decode_path(struct vla_model* m, int32_t persistent);
+
+/* Phase timing of the persistent decode layer kernel: the launch of decoder
+ * layer `layer` at the first decode step of later vla_decode_actions calls
+ * (first 128-row chunk) writes, per workgroup g, 14 wall-clock stamps (the
+ * 100 MHz device clock) at stamps[16 g + k]: the start, then before and after
+ * each of its 6 grid barriers, and the end.  `stamps` is device memory of
+ * 16 * (compute units) uint64, or NULL to stop. */
+int vla_debug_trace_decode_layer(struct vla_model* m, int32_t layer, void* stamps);
+
 #ifdef __cplusplus
 }
 #endif

@@ -100,6 +100,31 @@ __device__ inline float skinny_sum(const float* __restrict__ part, const SkinnyP
 SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots);
 hipError_t launch_skinny(const SkinnyArgs& a, const SkinnyPlan& p, hipStream_t s);
 
+// Persistent decode layer (decode_layer.hip): everything of a decoder layer
+// after attention at one decode step, plus the next projection, in one
+// cooperative launch of G workgroups (one per CU).
+struct DecodeLayerArgs {
+  SkinnyArgs o, gu, dn, nx;            // O, [gate; up], down, and the next (QKV or action head) projections
+  SkinnyPlan p_o, p_gu, p_dn, p_nx;
+  float* x;                            // residual [M, d] fp32
+  const float* g_mlp;                  // MLP RMSNorm gain
+  const float* g_next;                 // the next RMSNorm's gain (next layer's attention norm, or the final norm)
+  bf16_t* ua;                          // MLP norm output [M, d] frag (gu.A)
+  bf16_t* h;                           // SwiGLU output [M, Fp] frag (dn.A)
+  bf16_t* ub;                          // next norm output [M, d] frag (nx.A)
+  int M, d, Fp;
+  float eps;
+  unsigned* bar;                       // barrier block: [0] global count, [1] abort word, [16 (1 + g % 8)] group counts
+  unsigned bar_base;                   // barriers passed before this launch in the current decode call
+  uint32_t* flags;                     // VLA flags (4: a barrier wait timed out)
+  unsigned long long* trace;           // test hook, or null: per workgroup 16 wall-clock stamps of its phases
+};
+constexpr int kDecodeLayerBarriers = 6;  // grid barriers per launch
+hipError_t launch_decode_layer(const DecodeLayerArgs& a, int G, hipStream_t s);
+// Whether the current device can run it: cooperative launches, and one workgroup
+// of every row-block variant resident per CU.
+bool decode_layer_supported();
+
 // Set the calling thread's message for vla_last_error and return `code`.
 int set_error(int code, const char* msg);
 

@@ -42,6 +42,7 @@ namespace {
 
 constexpr int kMaxSplits = 16;
 constexpr int kSkinnyRows = 128;
+constexpr int kMetaRing = 4;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up(int v, int a) { return (v + a - 1) / a * a; }
@@ -143,9 +144,12 @@ struct vla_model {
   int32_t* next_tok;  // [Bmax]
   uint32_t* flags;
   int32_t* meta_dev;
-  int32_t* meta_host;  // pinned staging
-  hipEvent_t meta_event;
-  bool meta_pending;
+  // pinned host staging of the per-call metadata: a ring of kMetaRing buffers, so that the
+  // host waits for a buffer's upload only when it runs kMetaRing calls ahead of the device
+  int32_t* meta_host;  // kMetaRing * meta_ints
+  hipEvent_t meta_event[kMetaRing];
+  bool meta_pending[kMetaRing];
+  int meta_slot;
   // device views into meta_dev
   int32_t *row_pos, *row_env, *env_row0, *env_len, *env_prefix, *env_prompt_off, *env_q0, *page_table, *head_rows;
   // decode state
@@ -158,6 +162,14 @@ struct vla_model {
   // decode GEMM work splits (one persistent workgroup per CU)
   SkinnyPlan plan_qkv, plan_o, plan_gu, plan_d, plan_head;
   int cus;  // compute units: the skinny GEMM's persistent grid
+  // persistent decode layer kernel: its buffers, and whether the device runs it
+  float *part_o, *part_gu, *part_dn, *part_nx;  // split-K partials of each projection of a layer launch
+  bf16_t *dec_ua, *dec_ub;                      // [Bmax, d] frag: MLP norm output, next norm output
+  unsigned* dec_bar;                            // barrier block (zeroed per decode call)
+  bool fused_ok;                                // cooperative launch of one workgroup per CU is possible
+  int decode_path;                              // test hook: 1 = persistent layer kernel, 0 = per-kernel (default)
+  unsigned long long* trace_buf;                // test hook: phase stamps of one layer launch, or null
+  int trace_layer;
   // live profiling
   struct ProfSlot {
     hipEvent_t a, b;
@@ -208,6 +220,15 @@ void plan(Layout& L, vla_model* m, const Dims& D, int n_layers) {
   M.hc = L.take<bf16_t>(frag_elems((size_t)D.Bmax * D.nact, D.Fp));
   M.next_tok = L.take<int32_t>(D.Bmax);
   M.flags = L.take<uint32_t>(4);
+  // persistent decode layer: one partial region per projection of a launch (each is read
+  // once per launch, so none needs cache maintenance between its phases)
+  M.part_o = L.take<float>((size_t)kMaxSplits * kSkinnyRows * D.d);
+  M.part_gu = L.take<float>((size_t)kMaxSplits * kSkinnyRows * 2 * D.Fp);
+  M.part_dn = L.take<float>((size_t)kMaxSplits * kSkinnyRows * D.d);
+  M.part_nx = L.take<float>((size_t)kMaxSplits * kSkinnyRows * std::max(3 * D.d, D.Ap));
+  M.dec_ua = L.take<bf16_t>(frag_elems(D.Bmax, D.d));
+  M.dec_ub = L.take<bf16_t>(frag_elems(D.Bmax, D.d));
+  M.dec_bar = L.take<unsigned>(256);
   M.meta_dev = L.take<int32_t>(D.meta_ints);
   L.off = align_up(L.off, 256);
 }
@@ -280,6 +301,60 @@ int head_logits(vla_model* m, const bf16_t* u, int R, float* logits, hipStream_t
   return VLA_OK;
 }
 
+// One decode step (token position prefix + step - 1) on the persistent layer
+// kernel: the token's embedding and first RMSNorm, layer 0's QKV projection,
+// then per layer the decode attention (with the QKV consumer) and one
+// decode_layer launch (everything after attention plus the next projection;
+// after the last layer the action head's), and the head's reduction into
+// logits_dec.  The arithmetic is that of the per-kernel path.
+int decode_step_fused(vla_model* m, int B, int step, unsigned& bar_base, hipStream_t s) {
+  const Dims& D = m->D;
+  const float eps = m->cfg.rms_eps;
+  VLA_CK(launch_embed_token_norm(m->next_tok, m->emb, m->x, m->dec_ub, m->lw[0].attn_norm, eps, B, D.d, D.V,
+                                 m->flags, s));
+  for (int r0 = 0; r0 < B; r0 += kSkinnyRows) {
+    const int rows = std::min(kSkinnyRows, B - r0);
+    float* x = m->x + (size_t)r0 * D.d;
+    bf16_t* o = m->u + frag_index(r0, 0, D.d);  // r0 is a multiple of 16: whole frag blocks
+    bf16_t* ua = m->dec_ua + frag_index(r0, 0, D.d);
+    bf16_t* ub = m->dec_ub + frag_index(r0, 0, D.d);
+    bf16_t* h = m->h + frag_index(r0, 0, D.Fp);
+    const int32_t* ptab = m->page_table + (size_t)r0 * D.max_pages;
+    const int32_t* eprefix = m->env_prefix + r0;
+    double kv_bytes = 0.0;
+    for (int b = r0; b < r0 + rows; ++b) kv_bytes += 2.0 * 2.0 * D.d * (double)(m->prefix_host[b] + step);
+    SkinnyArgs sq{ub, rows, m->lw[0].wqkv, 3 * D.d, D.d, m->part_nx};
+    PROF_LAUNCH(VLA_PROF_DECODE_GEMM, skinny_bytes(3.0 * D.d, D.d, rows), launch_skinny(sq, m->plan_qkv, s));
+    for (int l = 0; l < D.L; ++l) {
+      const LayerW& w = m->lw[l];
+      DecodeAttnArgs da{m->part_nx, m->plan_qkv, m->rope, o, m->kv[l], ptab, D.max_pages, eprefix,
+                        step, rows, D.d, D.H, D.hd, m->scale};
+      PROF_LAUNCH(VLA_PROF_DECODE_ATTN, kv_bytes, launch_attn_decode(da, s));
+      const bool last = l + 1 == D.L;
+      DecodeLayerArgs a{};
+      a.o = SkinnyArgs{o, rows, w.wo, D.d, D.d, m->part_o};
+      a.gu = SkinnyArgs{ua, rows, w.wgu, 2 * D.Fp, D.d, m->part_gu};
+      a.dn = SkinnyArgs{h, rows, w.wd, D.d, D.Fp, m->part_dn};
+      a.nx = last ? SkinnyArgs{ub, rows, m->lm_act, D.Ap, D.d, m->part_nx}
+                  : SkinnyArgs{ub, rows, m->lw[l + 1].wqkv, 3 * D.d, D.d, m->part_nx};
+      a.p_o = m->plan_o; a.p_gu = m->plan_gu; a.p_dn = m->plan_d; a.p_nx = last ? m->plan_head : m->plan_qkv;
+      a.x = x; a.g_mlp = w.mlp_norm; a.g_next = last ? m->final_norm : m->lw[l + 1].attn_norm;
+      a.ua = ua; a.h = h; a.ub = ub;
+      a.M = rows; a.d = D.d; a.Fp = D.Fp; a.eps = eps;
+      a.bar = m->dec_bar; a.bar_base = bar_base; a.flags = m->flags;
+      a.trace = (step == 1 && l == m->trace_layer && r0 == 0) ? m->trace_buf : nullptr;
+      bar_base += kDecodeLayerBarriers;
+      // algorithmic bytes: the four projections' weights (real F) and activations once
+      const double bytes = skinny_bytes(D.d, D.d, rows) + skinny_bytes(2.0 * D.F, D.d, rows) +
+                           skinny_bytes(D.d, D.F, rows) +
+                           (last ? skinny_bytes(D.A, D.d, rows) : skinny_bytes(3.0 * D.d, D.d, rows));
+      PROF_LAUNCH(VLA_PROF_DECODE_LAYER, bytes, launch_decode_layer(a, m->cus, s));
+    }
+    VLA_CK(launch_reduce_sum(m->part_nx, m->plan_head, m->logits_dec + (size_t)r0 * D.A, rows, D.A, s));
+  }
+  return VLA_OK;
+}
+
 // Shared forward over a packed ragged batch: prefill (actions == nullptr) or
 // teacher-forced (each environment's rows extended by its action tokens).
 // save_x (training): per-layer device buffers that receive each layer's input
@@ -310,12 +385,14 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
     rows[b] = prefix[b] + (tf ? D.nact : 0);
     M += rows[b];
   }
-  // host metadata -> pinned staging -> one async upload
-  if (m->meta_pending) {
-    VLA_CK(hipEventSynchronize(m->meta_event));
-    m->meta_pending = false;
+  // host metadata -> pinned staging (the next buffer of the ring) -> one async upload
+  const int ms = m->meta_slot;
+  m->meta_slot = (ms + 1) % kMetaRing;
+  if (m->meta_pending[ms]) {  // this buffer's previous upload: kMetaRing calls ago
+    VLA_CK(hipEventSynchronize(m->meta_event[ms]));
+    m->meta_pending[ms] = false;
   }
-  int32_t* h = m->meta_host;
+  int32_t* h = m->meta_host + (size_t)ms * D.meta_ints;
   int32_t* hp = h + meta_index(m, m->row_pos);
   int32_t* he = h + meta_index(m, m->row_env);
   int32_t* hr0 = h + meta_index(m, m->env_row0);
@@ -347,9 +424,9 @@ int forward(vla_model* m, int B, const void* vis, const int32_t* prompt_ids, con
       hh[b] = hr0[b] + prefix[b] - 1;
     }
   }
-  VLA_CK(hipMemcpyAsync(m->meta_dev, m->meta_host, D.meta_ints * sizeof(int32_t), hipMemcpyHostToDevice, s));
-  VLA_CK(hipEventRecord(m->meta_event, s));
-  m->meta_pending = true;
+  VLA_CK(hipMemcpyAsync(m->meta_dev, h, D.meta_ints * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  VLA_CK(hipEventRecord(m->meta_event[ms], s));
+  m->meta_pending[ms] = true;
 
   const int Mi = (int)M;
   // causal attention flops of one layer: q.k and p.v over (t + 1) keys per row
@@ -726,24 +803,28 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
     m->plan_gu = skinny_plan(2 * D.Fp, D.d, cus, kMaxSplits);
     m->plan_d = skinny_plan(D.d, D.Fp, cus, kMaxSplits);
     m->plan_head = skinny_plan(D.Ap, D.d, cus, kMaxSplits);
+    m->fused_ok = decode_layer_supported();
+    m->decode_path = 0;  // the per-kernel path: measured faster than the persistent layer kernel
   }
   set_meta_views(m, m->meta_dev);
-  m->meta_pending = false;
   m->state_batch = 0;
   m->state_valid = false;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  int n_events = 0;
   auto cleanup = [&](int code) {
+    for (int i = 0; i < n_events; ++i) (void)hipEventDestroy(m->meta_event[i]);
     if (m->meta_host) (void)hipHostFree(m->meta_host);
     delete m;
     return code;
   };
   m->meta_host = nullptr;
-  if (hipHostMalloc(reinterpret_cast<void**>(&m->meta_host), D.meta_ints * sizeof(int32_t), hipHostMallocDefault) !=
-      hipSuccess)
-    return cleanup(fail(VLA_EHIP, "hipHostMalloc of the metadata staging buffer failed"));
-  std::memset(m->meta_host, 0, D.meta_ints * sizeof(int32_t));
-  if (hipEventCreateWithFlags(&m->meta_event, hipEventDisableTiming) != hipSuccess)
-    return cleanup(fail(VLA_EHIP, "hipEventCreate failed"));
+  if (hipHostMalloc(reinterpret_cast<void**>(&m->meta_host), kMetaRing * D.meta_ints * sizeof(int32_t),
+                    hipHostMallocDefault) != hipSuccess)
+    return cleanup(fail(VLA_EHIP, "hipHostMalloc of the metadata staging buffers failed"));
+  std::memset(m->meta_host, 0, kMetaRing * D.meta_ints * sizeof(int32_t));
+  for (; n_events < kMetaRing; ++n_events)
+    if (hipEventCreateWithFlags(&m->meta_event[n_events], hipEventDisableTiming) != hipSuccess)
+      return cleanup(fail(VLA_EHIP, "hipEventCreate failed"));
 
   auto ck = [&](hipError_t e, const char* what) -> int {
     if (e == hipSuccess) return VLA_OK;
@@ -752,10 +833,7 @@ int vla_create(const vla_config* cfg, const vla_weights* w, void* workspace, siz
 #define CREATE_CK(expr)                      \
   do {                                       \
     int r_ = ck((expr), #expr);              \
-    if (r_) {                                \
-      (void)hipEventDestroy(m->meta_event);  \
-      return cleanup(r_);                    \
-    }                                        \
+    if (r_) return cleanup(r_);              \
   } while (0)
 
   const bf16_t* emb = static_cast<const bf16_t*>(w->embed);
@@ -848,9 +926,16 @@ int vla_decode_actions(vla_model* m, int32_t B, const float* gumbel, float T, in
   hipStream_t s = static_cast<hipStream_t>(stream);
   m->state_valid = false;
   const float eps = m->cfg.rms_eps;
+  const bool fused = m->fused_ok && m->decode_path == 1;
+  unsigned bar_base = 0;
+  if (fused) VLA_CK(launch_fill_zero(m->dec_bar, 256 * sizeof(unsigned), s));
   for (int i = 0; i < D.nact; ++i) {
     const float* z = m->logits_pre;
-    if (i > 0) {
+    if (i > 0 && fused) {
+      int rc = decode_step_fused(m, B, i, bar_base, s);
+      if (rc) return rc;
+      z = m->logits_dec;
+    } else if (i > 0) {
       VLA_CK(launch_embed_token_norm(m->next_tok, m->emb, m->x, m->u, m->lw[0].attn_norm, eps, B, D.d, D.V, m->flags,
                                      s));
       // The decode GEMMs take at most kSkinnyRows rows: larger batches run the
@@ -1186,8 +1271,10 @@ void vla_destroy(vla_model* m) {
     (void)hipEventDestroy(p.a);
     (void)hipEventDestroy(p.b);
   }
-  if (m->meta_pending) (void)hipEventSynchronize(m->meta_event);
-  (void)hipEventDestroy(m->meta_event);
+  for (int i = 0; i < kMetaRing; ++i) {
+    if (m->meta_pending[i]) (void)hipEventSynchronize(m->meta_event[i]);
+    (void)hipEventDestroy(m->meta_event[i]);
+  }
   if (m->meta_host) (void)hipHostFree(m->meta_host);
   delete m;
 }
@@ -1197,6 +1284,19 @@ const char* vla_last_error(void) { return g_err.c_str(); }
 int vla_debug_set_layer_limit(vla_model* m, int32_t n_layers) {
   if (!m || n_layers < 0) return fail(VLA_EINVAL, "bad argument");
   m->layer_limit = n_layers;
+  return VLA_OK;
+}
+
+int vla_debug_set_decode_path(vla_model* m, int32_t persistent) {
+  if (!m || persistent < 0 || persistent > 1) return fail(VLA_EINVAL, "bad argument");
+  m->decode_path = persistent;
+  return VLA_OK;
+}
+
+int vla_debug_trace_decode_layer(vla_model* m, int32_t layer, void* stamps) {
+  if (!m || layer < 0 || layer >= m->D.L) return fail(VLA_EINVAL, "bad argument");
+  m->trace_layer = layer;
+  m->trace_buf = static_cast<unsigned long long*>(stamps);
   return VLA_OK;
 }
 

@@ -28,11 +28,12 @@ EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_action
            "vla_train_workspace_size", "vla_ppo_lora_grads")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
 PROJECTIONS = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
-PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn")
+PROF_CATEGORIES = ("prefill_gemm", "prefill_attn", "decode_gemm", "decode_attn", "decode_layer")
 # training modes of vla_ppo_lora_grads (VLA_TRAIN_*): recompute each layer's forward, or keep it
 TRAIN_RECOMPUTE, TRAIN_KEEP = 0, 1
 DEBUG_EXPORTS = ("vla_debug_gemm", "vla_debug_skinny", "vla_debug_pack_frag", "vla_debug_sample", "vla_debug_read",
-                 "vla_debug_set_layer_limit", "vla_debug_set_stop", "vla_debug_skinny_noalloc")
+                 "vla_debug_set_layer_limit", "vla_debug_set_stop", "vla_debug_skinny_noalloc",
+                 "vla_debug_set_decode_path", "vla_debug_trace_decode_layer")
 
 
 class VlaError(RuntimeError):
@@ -102,6 +103,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_debug_read.argtypes = [vp, i32, i32, vp, ctypes.c_size_t, vp]
     lib.vla_debug_set_layer_limit.argtypes = [vp, i32]
     lib.vla_debug_set_stop.argtypes = [vp, i32]
+    lib.vla_debug_set_decode_path.argtypes = [vp, i32]
+    lib.vla_debug_trace_decode_layer.argtypes = [vp, i32, vp]
     for name in EXPORTS + DEBUG_EXPORTS:
         if name not in ("vla_destroy", "vla_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -307,6 +310,14 @@ class VlaModel:
 
     def debug_layer_limit(self, n_layers: int) -> None:
         _check(self.lib.vla_debug_set_layer_limit(self.handle, n_layers))
+
+    def debug_decode_path(self, persistent: int) -> None:
+        """0: one kernel per projection and consumer (default); 1: decode steps on the persistent layer
+        kernel where the device allows (vla_debug.h)."""
+        _check(self.lib.vla_debug_set_decode_path(self.handle, persistent))
+
+    def debug_trace_decode_layer(self, layer: int, stamps: Optional[torch.Tensor]) -> None:
+        _check(self.lib.vla_debug_trace_decode_layer(self.handle, layer, _ptr(stamps)))
 
     def debug_stop(self, stage: int) -> None:
         """Stop point inside the last layer of a layer-limited pass (vla_debug.h)."""
