@@ -631,16 +631,17 @@ int layer_backward(vla_model* m, TrainBufs& t, int l, int B, int M, const vla_lo
     g.A = u1; g.W = w.wqkv; g.M = M; g.N = 3 * d; g.K = d;
     g.q = qb; g.ldq = d; g.kv = m->kv[l]; g.meta = row_meta(m); g.rope = m->rope;
     g.d_model = d; g.n_heads = D.H; g.head_dim = D.hd;
-    VLA_CK(launch_gemm(g, kEpiQkvRope, s));
+    // the recompute of the layer's forward (recompute mode only) is profiled like the forward's launches
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(M, 3.0 * d, d), launch_gemm(g, kEpiQkvRope, s));
     PrefillAttnArgs pa{qb, ob, m->kv[l], m->page_table, D.max_pages, m->env_row0, m->env_len,
                        B, d, D.H, D.hd, m->scale, nullptr, stats};
-    VLA_CK(launch_attn_prefill(pa, s));
+    PROF_LAUNCH(VLA_PROF_PREFILL_ATTN, 0.0, launch_attn_prefill(pa, s));
     VLA_CK(hipMemcpyAsync(xm, xs, (size_t)M * d * sizeof(float), hipMemcpyDeviceToDevice, s));
     GemmArgs go{};
     go.A = ob; go.W = w.wo; go.M = M; go.N = d; go.K = d; go.C = xm; go.ldc = d;
-    VLA_CK(launch_gemm(go, kEpiResidual, s));
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(M, d, d), launch_gemm(go, kEpiResidual, s));
     VLA_CK(launch_rmsnorm(xm, d, nullptr, w.mlp_norm, eps, u2, d, M, d, s, true));
-    VLA_CK(gemm_f32(u2, 0, w.wgu, 0, M, Fg, d, cgu, 2 * Fp, s));
+    PROF_LAUNCH(VLA_PROF_PREFILL_GEMM, gemm_flops(M, 2.0 * D.F, d), gemm_f32(u2, 0, w.wgu, 0, M, Fg, d, cgu, 2 * Fp, s));
   }
   // MLP: dh = dy Wd, SwiGLU backward, du2 = d[g; up] Wgu, RMSNorm backward
   VLA_CK(launch_to_frag(t.dx, d, M, d, d, t.dxf, s));

@@ -192,8 +192,10 @@ def test_keep_and_recompute_modes_give_the_same_bits(cfg):
 
 def test_training_workspace_sizes_select_the_mode():
     """A workspace of the keep size runs the keep mode, one of the recompute size
-    the recompute mode (same bits), and one byte less than that is refused with
-    VLA_EWORKSPACE before any device work."""
+    the recompute mode, observed through the profiled launches (the recompute
+    re-runs each layer's QKV, O and gate/up GEMMs and its attention before the
+    layer's backward), with the same bits; one byte less than the recompute
+    size is refused with VLA_EWORKSPACE before any device work."""
     import ctypes
     cfg = inputs.TINY.replace(name="tiny_ws", batch=2, prompt_min=4, prompt_max=8)
     S = Setup(cfg, seed=9)
@@ -212,10 +214,26 @@ def test_training_workspace_sizes_select_the_mode():
         assert lib.vla_train_workspace_size(ctypes.byref(S.model.c_cfg), mode, ctypes.byref(n)) == 0
         sizes[mode] = n.value
     assert sizes[vla.TRAIN_KEEP] > sizes[vla.TRAIN_RECOMPUTE]
-    st, _, _ = S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, old, adv, 0.2, 1.0, ad, 0.5,
-                                      mode=vla.TRAIN_RECOMPUTE)
-    torch.cuda.synchronize()
-    assert np.isfinite(st.cpu().numpy()).all()
+    runs = {}
+    for mode in (vla.TRAIN_KEEP, vla.TRAIN_RECOMPUTE):
+        S.model.profile_begin(("prefill_gemm", "prefill_attn"))
+        st, lp, gr = S.model.ppo_lora_grads(dev["vis"], dev["ids"], inp.prompt_lens, acts, old, adv, 0.2, 1.0, ad,
+                                            0.5, mode=mode)
+        prof = S.model.profile_end()
+        torch.cuda.synchronize()
+        assert S.model._train_ws.numel() == sizes[mode]
+        runs[mode] = (prof, st.cpu(), lp.cpu(), [{k: (a.cpu(), b.cpu()) for k, (a, b) in l.items()} for l in gr])
+        log(f"[workspace modes] mode {mode}: {prof['prefill_gemm']['launches']} prefill GEMM and "
+            f"{prof['prefill_attn']['launches']} attention launches")
+    keep, rec = runs[vla.TRAIN_KEEP], runs[vla.TRAIN_RECOMPUTE]
+    L = cfg.n_layers
+    assert rec[0]["prefill_gemm"]["launches"] == keep[0]["prefill_gemm"]["launches"] + 3 * L
+    assert rec[0]["prefill_attn"]["launches"] == keep[0]["prefill_attn"]["launches"] + L
+    assert np.isfinite(rec[1].numpy()).all()
+    assert torch.equal(keep[1], rec[1]) and torch.equal(keep[2], rec[2])
+    for a, b in zip(keep[3], rec[3]):
+        for k in a:
+            assert torch.equal(a[k][0], b[k][0]) and torch.equal(a[k][1], b[k][1]), k
     # one byte short of the recompute size: refused on the host
     S.model._train_ws_mode = None
     S.model._train_ws = None
