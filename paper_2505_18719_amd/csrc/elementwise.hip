@@ -193,12 +193,8 @@ __global__ __launch_bounds__(1024) void reduce_residual_norm_kernel(const float*
   for (int t = 0; t < 2; ++t) {  // d <= 8192
     const int c = 4 * (threadIdx.x + 1024 * t);
     if (c >= d) break;
-    float4 a = *reinterpret_cast<const float4*>(x + (size_t)m * d + c);
-    const int ns = skinny_slots(p, c >> 6);
-    for (int sl = 0; sl < ns; ++sl) {
-      const float4 q = *reinterpret_cast<const float4*>(part + ((size_t)sl * M + m) * d + c);
-      a.x += q.x; a.y += q.y; a.z += q.z; a.w += q.w;
-    }
+    const float4 a = sum_slots4(part + (size_t)m * d + c, (size_t)M * d, skinny_slots(p, c >> 6),
+                                *reinterpret_cast<const float4*>(x + (size_t)m * d + c));
     v[t] = a;
     ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
   }
@@ -236,13 +232,9 @@ __global__ __launch_bounds__(256) void reduce_swiglu_kernel(const float* __restr
   const int N = p.tiles * 64;
   const int cg = 64 * (j >> 5) + (j & 31);  // gate columns cg .. cg+3, up columns 32 further (one 64-column tile)
   const int ns = skinny_slots(p, cg >> 6);
-  float4 gs = make_float4(0.f, 0.f, 0.f, 0.f), us = gs;
-  for (int sl = 0; sl < ns; ++sl) {
-    const float* pr = part + ((size_t)sl * M + m) * N + cg;
-    const float4 a = *reinterpret_cast<const float4*>(pr), b = *reinterpret_cast<const float4*>(pr + 32);
-    gs.x += a.x; gs.y += a.y; gs.z += a.z; gs.w += a.w;
-    us.x += b.x; us.y += b.y; us.z += b.z; us.w += b.w;
-  }
+  const float* pr = part + (size_t)m * N + cg;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 gs = sum_slots4(pr, (size_t)M * N, ns, z), us = sum_slots4(pr + 32, (size_t)M * N, ns, z);
   auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
   *reinterpret_cast<uint2*>(h + frag_index(m, j, ldh)) =
       make_uint2(pack2bf(sw(gs.x, us.x), sw(gs.y, us.y)), pack2bf(sw(gs.z, us.z), sw(gs.w, us.w)));

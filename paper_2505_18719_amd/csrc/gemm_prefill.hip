@@ -61,65 +61,22 @@ __device__ __forceinline__ void map_tile(int pid, int G, int tiles_m, int tiles_
 // nothing may be scheduled across this point
 #define PIN() __builtin_amdgcn_sched_barrier(0)
 
-// Epilogues that pair column c of a 64-column group with column c + 32:
-// SwiGLU (gate rows, then the matching up rows) and the QKV projection
-// (rotary pairs).  v1, v2: float4 chunks q and q + 8 of output row `row`,
-// group starting at column c0.
+// SwiGLU epilogue: columns [c0, c0+32) of a 64-column group are gate rows,
+// [c0+32, c0+64) the matching up rows.  v1, v2: float4 chunks q and q + 8 of
+// output row `row`, group starting at column c0.
 template <int EPI>
-__device__ __forceinline__ void pair_epilogue(const GemmArgs& a, int row, int c0, int q, const float4& v1,
-                                              const float4& v2) {
+__device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, int row, int c0, int q, const float4& v1,
+                                                const float4& v2) {
   const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
-  if constexpr (EPI == kEpiSwiGlu || EPI == kEpiSwiGluKeep) {
-    // columns [c0, c0+32) are gate rows, [c0+32, c0+64) the matching up rows
-    float o[4];
+  float o[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
-    *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
-        make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
-    if constexpr (EPI == kEpiSwiGluKeep) {
-      float* cr = a.C + (size_t)row * a.ldc + c0 + 4 * q;
-      *reinterpret_cast<float4*>(cr) = v1;
-      *reinterpret_cast<float4*>(cr + 32) = v2;
-    }
-  } else {  // kEpiQkvRope
-    const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
-    const int region = c0 / d;
-    const int cc0 = c0 - region * d;
-    const int head = cc0 / hd;
-    const int blk = (cc0 % hd) / 64;
-    const int pos = a.meta.row_pos[row];
-    if (region < 2) {
-      // q and k rows were permuted per head so that columns c and c+32 of
-      // this 64-column group are the rotary pair (32*blk + c, half + 32*blk + c)
-      const int ai = 32 * blk + 4 * q;
-      float o1[4], o2[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float2 cs = a.rope[pos * half + ai + t];
-        o1[t] = x1[t] * cs.x - x2[t] * cs.y;
-        o2[t] = x1[t] * cs.y + x2[t] * cs.x;
-      }
-      bf16_t* dst;
-      if (region == 0) {
-        dst = a.q + (size_t)row * a.ldq + head * hd;
-      } else {
-        const int env = a.meta.row_env[row];
-        const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
-        dst = a.kv.k + (((size_t)page * H + head) * kPage + pos % kPage) * hd;
-      }
-      *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
-      *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
-    } else {
-      const int env = a.meta.row_env[row];
-      const int page = a.meta.page_table[env * a.meta.max_pages + pos / kPage];
-      bf16_t* vb = a.kv.v + ((size_t)page * H + head) * hd * kPage + pos % kPage;
-      const int i1 = cc0 % hd + 4 * q;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        vb[(size_t)(i1 + t) * kPage] = f2bf(x1[t]);
-        vb[(size_t)(i1 + t + 32) * kPage] = f2bf(x2[t]);
-      }
-    }
+  for (int t = 0; t < 4; ++t) o[t] = x1[t] / (1.f + expf(-x1[t])) * x2[t];
+  *reinterpret_cast<uint2*>(a.H + frag_index(row, c0 / 2 + 4 * q, a.ldh)) =  // frag layout, K = ldh
+      make_uint2(pack2bf(o[0], o[1]), pack2bf(o[2], o[3]));
+  if constexpr (EPI == kEpiSwiGluKeep) {
+    float* cr = a.C + (size_t)row * a.ldc + c0 + 4 * q;
+    *reinterpret_cast<float4*>(cr) = v1;
+    *reinterpret_cast<float4*>(cr + 32) = v2;
   }
 }
 
@@ -222,9 +179,21 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
           const int cl = jj * 16 + (lane & 15);
           st[rl * 64 + (((cl >> 2) ^ (rl & 15)) << 2) + (cl & 3)] = acc[4 * h + ii][jj][r];
         }
-    __builtin_amdgcn_s_waitcnt(0);
+    // the wave's own staging area: its LDS writes and reads are ordered (no wait for global stores here)
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
     if constexpr (EPI == kEpiStoreF32 || EPI == kEpiResidual) {
       const int q = lane & 15;
+      float4 res[16];
+      if constexpr (EPI == kEpiResidual) {
+        // every residual row of the half is loaded before the first store (independent loads in flight)
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+          const int row = wrow0 + it * 4 + (lane >> 4);
+          const float* src = a.R ? a.R : a.C;
+          if (row < M) res[it] = *reinterpret_cast<const float4*>(src + (size_t)row * a.ldc + c0 + 4 * q);
+        }
+      }
+#pragma unroll
       for (int it = 0; it < 16; ++it) {
         const int rl = it * 4 + (lane >> 4);
         const int row = wrow0 + rl;
@@ -232,10 +201,72 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
         if (row < M) {
           float4* p = reinterpret_cast<float4*>(a.C + (size_t)row * a.ldc + c0 + 4 * q);
           if constexpr (EPI == kEpiResidual) {
-            const float4 o = a.R ? *reinterpret_cast<const float4*>(a.R + (size_t)row * a.ldc + c0 + 4 * q) : *p;
+            const float4 o = res[it];
             *p = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
           } else {
             *p = v;
+          }
+        }
+      }
+    } else if constexpr (EPI == kEpiQkvRope) {
+      // RoPE + q store / paged K, V append for the 8 rows per lane of this half.  The rows'
+      // positions, pages and rotary factors are loaded together first (the loads of one row
+      // depend on each other: position -> page, rotary factors).
+      const int q = lane & 7;
+      const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
+      const int region = c0 / d;  // 0 q, 1 k, 2 v: one region per 64-column group
+      const int cc0 = c0 - region * d;
+      const int head = cc0 / hd;
+      const int blk = (cc0 % hd) / 64;
+      const int ai = 32 * blk + 4 * q;
+      int pos[8], page[8];
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int row = wrow0 + it * 8 + (lane >> 3);
+        pos[it] = row < M ? a.meta.row_pos[row] : 0;
+        page[it] = row < M ? a.meta.row_env[row] : 0;
+      }
+      if (region > 0) {
+#pragma unroll
+        for (int it = 0; it < 8; ++it) page[it] = a.meta.page_table[page[it] * a.meta.max_pages + pos[it] / kPage];
+      }
+      float4 cs[8][2];  // (cos, sin) of rotary pairs ai .. ai + 3 at each row's position
+      if (region < 2) {
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const float4* rp = reinterpret_cast<const float4*>(a.rope + pos[it] * half + ai);
+          cs[it][0] = rp[0];
+          cs[it][1] = rp[1];
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int rl = it * 8 + (lane >> 3);
+        const int row = wrow0 + rl;
+        const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
+        const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
+        if (row >= M) continue;
+        const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
+        if (region < 2) {
+          const float c[4] = {cs[it][0].x, cs[it][0].z, cs[it][1].x, cs[it][1].z};
+          const float sn[4] = {cs[it][0].y, cs[it][0].w, cs[it][1].y, cs[it][1].w};
+          float o1[4], o2[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {  // the rotation, with its fused multiply-adds spelled out
+            o1[t] = fmaf(x1[t], c[t], -(x2[t] * sn[t]));
+            o2[t] = fmaf(x2[t], c[t], x1[t] * sn[t]);
+          }
+          bf16_t* dst = region == 0 ? a.q + (size_t)row * a.ldq + head * hd
+                                    : a.kv.k + (((size_t)page[it] * H + head) * kPage + pos[it] % kPage) * hd;
+          *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
+          *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
+        } else {
+          bf16_t* vb = a.kv.v + ((size_t)page[it] * H + head) * hd * kPage + pos[it] % kPage;
+          const int i1 = cc0 % hd + 4 * q;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            vb[(size_t)(i1 + t) * kPage] = f2bf(x1[t]);
+            vb[(size_t)(i1 + t + 32) * kPage] = f2bf(x2[t]);
           }
         }
       }
@@ -247,10 +278,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
         const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
         const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
         if (row >= M) continue;
-        pair_epilogue<EPI>(a, row, c0, q, v1, v2);
+        swiglu_epilogue<EPI>(a, row, c0, q, v1, v2);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this half's staging reads are done before the next half's writes
   }
 }
 

@@ -89,12 +89,41 @@ __host__ __device__ inline int skinny_slots(const SkinnyPlan& p, int tile) {
   const int U = (p.tiles - p.dp_tiles) * p.chunks, t = tile - p.dp_tiles;
   return skinny_owner((t + 1) * p.chunks - 1, U, p.G) - skinny_owner(t * p.chunks, U, p.G) + 1;
 }
+// Partial slots loaded together before they are summed (more slots: summed one by one after).
+constexpr int kSlotsAhead = 8;
+
+// v + the sum of ns partial slots (slot s at p[s * stride]), added in slot order.
+__device__ inline float sum_slots(const float* __restrict__ p, size_t stride, int ns, float v) {
+  float q[kSlotsAhead];
+#pragma unroll
+  for (int s = 0; s < kSlotsAhead; ++s)
+    if (s < ns) q[s] = p[s * stride];
+#pragma unroll
+  for (int s = 0; s < kSlotsAhead; ++s)
+    if (s < ns) v += q[s];
+  for (int s = kSlotsAhead; s < ns; ++s) v += p[s * stride];
+  return v;
+}
+__device__ inline float4 sum_slots4(const float* __restrict__ p, size_t stride, int ns, float4 v) {
+  float4 q[kSlotsAhead];
+#pragma unroll
+  for (int s = 0; s < kSlotsAhead; ++s)
+    if (s < ns) q[s] = *reinterpret_cast<const float4*>(p + s * stride);
+#pragma unroll
+  for (int s = 0; s < kSlotsAhead; ++s)
+    if (s < ns) {
+      v.x += q[s].x; v.y += q[s].y; v.z += q[s].z; v.w += q[s].w;
+    }
+  for (int s = kSlotsAhead; s < ns; ++s) {
+    const float4 t = *reinterpret_cast<const float4*>(p + s * stride);
+    v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+  }
+  return v;
+}
+
 // Sum of the partial slots of column n of a skinny GEMM (N columns) at row m.
 __device__ inline float skinny_sum(const float* __restrict__ part, const SkinnyPlan& p, int M, int N, int m, int n) {
-  const int ns = skinny_slots(p, n >> 6);
-  float v = 0.f;
-  for (int s = 0; s < ns; ++s) v += part[((size_t)s * M + m) * N + n];
-  return v;
+  return sum_slots(part + (size_t)m * N + n, (size_t)M * N, skinny_slots(p, n >> 6), 0.f);
 }
 // The plan for `workgroups` workgroups, with fewer if needed to keep every tile within `max_slots`.
 SkinnyPlan skinny_plan(int N, int K, int workgroups, int max_slots);
