@@ -29,7 +29,12 @@
 // per flop of the 32x32x16 one and ran ~5 % faster at the same tiling.
 // Workgroup ids are remapped so that the tiles one XCD runs are contiguous in
 // a grouped order (4 tile-rows high), which keeps A and W panels shared in
-// that XCD's L2.
+// that XCD's L2.  The grid is persistent (one workgroup per CU walking its
+// tiles in that order): a finished tile's stores are still draining while the
+// next tile's first copies are issued, where a workgroup that ended would
+// hold its CU until they had drained.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -80,15 +85,19 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, int row, int 
   }
 }
 
+// Tile `pid` of G (in the XCD-aware order of map_tile): main loop and epilogue.
 template <int EPI>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds[NSTAGE][STAGE_U4];
-
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int tiles_n, int pid, int G,
+                                          uint4 (&lds)[NSTAGE][STAGE_U4]) {
   int tm, tn;
-  map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  map_tile(pid, G, tiles_m, tiles_n, tm, tn);
   const int M = a.M, N = a.N, K = a.K;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63;
+  // threadIdx.x through an opaque copy: the per-lane values below are then recomputed for
+  // every tile instead of being hoisted out of the tile loop and kept live through it
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int wm = wave & 1, wn = wave >> 1;  // 128-row half, 64-column quarter of the tile
@@ -285,7 +294,37 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_
   }
 }
 
+// One workgroup per CU walks the tiles pid = blockIdx.x, blockIdx.x + gridDim.x,
+// ... (gridDim.x is a multiple of 8, so a workgroup's tiles stay on its XCD's
+// band).  The next tile's copies are issued as soon as every wave has read its
+// staged outputs, while the previous tile's stores are still draining (a
+// workgroup that ended instead would hold its CU until they had drained).
+template <int EPI>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
+  __shared__ uint4 lds[NSTAGE][STAGE_U4];
+  const int G = tiles_m * tiles_n;
+  for (int pid = blockIdx.x; pid < G; pid += gridDim.x) {
+    gemm_tile<EPI>(a, tiles_m, tiles_n, pid, G, lds);
+    // every wave's staging reads are done (each half ends with lgkmcnt(0)) before the
+    // ring is refilled; a plain barrier, so that no wait covers the stores in flight
+    __builtin_amdgcn_s_barrier();
+  }
+}
+
 }  // namespace
+
+// One workgroup per CU of the current device, rounded down to a multiple of 8 (the XCDs).
+static int persistent_workgroups() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 8;
+  if (!cus[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8) n = 8;
+    cus[dev] = n / 8 * 8;
+  }
+  return cus[dev];
+}
 
 hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
@@ -295,7 +334,7 @@ hipError_t launch_gemm(const GemmArgs& a, GemmEpilogue epi, hipStream_t s) {
       (long long)frag_elems(a.M, ka) * 2 >= (1ll << 31) || (long long)frag_elems(a.N, kw) * 2 >= (1ll << 31))
     return hipErrorInvalidValue;
   const int tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  const dim3 grid(tm * tn), block(NT);
+  const dim3 grid(std::min(tm * tn, persistent_workgroups())), block(NT);
   switch (epi) {
     case kEpiStoreF32: hipLaunchKernelGGL(gemm_bf16_kernel<kEpiStoreF32>, grid, block, 0, s, a, tm, tn); break;
     case kEpiResidual: hipLaunchKernelGGL(gemm_bf16_kernel<kEpiResidual>, grid, block, 0, s, a, tm, tn); break;
