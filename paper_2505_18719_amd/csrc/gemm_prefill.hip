@@ -22,10 +22,10 @@
 // contiguous block: free of bank conflicts without a swizzle.
 //
 // Why these choices: the kernel runs at the chip's power limit (the shader
-// clock measured inside it is 1.2-1.6 GHz with all CUs busy), so what counts
-// is issue efficiency per clock and energy per flop.  The two-waves-per-SIMD
-// ping-pong keeps the MFMA pipe fed (measured ~93 % of MFMA cycles in the main
-// loop); the 16x16x32 instruction moves half the accumulator register traffic
+// clock measured inside it is 1.2-1.75 GHz with all CUs busy, depending on the
+// board), so what counts is issue efficiency per clock and energy per flop.
+// The two-waves-per-SIMD ping-pong keeps the MFMA pipe fed (measured 93-96 % of
+// MFMA cycles in the main loop); the 16x16x32 instruction moves half the accumulator register traffic
 // per flop of the 32x32x16 one and ran ~5 % faster at the same tiling.
 // Workgroup ids are remapped so that the tiles one XCD runs are contiguous in
 // a grouped order (4 tile-rows high), which keeps A and W panels shared in
