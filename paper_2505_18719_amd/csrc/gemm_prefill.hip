@@ -32,7 +32,12 @@
 // that XCD's L2.  The grid is persistent (one workgroup per CU walking its
 // tiles in that order): a finished tile's stores are still draining while the
 // next tile's first copies are issued, where a workgroup that ended would
-// hold its CU until they had drained.
+// hold its CU until they had drained.  With the SwiGLU epilogue the tile
+// boundary overlaps further: the last four iterations copy the next tile's
+// first four K steps (instead of re-copying the last one), the epilogue works
+// out of the one stage those copies leave free, and since vmcnt retires in
+// issue order, the next tile's first three waits count past the epilogue's
+// stores (a fixed number per wave), which drain while its first steps run.
 #include <algorithm>
 
 #include "common.h"
@@ -85,10 +90,23 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, int row, int 
   }
 }
 
+// Epilogues that run while the next tile's first AHEAD K steps are being copied
+// (they stage through one 32 KB ring stage only), and the number of vector
+// memory instructions each of their waves issues (a constant, so that the next
+// tile's first waits can count past them).
+template <int EPI>
+constexpr bool overlaps_next() { return EPI == kEpiSwiGlu; }
+template <int EPI>
+constexpr int epi_vm_ops() { return EPI == kEpiSwiGlu ? 8 : 0; }
+
 // Tile `pid` of G (in the XCD-aware order of map_tile): main loop and epilogue.
+// ring0: the ring stage of this tile's K step 0.  pending: -1 when no copy of
+// this tile is in flight yet; otherwise the previous tile's last iterations
+// copied this tile's first AHEAD steps (step 0 has landed) and `pending` is the
+// number of vector memory instructions its epilogue issued after them.
 template <int EPI>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int tiles_n, int pid, int G,
-                                          uint4 (&lds)[NSTAGE][STAGE_U4]) {
+                                          uint4 (&lds)[NSTAGE][STAGE_U4], int& ring0, int& pending) {
   int tm, tn;
   map_tile(pid, G, tiles_m, tiles_n, tm, tn);
   const int M = a.M, N = a.N, K = a.K;
@@ -112,10 +130,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int ti
   const int rb0 = copies_a ? (m0 >> 4) : (n0 >> 4), rb_last = copies_a ? last_rb_a : last_rb_w;
   const uint32_t voff = lane * 16;
   const uint32_t lds_base = (uint32_t)(uintptr_t)((lds_ptr_t*)&lds[0][0]);
-  auto copy = [&](int j, int st, int ks) {
+  auto copy = [&](int j, int st, int rb, int ks) {
     const int b = wave * 4 + j;
-    lds_dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb0 + (b & 15), rb_last) * KB + ks) * 1024);
+    lds_dma16(lds_base + (st * STAGE_U4 + b * 64) * 16, voff, rsC, (min(rb + (b & 15), rb_last) * KB + ks) * 1024);
   };
+  const int nk = K / BK;
+  // the last AHEAD iterations copy the next tile's first steps instead of re-copying the last one
+  const bool ov = overlaps_next<EPI>() && nk > AHEAD;
+  const int npid = pid + (int)gridDim.x;
+  const bool has_next = ov && npid < G;
+  int rb0n = rb0;
+  if (has_next) {
+    int tmn, tnn;
+    map_tile(npid, G, tiles_m, tiles_n, tmn, tnn);
+    rb0n = copies_a ? (tmn * BM) >> 4 : (tnn * BN) >> 4;
+  }
 
   f32x4 acc[8][4];
 #pragma unroll
@@ -130,28 +159,37 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int ti
   const uint4* ring = &lds[0][0];
   bf16x8 fa_r[8], fw_r[4];
 
-  const int nk = K / BK;
+  if (pending < 0) {
 #pragma unroll
-  for (int st = 0; st < AHEAD; ++st)
+    for (int st = 0; st < AHEAD; ++st)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) copy(j, st, min(st, nk - 1));
-  WAIT_VMCNT(4 * (AHEAD - 1));
+      for (int j = 0; j < 4; ++j) copy(j, (ring0 + st) % NSTAGE, rb0, min(st, nk - 1));
+    WAIT_VMCNT(4 * (AHEAD - 1));
+  }
   __builtin_amdgcn_s_barrier();
   if (grp) __builtin_amdgcn_s_barrier();
   PIN();
-  int cur = 0, fill = AHEAD;
-  for (int kt = 0; kt < nk; ++kt) {
+  int cur = ring0, fill = (ring0 + AHEAD) % NSTAGE;
+  // One K step.  `wide`: the previous epilogue's epi_vm_ops instructions were issued
+  // after this tile's first AHEAD steps' copies, so until step AHEAD's wait they sit
+  // between the copies waited for and the newer ones (vmcnt retires in issue order).
+  auto k_step = [&](int kt, bool wide) {
     // ---- memory phase: operand fragments of step kt, copies of step kt + AHEAD
     const uint4* sp = ring + cur * STAGE_U4;
 #pragma unroll
     for (int i = 0; i < 8; ++i) fa_r[i] = as_bf16x8(sp[fa + i * 64]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) fw_r[j] = as_bf16x8(sp[fw + j * 64]);
-    const int kfill = min(kt + AHEAD, nk - 1);  // past the end the last step is re-copied
+    // past the end: the next tile's first steps, or (no next tile) the last step again
+    const int kk = kt + AHEAD;
+    const bool past = kk >= nk;
+    const int rbf = past && has_next ? rb0n : rb0;
+    const int kfill = !past ? kk : (has_next ? kk - nk : nk - 1);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) copy(j, fill, kfill);
+    for (int j = 0; j < 4; ++j) copy(j, fill, rbf, kfill);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments in registers, this stage's reads done
-    WAIT_VMCNT(4 * (AHEAD - 1));      // this wave's copies of step kt + 1 have landed
+    if (wide) WAIT_VMCNT(4 * (AHEAD - 1) + epi_vm_ops<EPI>());  // this wave's copies of step kt + 1 have landed
+    else WAIT_VMCNT(4 * (AHEAD - 1));
     PIN();
     __builtin_amdgcn_s_barrier();
     PIN();
@@ -165,16 +203,65 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int ti
     PIN();
     cur = cur + 1 == NSTAGE ? 0 : cur + 1;
     fill = fill + 1 == NSTAGE ? 0 : fill + 1;
-  }
+  };
+  int kt = 0;
+  if (overlaps_next<EPI>() && pending > 0)
+    for (; kt < AHEAD - 1; ++kt) k_step(kt, true);
+  for (; kt < nk; ++kt) k_step(kt, false);
   if (!grp) __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  if (ov) {
+    // the next tile's copies stay in flight; this tile's own copies have all landed
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+  } else {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  const int stage_out = (ring0 + nk - 1) % NSTAGE;  // the last step's stage: free for staging
+  if (ov) ring0 = (ring0 + nk) % NSTAGE;
+  pending = has_next ? 0 : -1;
 
   // ---------------------------------------------------------------- epilogue
   // acc[i][j][r] holds row 16 i + 4 (lane / 16) + r, column 16 j + lane % 16 of the wave tile
-  float* st = reinterpret_cast<float*>(&lds[0][0]) + wave * (64 * 64);
   const int c0 = n0 + wn * 64;
   if (c0 >= N) return;
+  if constexpr (EPI == kEpiSwiGlu) {
+    // h = silu(gate) * up straight from the accumulators: the wave's 64 columns are
+    // 32 gate columns (j = 0, 1) and the matching up columns (j = 2, 3), so h of row
+    // 16 i + 4 (lane / 16) + r, feature 16 j + lane % 16 (j < 2) is in this lane.  Each
+    // 16-row block i of the wave's 32 features is one 1 KB frag block of H: it is
+    // transposed through 1 KB of the free stage and stored whole (16 bytes per lane).
+    // Stores of blocks past the last row block are dropped by the buffer's bound.
+    bf16_t* stg = reinterpret_cast<bf16_t*>(&lds[stage_out][0]) + wave * 2048;  // 4 KB per wave
+    const __amdgpu_buffer_rsrc_t rsH = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.H, (short)0, (int)(frag_elems(M, a.ldh) * 2), 0x00020000);
+    const int kbh = frag_kb(a.ldh), fblk = c0 >> 6;
+#pragma unroll
+    for (int rnd = 0; rnd < 2; ++rnd) {
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float x1 = acc[4 * rnd + ii][j][r], x2 = acc[4 * rnd + ii][j + 2][r];
+            const int rho = 4 * (lane >> 4) + r, f = 16 * j + (lane & 15);
+            stg[ii * 512 + (rho + 16 * (f >> 3)) * 8 + (f & 7)] = f2bf(x1 / (1.f + expf(-x1)) * x2);
+          }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const uint4 v = reinterpret_cast<const uint4*>(stg)[ii * 64 + lane];
+        const int rb = (m0 + wm * 128 + 16 * (4 * rnd + ii)) >> 4;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rsH,
+                                               (uint32_t)(((rb * kbh + fblk) * 64 + lane) * 16), 0, 0);
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // this round's reads are done before the next round's writes
+    }
+    if (has_next) pending = epi_vm_ops<EPI>();
+    return;
+  }
+  float* st = reinterpret_cast<float*>(&lds[0][0]) + wave * (64 * 64);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int wrow0 = m0 + wm * 128 + h * 64;
@@ -303,8 +390,9 @@ template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a, int tiles_m, int tiles_n) {
   __shared__ uint4 lds[NSTAGE][STAGE_U4];
   const int G = tiles_m * tiles_n;
+  int ring0 = 0, pending = -1;
   for (int pid = blockIdx.x; pid < G; pid += gridDim.x) {
-    gemm_tile<EPI>(a, tiles_m, tiles_n, pid, G, lds);
+    gemm_tile<EPI>(a, tiles_m, tiles_n, pid, G, lds, ring0, pending);
     // every wave's staging reads are done (each half ends with lgkmcnt(0)) before the
     // ring is refilled; a plain barrier, so that no wait covers the stores in flight
     __builtin_amdgcn_s_barrier();
