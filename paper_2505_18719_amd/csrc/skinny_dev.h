@@ -164,39 +164,64 @@ __device__ __forceinline__ void run(const Sched& sc, const SkinnyArgs& a, const 
     zero();
   };
 
-  // unit i: MFMAs on ring slot i % D, after issuing the loads of unit i + D - 1
-  auto step = [&](int i, uint4 (&w)[4][2], uint4 (&x)[MB][2], uint4 (&wn)[4][2], uint4 (&xn)[MB][2]) {
-    load_w<MB>(sc, a, i + D - 1, wave, wn);  // unconditional, so the wait counts are the same on every path
-    load_x<MB>(sc, a, i + D - 1, wave, xn);
-    SKINNY_PIN();
-    if (i < total) {
+  // The loads of unit i + D - 1 go out before the MFMAs of unit i (ring slot i % D); they are unconditional,
+  // so that the wait counts are the same on every path, and each unit's activations go out before its weights.
+  const int KB = frag_kb(a.K);
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
+  const uint32_t loff = lane * 16;
+  auto ldw = [&](int i, uint4 (&wv)[4][2]) {
+    int chunk;
+    const int tile = sc.unit_tile(min(i, total - 1), chunk);
+    const int kb = 8 * chunk + 2 * wave;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma16(as_bf16x8(x[mb][h]), as_bf16x8(w[nb][h]), acc[mb][nb]);
-      int c0, c1;
-      const int t0 = sc.unit_tile(i, c0);
-      if (i + 1 >= total || sc.unit_tile(i + 1, c1) != t0) flush(t0);
-    }
-    SKINNY_PIN();
+        wv[nb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsW, loff, ((tile * 4 + nb) * KB + kb + h) * 1024, 0));
   };
-
+  auto ldx = [&](int i, uint4 (&xv)[MB][2]) {
+    int chunk;
+    (void)sc.unit_tile(min(i, total - 1), chunk);
+    const int kb = 8 * chunk + 2 * wave;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        xv[mb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, loff, (mb * KB + kb + h) * 1024, 0));
+  };
   if (!prefetched) {
 #pragma unroll
     for (int j = 0; j < D - 1; ++j) {
-      load_w<MB>(sc, a, j, wave, r.w[j]);
-      load_x<MB>(sc, a, j, wave, r.x[j]);
+      ldx(j, r.x[j]);
+      ldw(j, r.w[j]);
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j) load_x<MB>(sc, a, j, wave, r.x[j]);
+    for (int j = 0; j < D - 1; ++j) ldx(j, r.x[j]);
   }
-  for (int i = 0; i < total; i += D) {
-    // ring slots rotate statically: unit i + j uses slot j, its loads go to slot (j + D - 1) % D
+  for (int i0 = 0; i0 < total; i0 += D) {
+    // ring slots rotate statically: unit i0 + j uses slot j, its loads go to slot (j + D - 1) % D
 #pragma unroll
-    for (int j = 0; j < D; ++j) step(i + j, r.w[j], r.x[j], r.w[(j + D - 1) % D], r.x[(j + D - 1) % D]);
+    for (int j = 0; j < D; ++j) {
+      const int i = i0 + j;
+      ldx(i + D - 1, r.x[(j + D - 1) % D]);
+      ldw(i + D - 1, r.w[(j + D - 1) % D]);
+      SKINNY_PIN();
+      if (i < total) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+              acc[mb][nb] = mfma16(as_bf16x8(r.x[j][mb][h]), as_bf16x8(r.w[j][nb][h]), acc[mb][nb]);
+        int c0, c1;
+        const int t0 = sc.unit_tile(i, c0);
+        if (i + 1 >= total || sc.unit_tile(i + 1, c1) != t0) flush(t0);
+      }
+      SKINNY_PIN();
+    }
   }
 }
 
