@@ -378,51 +378,68 @@ hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* 
   return hipGetLastError();
 }
 
-// LoRA merge, one 256-thread workgroup per 64 destination rows x 64 K
-// columns.  The update B A of the tile is a 64 x 64 x rank product on MFMA:
-// wave w takes destination rows 16 w .. 16 w + 15, its A operand the 16 B rows
-// of their source rows (contiguous 16-byte reads), its B operand the adapter's
-// A factor staged transposed in LDS; the fp32 update is staged in LDS and each
-// thread then adds two 8-element chunks of it to the original weights, rounds
-// to bf16 and writes them in frag layout.
+// LoRA merge, one 256-thread workgroup per 64 rows x 64 K columns.  Rows are
+// the projection's own rows in packed order: for the interleaved [gate; up]
+// weight only the 32-row halves of `part`, so no workgroup computes rows it
+// does not write.  The update B A of the tile is a 64 x 64 x rank product on
+// MFMA: wave w takes rows 16 w .. 16 w + 15, its A operand the 16 B rows of
+// their source rows (contiguous 16-byte reads), its B operand the adapter's A
+// factor staged transposed in LDS.  The original weights are loaded first;
+// each wave stages its fp32 update in its own LDS rows (no workgroup barrier
+// after the staging of A), adds two 8-element chunks per lane to the original
+// weights, rounds to bf16 and writes them in frag layout.  (Measured: wider
+// tiles that reuse the staged A over 128 or 256 columns are slower, 7.7 and
+// 12.1 ms against 6.9 ms for every projection of the 7B shape at rank 32:
+// fewer workgroups fit on a CU to cover the loads' latency.)
+constexpr int kMergeCols = 64;
+
 __global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t at[64][72];  // A^T: [column][rank], padded rows
-  __shared__ float dw[64][68];                                // scale-free update B A of the tile
-  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  __shared__ __attribute__((aligned(16))) bf16_t at[kMergeCols][72];  // A^T: [column][rank], padded rows
+  __shared__ float dws[4][16][68];                                     // per wave: the block's update of its rows
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c0 = blockIdx.y * kMergeCols;
+  const int nblk = min(kMergeCols, a.K - c0) / 64;  // K % 64 == 0
   const int RK = (a.rank + 31) / 32 * 32;
-  // this thread's two 8-column chunks of the tile: the original weights are
-  // loaded first, so that their latency overlaps the update's computation
-  int crow[2], ccol[2], csrc[2];
-  bool cwrite[2];
-  uint4 w0v[2];
+  const bool gu = a.mode == kPackGateUp;
+  const int nrows = gu ? a.rows / 2 : a.rows;  // rows of this projection
+  // packed row of the projection's row l
+  auto prow = [&](int l) { return gu ? 64 * (l >> 5) + 32 * a.part + (l & 31) : l; };
+  // this lane's two 8-column chunks of each block: row 16 wave + e / 8, columns 8 (e % 8), e = lane + 64 t
+  int crow[2], csrc[2];
+  bool cin[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    const int e = tid + 256 * t;
-    crow[t] = r0 + e / 8;
-    ccol[t] = c0 + 8 * (e % 8);
+    const int l = blockIdx.x * 64 + 16 * wave + (lane + 64 * t) / 8;
+    cin[t] = l < nrows;
+    crow[t] = prow(l);
     int pt;
-    csrc[t] = crow[t] < a.rows ? pack_src_row(a.mode, crow[t], a.head_dim, a.src_rows, pt) : -1;
-    // rows past the matrix and the other projection's rows of [gate; up] are not written
-    cwrite[t] = crow[t] < a.rows && (a.mode != kPackGateUp || pt == a.part);
-    w0v[t] = make_uint4(0, 0, 0, 0);  // zero rows and columns of the packed layout
-    if (cwrite[t] && csrc[t] >= 0 && ccol[t] < a.src_cols)  // src_cols % 8 == 0: a chunk is wholly in or out
-      w0v[t] = *reinterpret_cast<const uint4*>(a.w0 + (size_t)csrc[t] * a.src_ld + ccol[t]);
+    csrc[t] = cin[t] ? pack_src_row(a.mode, crow[t], a.head_dim, a.src_rows, pt) : -1;
   }
-  // this lane's A-operand row (destination row r0 + 16 wave + lane % 16) of B, both rank halves
+  uint4 w0v[kMergeCols / 64][2];
+#pragma unroll
+  for (int cb = 0; cb < kMergeCols / 64; ++cb)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int col = c0 + 64 * cb + 8 * ((lane + 64 * t) % 8);
+      w0v[cb][t] = make_uint4(0, 0, 0, 0);  // zero rows and columns of the packed layout
+      if (cb < nblk && csrc[t] >= 0 && col < a.src_cols)  // src_cols % 8 == 0: a chunk is wholly in or out
+        w0v[cb][t] = *reinterpret_cast<const uint4*>(a.w0 + (size_t)csrc[t] * a.src_ld + col);
+    }
+  // this lane's A-operand row (row 16 wave + lane % 16) of B, both rank halves
+  const int lb = blockIdx.x * 64 + 16 * wave + (lane & 15);
   int part;
-  const int j = pack_src_row(a.mode, r0 + 16 * wave + (lane & 15), a.head_dim, a.src_rows, part);
+  const int j = lb < nrows ? pack_src_row(a.mode, prow(lb), a.head_dim, a.src_rows, part) : -1;
   uint4 bv[2];
 #pragma unroll
   for (int kc = 0; kc < 2; ++kc) {
     const int k = 32 * kc + 8 * (lane >> 4);
     bv[kc] = make_uint4(0, 0, 0, 0);
-    if (kc < RK / 32 && j >= 0 && r0 + 16 * wave + (lane & 15) < a.rows && k < a.rank)
-      bv[kc] = *reinterpret_cast<const uint4*>(a.b + (size_t)j * a.rank + k);
+    if (kc < RK / 32 && j >= 0 && k < a.rank) bv[kc] = *reinterpret_cast<const uint4*>(a.b + (size_t)j * a.rank + k);
   }
-  // A^T, zero past the rank and past the source columns: 8 columns of one rank row per 16-byte load
-  for (int e = tid; e < RK * 8; e += 256) {
-    const int kr = e / 8, c = 8 * (e % 8);
+  // A^T of the tile's columns, zero past the rank and past the source columns: 8 columns of one rank row per
+  // 16-byte load
+  for (int e = tid; e < RK * (kMergeCols / 8); e += 256) {
+    const int kr = e / (kMergeCols / 8), c = 8 * (e % (kMergeCols / 8));
     uint4 v = make_uint4(0, 0, 0, 0);
     if (kr < a.rank && c0 + c < a.src_cols) v = *reinterpret_cast<const uint4*>(a.a + (size_t)kr * a.src_cols + c0 + c);
     const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
@@ -430,48 +447,56 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
     for (int x = 0; x < 8; ++x) at[c + x][kr] = (bf16_t)(vv[x >> 1] >> (16 * (x & 1)));
   }
   __syncthreads();
-  f32x4 acc[4];
+  float(*dw)[68] = dws[wave];
 #pragma unroll
-  for (int jb = 0; jb < 4; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int cb = 0; cb < kMergeCols / 64; ++cb) {
+    if (cb >= nblk) break;
+    f32x4 acc[4];
 #pragma unroll
-  for (int kc = 0; kc < 2; ++kc) {
-    if (kc < RK / 32) {
-      const int k = 32 * kc + 8 * (lane >> 4);
+    for (int jb = 0; jb < 4; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        const uint4 av = *reinterpret_cast<const uint4*>(&at[16 * jb + (lane & 15)][k]);
-        acc[jb] = mfma16(as_bf16x8(bv[kc]), as_bf16x8(av), acc[jb]);
+    for (int kc = 0; kc < 2; ++kc) {
+      if (kc < RK / 32) {
+        const int k = 32 * kc + 8 * (lane >> 4);
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+          const uint4 av = *reinterpret_cast<const uint4*>(&at[64 * cb + 16 * jb + (lane & 15)][k]);
+          acc[jb] = mfma16(as_bf16x8(bv[kc]), as_bf16x8(av), acc[jb]);
+        }
       }
     }
-  }
-  // acc[jb][r]: update of row 16 wave + 4 (lane / 16) + r, column 16 jb + lane % 16
+    // acc[jb][r]: update of row 16 wave + 4 (lane / 16) + r, column 64 cb + 16 jb + lane % 16
 #pragma unroll
-  for (int jb = 0; jb < 4; ++jb)
+    for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) dw[16 * wave + 4 * (lane >> 4) + r][16 * jb + (lane & 15)] = acc[jb][r];
-  __syncthreads();
-  // add the scaled update to the original weights, round to bf16, write in frag layout
+      for (int r = 0; r < 4; ++r) dw[4 * (lane >> 4) + r][16 * jb + (lane & 15)] = acc[jb][r];
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the wave's own staging rows are written
+    // add the scaled update to the original weights, round to bf16, write in frag layout
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    if (!cwrite[t]) continue;
-    const int rr = crow[t] - r0, cc = ccol[t] - c0;
-    float w[8];
-    unpack8(w0v[t], w);
-    if (csrc[t] >= 0 && ccol[t] < a.src_cols) {
+    for (int t = 0; t < 2; ++t) {
+      if (!cin[t]) continue;
+      const int e = lane + 64 * t, rr = e / 8, cc = 8 * (e % 8), col = c0 + 64 * cb + cc;
+      float w[8];
+      unpack8(w0v[cb][t], w);
+      if (csrc[t] >= 0 && col < a.src_cols) {
 #pragma unroll
-      for (int x = 0; x < 8; ++x) w[x] += a.scale * dw[rr][cc + x];
+        for (int x = 0; x < 8; ++x) w[x] += a.scale * dw[rr][cc + x];
+      }
+      *reinterpret_cast<uint4*>(a.dst + frag_index(crow[t], col, a.K)) =
+          make_uint4(pack2bf(w[0], w[1]), pack2bf(w[2], w[3]), pack2bf(w[4], w[5]), pack2bf(w[6], w[7]));
     }
-    *reinterpret_cast<uint4*>(a.dst + frag_index(crow[t], ccol[t], a.K)) =
-        make_uint4(pack2bf(w[0], w[1]), pack2bf(w[2], w[3]), pack2bf(w[4], w[5]), pack2bf(w[6], w[7]));
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // this block's staging reads are done before the next block's writes
   }
 }
 
 hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   if (a.K % 64 != 0 || a.rank < 8 || a.rank > 64 || a.rank % 8 != 0 || a.src_ld % 8 != 0 || a.src_cols % 8 != 0 ||
-      (a.mode == kPackGateUp && (a.part < 0 || a.part > 1)))
+      (a.mode == kPackGateUp && (a.part < 0 || a.part > 1 || a.rows % 64 != 0)))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(lora_merge_kernel, dim3((a.rows + 63) / 64, a.K / 64), dim3(256), 0, s, a);
+  const int nrows = a.mode == kPackGateUp ? a.rows / 2 : a.rows;
+  hipLaunchKernelGGL(lora_merge_kernel, dim3((nrows + 63) / 64, (a.K + kMergeCols - 1) / kMergeCols), dim3(256), 0, s,
+                     a);
   return hipGetLastError();
 }
 

@@ -282,7 +282,7 @@ hipError_t launch_pack_frag(const PackArgs& a, hipStream_t s);
 // places them for `mode`): destination row r of source row j gets
 // bf16(w0[j, :] + scale * (b[j, :] a)) with a [rank, src_cols], b [src_rows, rank]
 // row-major bf16 and the rank sum accumulated in fp32.  For kPackGateUp only
-// the rows of `part` (0 gate, 1 up) are written.  Requires K % 64 == 0,
+// the rows of `part` (0 gate, 1 up) are computed and written (rows % 64 == 0).  Requires K % 64 == 0,
 // rank % 8 == 0, 8 <= rank <= 64, src_ld and src_cols multiples of 8.
 struct MergeArgs {
   bf16_t* dst;
