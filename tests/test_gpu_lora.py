@@ -170,6 +170,26 @@ def test_lora_merge_packed_weights_match_oracle(tiny, rank):
     _merge_all(S, [{k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}], SCALE, [1])
 
 
+@pytest.mark.parametrize("key", ["wgate", "wup"])
+def test_lora_merge_of_one_mlp_part_leaves_the_other_rows(tiny, key):
+    """The packed [gate; up] weight interleaves the two projections in 32-row
+    halves; merging one of them computes and writes only its own rows (checked
+    against the oracle), the other part's rows keep their bits, and a zero
+    update restores the whole buffer."""
+    S, cfg = tiny, inputs.TINY
+    before = _read_packed(S.model, cfg, 7, 0).clone()
+    a, b = inputs.make_lora(cfg, 16, seed=11, device="cuda", layers=[0])[0][key]
+    S.model.lora_merge(0, key, S.w["layers"][0][key], a, b, SCALE)
+    buf = _read_packed(S.model, cfg, 7, 0)
+    R, K = _packed_shape(cfg, 7)
+    mine = [r for r in range(R) if _packed_source(cfg, 7, r)[0] == key]
+    other = [r for r in range(R) if _packed_source(cfg, 7, r)[0] != key]
+    _check_packed(cfg, buf, 7, mine, S.wc["layers"][0], {key: (a.cpu(), b.cpu())}, SCALE, f"tiny {key} alone")
+    assert np.array_equal(_frag_gather(buf, other, K), _frag_gather(before, other, K)), "the other part's rows changed"
+    S.model.lora_merge(0, key, S.w["layers"][0][key], a, torch.zeros_like(b), SCALE)
+    _assert_same_packed(cfg, 7, _read_packed(S.model, cfg, 7, 0), before, "a zero update must restore the packing")
+
+
 def test_lora_merge_starts_from_the_original_and_a_zero_update_restores(tiny):
     S, cfg = tiny, inputs.TINY
     packed0 = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}
