@@ -305,58 +305,88 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int tiles_m, int ti
         }
       }
     } else if constexpr (EPI == kEpiQkvRope) {
-      // RoPE + q store / paged K, V append for the 8 rows per lane of this half.  The rows'
-      // positions, pages and rotary factors are loaded together first (the loads of one row
-      // depend on each other: position -> page, rotary factors).
-      const int q = lane & 7;
+      // RoPE + q store / paged K, V append for this half's 64 rows.  The rows' positions, pages
+      // and rotary factors are loaded together first (the loads of one row depend on each other:
+      // position -> page, rotary factors).
       const int d = a.d_model, hd = a.head_dim, H = a.n_heads, half = hd / 2;
       const int region = c0 / d;  // 0 q, 1 k, 2 v: one region per 64-column group
       const int cc0 = c0 - region * d;
       const int head = cc0 / hd;
       const int blk = (cc0 % hd) / 64;
-      const int ai = 32 * blk + 4 * q;
-      int pos[8], page[8];
-#pragma unroll
-      for (int it = 0; it < 8; ++it) {
-        const int row = wrow0 + it * 8 + (lane >> 3);
-        pos[it] = row < M ? a.meta.row_pos[row] : 0;
-        page[it] = row < M ? a.meta.row_env[row] : 0;
-      }
-      if (region > 0) {
-#pragma unroll
-        for (int it = 0; it < 8; ++it) page[it] = a.meta.page_table[page[it] * a.meta.max_pages + pos[it] / kPage];
-      }
-      float4 cs[8][2];  // (cos, sin) of rotary pairs ai .. ai + 3 at each row's position
       if (region < 2) {
+        // q, k: the group's columns are 32 first-half features and their rotary partners; lane
+        // takes 8 consecutive ones (octet q8) and their partners for 4 rows (16 rows a pass), so
+        // every store is 16 bytes
+        const int q8 = lane & 3;
+        const int ai = 32 * blk + 8 * q8;
+        int pos[4], page[4];
 #pragma unroll
-        for (int it = 0; it < 8; ++it) {
-          const float4* rp = reinterpret_cast<const float4*>(a.rope + pos[it] * half + ai);
-          cs[it][0] = rp[0];
-          cs[it][1] = rp[1];
+        for (int it = 0; it < 4; ++it) {
+          const int row = wrow0 + it * 16 + (lane >> 2);
+          pos[it] = row < M ? a.meta.row_pos[row] : 0;
+          page[it] = row < M ? a.meta.row_env[row] : 0;
         }
-      }
+        if (region == 1) {
 #pragma unroll
-      for (int it = 0; it < 8; ++it) {
-        const int rl = it * 8 + (lane >> 3);
-        const int row = wrow0 + rl;
-        const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
-        const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
-        if (row >= M) continue;
-        const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
-        if (region < 2) {
-          const float c[4] = {cs[it][0].x, cs[it][0].z, cs[it][1].x, cs[it][1].z};
-          const float sn[4] = {cs[it][0].y, cs[it][0].w, cs[it][1].y, cs[it][1].w};
-          float o1[4], o2[4];
+          for (int it = 0; it < 4; ++it) page[it] = a.meta.page_table[page[it] * a.meta.max_pages + pos[it] / kPage];
+        }
+        float4 cs[4][4];  // (cos, sin) of rotary pairs ai .. ai + 7 at each row's position
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {  // the rotation, with its fused multiply-adds spelled out
-            o1[t] = fmaf(x1[t], c[t], -(x2[t] * sn[t]));
-            o2[t] = fmaf(x2[t], c[t], x1[t] * sn[t]);
+        for (int it = 0; it < 4; ++it) {
+          const float4* rp = reinterpret_cast<const float4*>(a.rope + pos[it] * half + ai);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) cs[it][u] = rp[u];
+        }
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+          const int rl = it * 16 + (lane >> 2);
+          const int row = wrow0 + rl;
+          float x1[8], x2[8];
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2) {
+            const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + (((2 * q8 + h2) ^ (rl & 15)) << 2));
+            const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((8 + 2 * q8 + h2) ^ (rl & 15)) << 2));
+            x1[4 * h2] = v1.x; x1[4 * h2 + 1] = v1.y; x1[4 * h2 + 2] = v1.z; x1[4 * h2 + 3] = v1.w;
+            x2[4 * h2] = v2.x; x2[4 * h2 + 1] = v2.y; x2[4 * h2 + 2] = v2.z; x2[4 * h2 + 3] = v2.w;
+          }
+          if (row >= M) continue;
+          float o1[8], o2[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {  // the rotation, with its fused multiply-adds spelled out
+            const float c = (t & 1) ? cs[it][t >> 1].z : cs[it][t >> 1].x;
+            const float sn = (t & 1) ? cs[it][t >> 1].w : cs[it][t >> 1].y;
+            o1[t] = fmaf(x1[t], c, -(x2[t] * sn));
+            o2[t] = fmaf(x2[t], c, x1[t] * sn);
           }
           bf16_t* dst = region == 0 ? a.q + (size_t)row * a.ldq + head * hd
                                     : a.kv.k + (((size_t)page[it] * H + head) * kPage + pos[it] % kPage) * hd;
-          *reinterpret_cast<uint2*>(dst + ai) = make_uint2(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]));
-          *reinterpret_cast<uint2*>(dst + half + ai) = make_uint2(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]));
-        } else {
+          *reinterpret_cast<uint4*>(dst + ai) =
+              make_uint4(pack2bf(o1[0], o1[1]), pack2bf(o1[2], o1[3]), pack2bf(o1[4], o1[5]), pack2bf(o1[6], o1[7]));
+          *reinterpret_cast<uint4*>(dst + half + ai) =
+              make_uint4(pack2bf(o2[0], o2[1]), pack2bf(o2[2], o2[3]), pack2bf(o2[4], o2[5]), pack2bf(o2[6], o2[7]));
+        }
+      } else {
+        // v: 8 rows per lane, 4 features and the 4 of the group's second half; the cache keeps V
+        // transposed (16 keys of one feature per 32 bytes), and the 8 lanes that share a feature
+        // hold 8 consecutive rows, so their 2-byte stores fill 16-byte pieces
+        const int q = lane & 7;
+        int pos[8], page[8];
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int row = wrow0 + it * 8 + (lane >> 3);
+          pos[it] = row < M ? a.meta.row_pos[row] : 0;
+          page[it] = row < M ? a.meta.row_env[row] : 0;
+        }
+#pragma unroll
+        for (int it = 0; it < 8; ++it) page[it] = a.meta.page_table[page[it] * a.meta.max_pages + pos[it] / kPage];
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int rl = it * 8 + (lane >> 3);
+          const int row = wrow0 + rl;
+          const float4 v1 = *reinterpret_cast<const float4*>(st + rl * 64 + ((q ^ (rl & 15)) << 2));
+          const float4 v2 = *reinterpret_cast<const float4*>(st + rl * 64 + (((q + 8) ^ (rl & 15)) << 2));
+          if (row >= M) continue;
+          const float x1[4] = {v1.x, v1.y, v1.z, v1.w}, x2[4] = {v2.x, v2.y, v2.z, v2.w};
           bf16_t* vb = a.kv.v + ((size_t)page[it] * H + head) * hd * kPage + pos[it] % kPage;
           const int i1 = cc0 % hd + 4 * q;
 #pragma unroll
