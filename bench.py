@@ -519,10 +519,9 @@ def main():
         # rank 32, from the original checkpoint; timed after the rollout figures
         rank = 32
         adapters = I.make_lora(cfg, rank, seed=0, device=dev)
-        def merge_all():
+        def merge_all():  # every projection of a layer in one launch (vla_lora_merge_layer)
             for li, ad in enumerate(adapters):
-                for key, (a, b) in ad.items():
-                    model.lora_merge(li, key, w["layers"][li][key], a, b, 0.5)
+                model.lora_merge_layer(li, w["layers"][li], ad, 0.5)
         merge_all()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -538,7 +537,7 @@ def main():
                                  + 4 * d * d + 2 * Fp * d + d * Fp    # packed (gate/up rows and down columns padded to Fp)
                                  + rank * (4 * d + 2 * d + F)         # A factors [rank, in]
                                  + rank * (4 * d + 2 * F + d))        # B factors [out, rank]
-        result["lora_merge"] = {"ms": merge_ms, "rank": rank, "projections": 7 * L,
+        result["lora_merge"] = {"ms": merge_ms, "rank": rank, "projections": 7 * L, "launches": L,
                                 "achieved": merge_bytes / (merge_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
                                 "unit": "GB/s", "frac": merge_bytes / (merge_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
                                 "bytes": merge_bytes}

@@ -206,6 +206,15 @@ int vla_value(vla_model* m, int32_t batch, const void* vis_emb, const int32_t* p
 int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
                    const void* lora_b, int32_t rank, float scale, void* stream);
 
+/* Every projection of one layer in one launch: vla_lora_merge for each
+ * projection p (VLA_PROJ_* order, arrays of 7 device pointers held in host
+ * memory) whose w0[p] is not NULL, the others left as they are; the merged
+ * weights are the bits the seven separate calls give.  Same argument rules
+ * and errors as vla_lora_merge (checked for every merged projection before
+ * anything is launched); rank and scale are shared by the layer's adapters. */
+int vla_lora_merge_layer(vla_model* m, int32_t layer, const void* const* w0, const void* const* lora_a,
+                         const void* const* lora_b, int32_t rank, float scale, void* stream);
+
 /* Teacher-forced pass (numerator of the PPO ratio, Eq. 2): one causal forward
  * over [visual ; prompt ; the n_actions given action tokens] per environment,
  * with no KV reuse, scoring token i by the logits at row L_b - 1 + i.

@@ -393,15 +393,19 @@ hipError_t launch_reduce_swiglu(const float* part, const SkinnyPlan& p, bf16_t* 
 // fewer workgroups fit on a CU to cover the loads' latency.)
 constexpr int kMergeCols = 64;
 
-__global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
+// Rows of the projection a merge computes (for [gate; up], the part's half of the packed rows).
+__host__ __device__ inline int merge_rows(const MergeArgs& a) { return a.mode == kPackGateUp ? a.rows / 2 : a.rows; }
+
+// Tile (rows 64 rb .., columns kMergeCols cb ..) of one merge.
+__device__ __forceinline__ void merge_tile(const MergeArgs& a, int rb, int cb) {
   __shared__ __attribute__((aligned(16))) bf16_t at[kMergeCols][72];  // A^T: [column][rank], padded rows
   __shared__ float dws[4][16][68];                                     // per wave: the block's update of its rows
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int c0 = blockIdx.y * kMergeCols;
+  const int c0 = cb * kMergeCols;
   const int nblk = min(kMergeCols, a.K - c0) / 64;  // K % 64 == 0
   const int RK = (a.rank + 31) / 32 * 32;
   const bool gu = a.mode == kPackGateUp;
-  const int nrows = gu ? a.rows / 2 : a.rows;  // rows of this projection
+  const int nrows = merge_rows(a);
   // packed row of the projection's row l
   auto prow = [&](int l) { return gu ? 64 * (l >> 5) + 32 * a.part + (l & 31) : l; };
   // this lane's two 8-column chunks of each block: row 16 wave + e / 8, columns 8 (e % 8), e = lane + 64 t
@@ -409,7 +413,7 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
   bool cin[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    const int l = blockIdx.x * 64 + 16 * wave + (lane + 64 * t) / 8;
+    const int l = rb * 64 + 16 * wave + (lane + 64 * t) / 8;
     cin[t] = l < nrows;
     crow[t] = prow(l);
     int pt;
@@ -426,7 +430,7 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
         w0v[cb][t] = *reinterpret_cast<const uint4*>(a.w0 + (size_t)csrc[t] * a.src_ld + col);
     }
   // this lane's A-operand row (row 16 wave + lane % 16) of B, both rank halves
-  const int lb = blockIdx.x * 64 + 16 * wave + (lane & 15);
+  const int lb = rb * 64 + 16 * wave + (lane & 15);
   int part;
   const int j = lb < nrows ? pack_src_row(a.mode, prow(lb), a.head_dim, a.src_rows, part) : -1;
   uint4 bv[2];
@@ -489,15 +493,40 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(MergeArgs a) {
   }
 }
 
+// One workgroup per tile of each item, the items' tiles one after the other (row blocks fastest).
+__global__ __launch_bounds__(256) void lora_merge_kernel(MergeBatch b) {
+  int i = 0;
+  while (i + 1 < b.n && (int)blockIdx.x >= b.wg0[i + 1]) ++i;
+  const MergeArgs& a = b.item[i];
+  const int local = (int)blockIdx.x - b.wg0[i], nrb = (merge_rows(a) + 63) / 64;
+  merge_tile(a, local % nrb, local / nrb);
+}
+
+static bool merge_ok(const MergeArgs& a) {
+  return a.K % 64 == 0 && a.rank >= 8 && a.rank <= 64 && a.rank % 8 == 0 && a.src_ld % 8 == 0 && a.src_cols % 8 == 0 &&
+         (a.mode != kPackGateUp || (a.part >= 0 && a.part <= 1 && a.rows % 64 == 0));
+}
+
+hipError_t launch_lora_merge_batch(MergeBatch b, hipStream_t s) {
+  if (b.n < 1 || b.n > kMergeBatchMax) return hipErrorInvalidValue;
+  int wg = 0;
+  for (int i = 0; i < b.n; ++i) {
+    if (b.item[i].rows < 0 || !merge_ok(b.item[i])) return hipErrorInvalidValue;
+    b.wg0[i] = wg;
+    wg += (merge_rows(b.item[i]) + 63) / 64 * ((b.item[i].K + kMergeCols - 1) / kMergeCols);
+  }
+  b.wg0[b.n] = wg;
+  if (wg == 0) return hipSuccess;
+  hipLaunchKernelGGL(lora_merge_kernel, dim3(wg), dim3(256), 0, s, b);
+  return hipGetLastError();
+}
+
 hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
-  if (a.K % 64 != 0 || a.rank < 8 || a.rank > 64 || a.rank % 8 != 0 || a.src_ld % 8 != 0 || a.src_cols % 8 != 0 ||
-      (a.mode == kPackGateUp && (a.part < 0 || a.part > 1 || a.rows % 64 != 0)))
-    return hipErrorInvalidValue;
-  const int nrows = a.mode == kPackGateUp ? a.rows / 2 : a.rows;
-  hipLaunchKernelGGL(lora_merge_kernel, dim3((nrows + 63) / 64, (a.K + kMergeCols - 1) / kMergeCols), dim3(256), 0, s,
-                     a);
-  return hipGetLastError();
+  MergeBatch b{};
+  b.item[0] = a;
+  b.n = 1;
+  return launch_lora_merge_batch(b, s);
 }
 
 // One wave per row: 16-byte chunks of 8 consecutive K elements (contiguous in

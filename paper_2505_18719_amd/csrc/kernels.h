@@ -296,6 +296,15 @@ struct MergeArgs {
   float scale;
 };
 hipError_t launch_lora_merge(const MergeArgs& a, hipStream_t s);
+// Up to seven merges (e.g. every projection of one layer) in one launch; each
+// item as launch_lora_merge requires it, item results as if merged one by one.
+constexpr int kMergeBatchMax = 7;
+struct MergeBatch {
+  MergeArgs item[kMergeBatchMax];
+  int wg0[kMergeBatchMax + 1];  // first workgroup of each item; wg0[n] = the launch's workgroups
+  int n;
+};
+hipError_t launch_lora_merge_batch(MergeBatch b, hipStream_t s);
 // Value head: values[r] = sum_k u[r, k] * head[k] for R rows of u (bf16,
 // frag layout with K = d) and head bf16 [d]; fp32, fixed summation order.
 hipError_t launch_value_head(const bf16_t* u, int R, int d, const bf16_t* head, float* values, hipStream_t s);

@@ -1031,9 +1031,9 @@ int vla_value(vla_model* m, int32_t B, const void* vis, const int32_t* ids, cons
   return VLA_OK;
 }
 
-int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
-                   const void* lora_b, int32_t rank, float scale, void* stream) {
-  if (!m) return fail(VLA_EINVAL, "model is NULL");
+// The merge of one projection of one layer: its packed destination and row mode.
+static int merge_args(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
+                      const void* lora_b, int32_t rank, float scale, MergeArgs* out) {
   if (!w0 || !lora_a || !lora_b) return fail(VLA_EINVAL, "NULL argument");
   const Dims& D = m->D;
   if (layer < 0 || layer >= D.L) return fail(VLA_EINVAL, "layer out of range");
@@ -1068,7 +1068,33 @@ int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* 
       break;
   }
   if (a.src_cols % 8 != 0) return fail(VLA_EUNSUPPORTED, "input features must be a multiple of 8");
+  *out = a;
+  return VLA_OK;
+}
+
+int vla_lora_merge(vla_model* m, int32_t layer, int32_t projection, const void* w0, const void* lora_a,
+                   const void* lora_b, int32_t rank, float scale, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  MergeArgs a;
+  const int rc = merge_args(m, layer, projection, w0, lora_a, lora_b, rank, scale, &a);
+  if (rc) return rc;
   VLA_CK(launch_lora_merge(a, static_cast<hipStream_t>(stream)));
+  g_err.clear();
+  return VLA_OK;
+}
+
+int vla_lora_merge_layer(vla_model* m, int32_t layer, const void* const* w0, const void* const* lora_a,
+                         const void* const* lora_b, int32_t rank, float scale, void* stream) {
+  if (!m) return fail(VLA_EINVAL, "model is NULL");
+  if (!w0 || !lora_a || !lora_b) return fail(VLA_EINVAL, "NULL array");
+  MergeBatch b{};
+  for (int32_t p = VLA_PROJ_Q; p <= VLA_PROJ_DOWN; ++p) {
+    if (!w0[p]) continue;  // this projection is not merged
+    const int rc = merge_args(m, layer, p, w0[p], lora_a[p], lora_b[p], rank, scale, &b.item[b.n]);
+    if (rc) return rc;
+    ++b.n;
+  }
+  if (b.n > 0) VLA_CK(launch_lora_merge_batch(b, static_cast<hipStream_t>(stream)));
   g_err.clear();
   return VLA_OK;
 }

@@ -23,7 +23,7 @@ FLAG_BAD_PROMPT_ID = 1
 FLAG_BAD_ACTION = 2
 
 EXPORTS = ("vla_workspace_size", "vla_create", "vla_prefill", "vla_decode_actions", "vla_token_logprobs",
-           "vla_value", "vla_lora_merge", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
+           "vla_value", "vla_lora_merge", "vla_lora_merge_layer", "vla_read_device_flags", "vla_profile_begin", "vla_profile_end", "vla_destroy",
            "vla_last_error", "vla_extract_actions", "vla_gae", "vla_ppo_clip", "vla_logprob_backward",
            "vla_train_workspace_size", "vla_ppo_lora_grads")
 # projections a LoRA adapter merges into (VLA_PROJ_* order), by weight-dict key
@@ -81,6 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vla_decode_actions.argtypes = [vp, i32, vp, f32, vp, vp, vp, vp, vp]
     lib.vla_token_logprobs.argtypes = [vp, i32, vp, vp, vp, vp, f32, vp, vp, vp, vp]
     lib.vla_lora_merge.argtypes = [vp, i32, i32, vp, vp, vp, i32, f32, vp]
+    lib.vla_lora_merge_layer.argtypes = [vp, i32, vp, vp, vp, i32, f32, vp]
     lib.vla_value.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp]
     lib.vla_read_device_flags.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_uint32)]
     lib.vla_extract_actions.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, vp]
@@ -235,6 +236,25 @@ class VlaModel:
             assert t.dtype == torch.bfloat16 and t.is_contiguous() and t.is_cuda
         _check(self.lib.vla_lora_merge(self.handle, layer, PROJECTIONS.index(projection), _ptr(w0), _ptr(lora_a),
                                        _ptr(lora_b), rank, float(scale), _stream(self.device)))
+
+    def lora_merge_layer(self, layer: int, w0: Dict[str, torch.Tensor], adapters: Dict[str, tuple],
+                         scale: float) -> None:
+        """lora_merge of every projection of `layer` that `adapters` ({key: (lora_a, lora_b)}, one shared
+        rank) holds, in one launch; w0 holds the original checkpoint weights by key."""
+        n = len(PROJECTIONS)
+        ws, As, Bs = (ctypes.c_void_p * n)(), (ctypes.c_void_p * n)(), (ctypes.c_void_p * n)()
+        ranks = set()
+        for i, key in enumerate(PROJECTIONS):
+            if key not in adapters:
+                continue
+            a, b = adapters[key]
+            for t in (w0[key], a, b):
+                assert t.dtype == torch.bfloat16 and t.is_contiguous() and t.is_cuda
+            ws[i], As[i], Bs[i] = _ptr(w0[key]), _ptr(a), _ptr(b)
+            ranks.add(int(a.shape[0]))
+        assert len(ranks) <= 1, "the adapters of one call share their rank"
+        rank = ranks.pop() if ranks else 8
+        _check(self.lib.vla_lora_merge_layer(self.handle, layer, ws, As, Bs, rank, float(scale), _stream(self.device)))
 
     def ppo_lora_grads(self, vis: torch.Tensor, prompt_ids: torch.Tensor, prompt_lens: np.ndarray,
                        actions: torch.Tensor, logp_old: torch.Tensor, advantages: torch.Tensor, eps: float,

@@ -190,6 +190,31 @@ def test_lora_merge_of_one_mlp_part_leaves_the_other_rows(tiny, key):
     _assert_same_packed(cfg, 7, _read_packed(S.model, cfg, 7, 0), before, "a zero update must restore the packing")
 
 
+def test_lora_merge_layer_gives_the_bits_of_the_separate_merges(tiny):
+    """vla_lora_merge_layer (every projection of a layer in one launch) leaves
+    the packed weights of the seven separate vla_lora_merge calls, bit for
+    bit; a projection without an adapter in the call keeps its bits."""
+    S, cfg = tiny, inputs.TINY
+    before = {w: _read_packed(S.model, cfg, w, 1).clone() for w in (5, 6, 7, 8)}
+    ad = inputs.make_lora(cfg, 24, seed=13, device="cuda", layers=[1])
+    _merge_all(S, ad, SCALE, [1])
+    sep = {w: _read_packed(S.model, cfg, w, 1).clone() for w in (5, 6, 7, 8)}
+    zero = {k: (a, torch.zeros_like(b)) for k, (a, b) in ad[0].items()}
+    _merge_all(S, [zero], SCALE, [1])
+    S.model.lora_merge_layer(1, S.w["layers"][1], ad[0], SCALE)
+    for w in (5, 6, 7, 8):
+        _assert_same_packed(cfg, w, _read_packed(S.model, cfg, w, 1), sep[w], "one launch per layer")
+    # without 'wo' and 'wup' in the call: o keeps the merged bits of the previous call, and
+    # after restoring the rest, [gate; up] holds the original up rows and o its merged rows
+    S.model.lora_merge_layer(1, S.w["layers"][1], {k: v for k, v in zero.items() if k not in ("wo", "wup")}, SCALE)
+    _assert_same_packed(cfg, 6, _read_packed(S.model, cfg, 6, 1), sep[6], "o not in the call")
+    _assert_same_packed(cfg, 5, _read_packed(S.model, cfg, 5, 1), before[5], "q, k, v restored")
+    _assert_same_packed(cfg, 8, _read_packed(S.model, cfg, 8, 1), before[8], "down restored")
+    S.model.lora_merge_layer(1, S.w["layers"][1], zero, SCALE)
+    for w in (5, 6, 7, 8):
+        _assert_same_packed(cfg, w, _read_packed(S.model, cfg, w, 1), before[w], "a zero update restores the layer")
+
+
 def test_lora_merge_starts_from_the_original_and_a_zero_update_restores(tiny):
     S, cfg = tiny, inputs.TINY
     packed0 = {w: _read_packed(S.model, cfg, w, 0).clone() for w in (5, 6, 7, 8)}

@@ -81,6 +81,9 @@ def test_lora_merge_validates_arguments_before_the_device(vla):
     p = ctypes.c_void_p(16)  # never dereferenced: validation fails first
     assert lib.vla_lora_merge(None, 0, 0, p, p, p, 8, 1.0, None) == -1
     assert b"model is NULL" in lib.vla_last_error()
+    arr = (ctypes.c_void_p * 7)(*([p] * 7))
+    assert lib.vla_lora_merge_layer(None, 0, arr, arr, arr, 8, 1.0, None) == -1
+    assert b"model is NULL" in lib.vla_last_error()
 
 
 def test_learning_entry_points_validate_on_the_host(vla):
