@@ -27,9 +27,17 @@ constexpr int UNIT_K = 256;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
-// Ring depth (units in flight) by the number of 16-row blocks of A.
+// Ring depths (units in flight) of the weights and of the activations by the
+// number of 16-row blocks of A.  At 8 blocks a unit's activations are twice its
+// weights, and their ring would not fit the registers beside the accumulators:
+// they are loaded in the step that uses them (an L2 hit), while the weights run
+// one unit ahead (measured: the 128-row launches 6 % faster than with both
+// rings two deep).
 template <int MB>
 constexpr int ring_depth() { return MB <= 4 ? 3 : 2; }
+template <int MB>
+constexpr int x_ring_depth() { return MB <= 4 ? 3 : 1; }
+constexpr int gcd_(int a, int b) { return b == 0 ? a : gcd_(b, a % b); }
 
 // LDS bytes of the cross-wave reduction.
 template <int MB>
@@ -38,7 +46,7 @@ constexpr size_t red_bytes() { return (size_t)NW * MB * 16 * COLS * sizeof(float
 template <int MB>
 struct Ring {
   uint4 w[ring_depth<MB>()][4][2];
-  uint4 x[ring_depth<MB>()][MB][2];
+  uint4 x[x_ring_depth<MB>()][MB][2];
 };
 
 // The units of workgroup g under plan p: whole tiles first, then its stream-K run.
@@ -117,7 +125,8 @@ __device__ __forceinline__ void prefetch_w(const Sched& sc, const SkinnyArgs& a,
 template <int MB, bool SC1>
 __device__ __forceinline__ void run(const Sched& sc, const SkinnyArgs& a, const SkinnyPlan& p, Ring<MB>& r,
                                     float* red, bool prefetched) {
-  constexpr int D = ring_depth<MB>();
+  constexpr int D = ring_depth<MB>(), DX = x_ring_depth<MB>();
+  constexpr int P = D * DX / gcd_(D, DX);  // the rings' common period
   constexpr int ROWS = MB * 16;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: keeps load offsets scalar
@@ -164,8 +173,6 @@ __device__ __forceinline__ void run(const Sched& sc, const SkinnyArgs& a, const 
     zero();
   };
 
-  // The loads of unit i + D - 1 go out before the MFMAs of unit i (ring slot i % D); they are unconditional,
-  // so that the wait counts are the same on every path, and each unit's activations go out before its weights.
   const int KB = frag_kb(a.K);
   const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc((void*)a.W, (short)0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)a.A, (short)0, 0x7fffffff, 0x00020000);
@@ -190,22 +197,26 @@ __device__ __forceinline__ void run(const Sched& sc, const SkinnyArgs& a, const 
       for (int h = 0; h < 2; ++h)
         xv[mb][h] = as_uint4(__builtin_amdgcn_raw_buffer_load_b128(rsA, loff, (mb * KB + kb + h) * 1024, 0));
   };
+  // The weight loads of unit i + D - 1 and the activation loads of unit i + DX - 1 go out before the MFMAs
+  // of unit i (ring slots i % D, i % DX); they are unconditional, so that the wait counts are the same on every
+  // path, and the activations go out first, so that the wait for a unit's activations does not also wait for
+  // later weights.
   if (!prefetched) {
 #pragma unroll
     for (int j = 0; j < D - 1; ++j) {
-      ldx(j, r.x[j]);
+      if (j < DX - 1) ldx(j, r.x[j]);
       ldw(j, r.w[j]);
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j) ldx(j, r.x[j]);
+    for (int j = 0; j < DX - 1; ++j) ldx(j, r.x[j]);
   }
-  for (int i0 = 0; i0 < total; i0 += D) {
-    // ring slots rotate statically: unit i0 + j uses slot j, its loads go to slot (j + D - 1) % D
+  for (int i0 = 0; i0 < total; i0 += P) {
+    // ring slots rotate statically: unit i0 + j uses slots j % D and j % DX
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
+    for (int j = 0; j < P; ++j) {
       const int i = i0 + j;
-      ldx(i + D - 1, r.x[(j + D - 1) % D]);
+      ldx(i + DX - 1, r.x[(j + DX - 1) % DX]);
       ldw(i + D - 1, r.w[(j + D - 1) % D]);
       SKINNY_PIN();
       if (i < total) {
@@ -215,7 +226,7 @@ __device__ __forceinline__ void run(const Sched& sc, const SkinnyArgs& a, const 
           for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb)
-              acc[mb][nb] = mfma16(as_bf16x8(r.x[j][mb][h]), as_bf16x8(r.w[j][nb][h]), acc[mb][nb]);
+              acc[mb][nb] = mfma16(as_bf16x8(r.x[j % DX][mb][h]), as_bf16x8(r.w[j % D][nb][h]), acc[mb][nb]);
         int c0, c1;
         const int t0 = sc.unit_tile(i, c0);
         if (i + 1 >= total || sc.unit_tile(i + 1, c1) != t0) flush(t0);
