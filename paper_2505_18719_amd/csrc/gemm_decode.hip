@@ -16,9 +16,10 @@
 //    v_mfma_f32_16x16x32_bf16 k-steps.  Weights and activations are both in
 //    frag layout, so every load instruction reads one contiguous 1 KB block
 //    that leaves each lane holding its MFMA fragment (the number of memory
-//    requests per byte is what bounds this kernel).  Loads run a ring of units
-//    ahead of the MFMAs (about 96 KB of weights in flight per CU), pinned in
-//    issue order.
+//    requests per byte is what bounds this kernel).  The next unit's weights
+//    are in flight while a unit's MFMAs run (32 KB per CU; deeper rings only
+//    queued more loads), its activations are loaded in the step that uses
+//    them, pinned in issue order.
 //  - The activations (<= 128 x K bf16) are read through L2, where every
 //    workgroup of an XCD shares them.  Per unit a wave loads 8 weight blocks
 //    and 2 MB activation blocks (MB = 16-row blocks of A), so at 64 rows the

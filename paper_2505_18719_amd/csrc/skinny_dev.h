@@ -27,16 +27,18 @@ constexpr int UNIT_K = 256;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 as_uint4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
 
-// Ring depths (units in flight) of the weights and of the activations by the
-// number of 16-row blocks of A.  At 8 blocks a unit's activations are twice its
-// weights, and their ring would not fit the registers beside the accumulators:
-// they are loaded in the step that uses them (an L2 hit), while the weights run
-// one unit ahead (measured: the 128-row launches 6 % faster than with both
-// rings two deep).
+// Ring depths (units in flight) of the weights and of the activations.  The
+// weights of the next unit are in flight while a unit's MFMAs run; a unit's
+// activations (shared by an XCD's workgroups, so L2 hits) are loaded in the
+// step that uses them.  Measured at 8 to 128 rows on the four projection
+// shapes: deeper rings (2-5 units ahead, with the activations as deep as the
+// weights) were 2-13 % slower per launch, since the extra loads only queue
+// and the registers they take leave the accumulators shuffled between the two
+// register files; at 8 row blocks the deeper rings also spilled.
 template <int MB>
-constexpr int ring_depth() { return MB <= 4 ? 3 : 2; }
+constexpr int ring_depth() { return 2; }
 template <int MB>
-constexpr int x_ring_depth() { return MB <= 4 ? 3 : 1; }
+constexpr int x_ring_depth() { return 1; }
 constexpr int gcd_(int a, int b) { return b == 0 ? a : gcd_(b, a % b); }
 
 // LDS bytes of the cross-wave reduction.
