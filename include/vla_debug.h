@@ -6,6 +6,7 @@
 #ifndef VLA_DEBUG_H_
 #define VLA_DEBUG_H_
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus

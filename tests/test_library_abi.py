@@ -31,6 +31,24 @@ def _declared_functions():
     return sorted(names)
 
 
+@pytest.mark.parametrize("header", ["vla.h", "vla_learn.h", "vla_debug.h"])
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_each_header_compiles_on_its_own(header, lang, tmp_path):
+    """A C-ABI header includes what it uses: it compiles alone, as C99 and as
+    C++, with warnings as errors (only the host compiler is needed)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    src = tmp_path / ("h.c" if lang == "c" else "h.cpp")
+    src.write_text(f'#include "{header}"\nint main(void) {{ return 0; }}\n')
+    std = ["-std=c99", "-pedantic"] if lang == "c" else ["-std=c++17"]
+    r = subprocess.run([cc, *std, "-Wall", "-Wextra", "-Werror", "-fsyntax-only", "-I", os.path.join(ROOT, "include"),
+                        str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
 def test_headers_declare_the_rollout_entry_points():
     names = _declared_functions()
     for n in ("vla_prefill", "vla_decode_actions", "vla_token_logprobs", "vla_create", "vla_workspace_size",
